@@ -1,0 +1,272 @@
+#!/usr/bin/env python3
+"""Throughput of the E2S-Pruner scoring path (score + fuse + select) on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload llava] [--mode mean_logit]
+
+One step is one e2s_prune call over the whole batch: the score kernel, the
+fused evidence kernel and the selection kernel, with Q and K already resident
+in HBM.  Prints ONE JSON line with images/s, a roofline object for the
+dominant (score) kernel and the CPU oracle's throughput on a bounded sample.
+
+Other modes (used by the profiling commands kept with the results):
+    --kernel-only   run only the timed e2s_prune steps (no CPU baseline)
+    --copy-calibrate N_MIB   time a plain device copy of N MiB (counter calibration)
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "images pruned/sec (score+fuse+select) at LLaVA shape; % MFMA / % HBM peak"
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_mean_logit_llava_traffic.txt")
+SCORE_SOURCES = ("score.hip", "score_prob.hip", "e2s_device.h")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="llava")
+    ap.add_argument("--mode", default="mean_logit", choices=["mean_logit", "mean_prob"])
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum CPU time spent timing the oracle")
+    ap.add_argument("--kernel-only", action="store_true")
+    ap.add_argument("--copy-calibrate", type=int, default=0, metavar="N_MIB")
+    return ap.parse_args()
+
+
+def source_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for name in SCORE_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_23253_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(mode: str):
+    """HBM bytes per score launch from the committed counter summary, or None when
+    it is missing or was taken on a different version of the score kernel."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                key, val = line.split(":", 1)
+                vals[key.strip()] = val.strip()
+    if vals.get("score_source_sha256_16") != source_digest() or vals.get("mode") != mode:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibrate(mib: int):
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, device="cuda", dtype=torch.float32)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(10):
+        dst.copy_(src)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / 10
+    moved = 2 * n * 4
+    print(json.dumps({"copy_mib": mib, "bytes_read": n * 4, "bytes_written": n * 4,
+                      "ms": ms, "GBps": moved / ms / 1e6}))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the path is data-parallel over images and needs no collective; see the "
+              "design notes for how it would shard)", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibrate:
+        copy_calibrate(args.copy_calibrate)
+        return
+
+    import numpy as np
+    import torch
+
+    import synth
+    import paper_2608_23253_amd as E
+    from paper_2608_23253_amd import _lib as L
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    cfg = synth.config_by_name(args.workload)
+    B, N = cfg.batch, cfg.num_visual
+    t0 = time.time()
+    q_np, k_np, _ = synth.gen_batch(cfg)
+    log(f"[bench] generated {cfg.name} batch {B} in {time.time() - t0:.1f}s")
+
+    def upload(x):
+        if cfg.dtype == "bf16":
+            bits = synth.to_bf16_bits(x).view(np.int16)
+            return torch.from_numpy(bits).cuda().view(torch.bfloat16)
+        return torch.from_numpy(x).cuda()
+
+    qd, kd = upload(q_np), upload(k_np)
+    torch.cuda.synchronize()
+    log(f"[bench] uploaded Q {tuple(qd.shape)} K {tuple(kd.shape)} {qd.dtype}")
+
+    pr = E.Pruner(qd, kd, cfg.grid_h, cfg.grid_w, cfg.keep, cfg.cells, cfg.lam, args.mode)
+    stream = torch.cuda.current_stream()
+
+    # ---- region A: the metric -------------------------------------------------
+    for _ in range(args.warmup):
+        pr(qd, kd)
+    torch.cuda.synchronize()
+    t_a = time.perf_counter()
+    for _ in range(args.steps):
+        pr(qd, kd)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_a
+    ms_step = wall * 1e3 / args.steps
+    value = B / (wall / args.steps)
+    log(f"[bench] e2s_prune: {ms_step:.4f} ms/step, {value:.1f} images/s")
+    if args.kernel_only:
+        print(json.dumps({"ms_per_step": ms_step, "value": value}))
+        return
+
+    # ---- region B: per-kernel durations (the same three kernels, staged) ------
+    lib = L.lib()
+    sh = pr.shape
+    pa = L.make_params(pr.params.dtype, args.mode, 0.0, cfg.cells, cfg.lam, cfg.keep)
+    e_buf = torch.empty((B, cfg.num_layers, cfg.num_heads, N), device="cuda", dtype=torch.float32)
+    c_buf = torch.empty((B, N), device="cuda", dtype=torch.float32)
+    keep_buf = torch.empty((B, cfg.keep), device="cuda", dtype=torch.int32)
+    st = stream.cuda_stream
+    shp, pap = ctypes.byref(sh), ctypes.byref(pa)
+    n_ev = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n_ev)]
+    for _ in range(args.warmup):
+        lib.e2s_score_heads(shp, pap, qd.data_ptr(), kd.data_ptr(), e_buf.data_ptr(), None, st)
+        lib.e2s_fuse_evidence(shp, e_buf.data_ptr(), None, None, c_buf.data_ptr(), st)
+        lib.e2s_spatial_select(shp, pap, c_buf.data_ptr(), keep_buf.data_ptr(), None, None, st)
+    torch.cuda.synchronize()
+    for i in range(n_ev):
+        ev[i][0].record(stream)
+        rc = lib.e2s_score_heads(shp, pap, qd.data_ptr(), kd.data_ptr(), e_buf.data_ptr(), None, st)
+        ev[i][1].record(stream)
+        rc |= lib.e2s_fuse_evidence(shp, e_buf.data_ptr(), None, None, c_buf.data_ptr(), st)
+        ev[i][2].record(stream)
+        rc |= lib.e2s_spatial_select(shp, pap, c_buf.data_ptr(), keep_buf.data_ptr(), None, None,
+                                     st)
+        ev[i][3].record(stream)
+        if rc:
+            raise RuntimeError(f"staged call failed with status {rc}")
+    torch.cuda.synchronize()
+    t_score = np.array([ev[i][0].elapsed_time(ev[i][1]) for i in range(n_ev)])
+    t_fuse = np.array([ev[i][1].elapsed_time(ev[i][2]) for i in range(n_ev)])
+    t_sel = np.array([ev[i][2].elapsed_time(ev[i][3]) for i in range(n_ev)])
+    assert torch.equal(keep_buf, pr.keep_idx), "staged and fused paths disagree"
+
+    per_img_qk = cfg.bytes_per_image()
+    per_img_e = 4 * cfg.num_layers * cfg.num_heads * N
+    algo_bytes = B * (per_img_qk + per_img_e)
+    score_ms = float(t_score.mean())
+    achieved = algo_bytes / (score_ms * 1e-3) / 1e9
+    traffic = read_traffic(args.mode)
+    flops_eq1 = 2.0 * B * cfg.num_layers * cfg.num_heads * cfg.num_text * N * cfg.head_dim
+    log(f"[bench] score {score_ms * 1e3:.1f} us (p10 {np.percentile(t_score, 10) * 1e3:.1f}, "
+        f"p90 {np.percentile(t_score, 90) * 1e3:.1f}), fuse {t_fuse.mean() * 1e3:.1f} us, "
+        f"select {t_sel.mean() * 1e3:.1f} us; score {achieved:.0f} GB/s")
+
+    # ---- CPU oracle baseline ----------------------------------------------------
+    import oracle as O
+    from threadpoolctl import threadpool_info
+    cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    t_c = time.perf_counter()
+    done = 0
+    passes = 0
+    while True:
+        for b in range(B):
+            O.prune_image(q_np[b], k_np[b], cfg.grid_h, cfg.grid_w, cfg.keep, cfg.cells, cfg.lam,
+                          args.mode)
+            done += 1
+            if time.perf_counter() - t_c >= args.cpu_seconds and done >= 8:
+                break
+        passes += 1
+        if time.perf_counter() - t_c >= args.cpu_seconds:
+            break
+    cpu_s = time.perf_counter() - t_c
+    cpu_value = done / cpu_s
+    log(f"[bench] oracle: {done} images in {cpu_s:.1f}s on {cores} threads")
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"{cfg.name}: LLaVA-1.5-7B-shaped, batch {B} images, {cfg.num_layers} "
+                         f"source layers, {cfg.num_heads} heads x {cfg.head_dim}, "
+                         f"{cfg.num_text} text queries, {cfg.grid_h}x{cfg.grid_w}={N} visual "
+                         f"tokens, keep {cfg.keep}, G={cfg.cells}, lambda={cfg.lam}"),
+            "score_mode": args.mode,
+            "input_dtype": cfg.dtype,
+            "batch": B,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "score (e2s_score_heads)",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": algo_bytes,
+            "launch_us": round(score_ms * 1e3, 2),
+            "mfma_frac_if_eq1_flops": round(flops_eq1 / (score_ms * 1e-3) / 1e12
+                                            / MFMA_BF16_PEAK_TFLOPS, 4),
+        },
+        "stages_us": {"score": round(score_ms * 1e3, 2), "fuse": round(float(t_fuse.mean()) * 1e3, 2),
+                      "select": round(float(t_sel.mean()) * 1e3, 2)},
+        "path_hbm_frac": round(B * (per_img_qk) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "cpu_baseline": {
+            "value": round(cpu_value, 2),
+            "unit": "images/s",
+            "cores": cores,
+            "kind": "oracle",
+            "sample": (f"{done} images of the same {cfg.name} batch ({passes} pass(es) over "
+                       f"images 0..{B - 1}), NumPy float64 oracle, mode {args.mode}"),
+        },
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

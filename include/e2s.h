@@ -1,0 +1,169 @@
+/*
+ * e2s.h - C ABI of the E2S-Pruner token-scoring path on AMD Instinct MI355X (gfx950).
+ *
+ * The path (arXiv 2608.23253, Sec. 3.1 and 4) takes, for every image of a batch,
+ * the text-query and visual-key projections of L source layers and returns the
+ * K visual tokens to keep:
+ *
+ *   score      text->visual attention per head, normalized over the visual tokens,
+ *              mapped to a support p in [0,1)                   (Eq. 1, 8, 9)
+ *   reliability head clarity x consistency, mean support        (Eq. 10)
+ *   masses     (m(I), m(U), m(Theta)) per token and layer        (Eq. 11)
+ *   fusion     Dempster's rule across the layers with the conflict
+ *              of every step exported; retention priority q      (Eq. 12-19)
+ *   select     cell representatives, novelty bonus, global top-K (Eq. 20-23)
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Every tensor argument is a DEVICE pointer to memory the caller allocated and
+ *    owns.  The library never allocates, frees, copies between host and device,
+ *    or synchronises.  Each call first validates all arguments on the host; an
+ *    invalid call returns an error and enqueues nothing.  A valid call enqueues
+ *    its kernels on `stream` (a hipStream_t; NULL = the null stream) and returns
+ *    E2S_OK without waiting.  Errors inside a kernel are not reported.
+ *  - Tensors are dense, row-major (last index fastest) with the layouts given
+ *    below.  q and k must be 16-byte aligned, float/int outputs 4-byte aligned,
+ *    double outputs 8-byte aligned.  Outputs must not overlap inputs or each other.
+ *  - The library is stateless and reentrant; calls on different streams may
+ *    run concurrently.  There is no global error state.
+ *  - Centred quantities: the support p is exported as e = p - 1/2 and the
+ *    retention priority q as c = 1 - q (Eq. 19 rewritten with Eq. 18 as
+ *    c = m~(U) * (1 - K)).  Near the uniform-attention point p = 1/2 and q = 1,
+ *    so the centred forms keep the digits that decide the ranking.
+ *  - NaN or Inf in q/k give undefined values for that image only.
+ *
+ * Shape symbols: B batch, L source layers, H query heads, Hkv key heads
+ * (H % Hkv == 0; query head h reads key head floor(h*Hkv/H)), d head_dim,
+ * N_T text queries, N = N_V = grid_h * grid_w visual tokens in row-major
+ * raster order, K tokens kept.
+ */
+#ifndef E2S_H
+#define E2S_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define E2S_ABI_VERSION 1
+
+#if defined(__GNUC__) || defined(__clang__)
+#define E2S_API __attribute__((visibility("default")))
+#else
+#define E2S_API
+#endif
+
+typedef enum {
+    E2S_OK = 0,
+    E2S_ERR_NULL_POINTER = 1,         /* a required pointer is NULL                    */
+    E2S_ERR_BAD_SHAPE = 2,            /* a count is out of range or inconsistent       */
+    E2S_ERR_BAD_PARAM = 3,            /* dtype, mode, scale, cells, lambda or keep     */
+    E2S_ERR_UNSUPPORTED = 4,          /* valid per the paper, not implemented here     */
+    E2S_ERR_MISALIGNED = 5,           /* a pointer violates the alignment rule         */
+    E2S_ERR_WORKSPACE_TOO_SMALL = 6,  /* e2s_prune workspace below the required size   */
+    E2S_ERR_LAUNCH = 7                /* the HIP runtime refused a kernel launch       */
+} e2s_status;
+
+typedef enum { E2S_DTYPE_F32 = 0, E2S_DTYPE_BF16 = 1 } e2s_dtype;
+
+/* The two readings of how the text queries are reduced (Sec. 3.1, Eq. 1 and Eq. 8):
+ *  MEAN_LOGIT: a_n = mean_t Q_t.K_n * scale (Eq. 1), r = softmax over n of a (Eq. 8).
+ *  MEAN_PROB:  r_n = mean_t softmax over n of (Q_t.K_n * scale).              */
+typedef enum { E2S_SCORE_MEAN_LOGIT = 0, E2S_SCORE_MEAN_PROB = 1 } e2s_score_mode;
+
+typedef struct {
+    int32_t batch;         /* B >= 1                                   */
+    int32_t num_layers;    /* L >= 1 source layers, fused in order      */
+    int32_t num_heads;     /* H >= 1                                   */
+    int32_t num_kv_heads;  /* Hkv >= 1, H % Hkv == 0                   */
+    int32_t head_dim;      /* d: 64 or 128                             */
+    int32_t num_text;      /* N_T >= 1                                 */
+    int32_t grid_h;        /* visual grid rows >= 1                    */
+    int32_t grid_w;        /* visual grid cols >= 1; N = grid_h*grid_w <= 16384 */
+} e2s_shape;
+
+typedef struct {
+    int32_t dtype;   /* e2s_dtype of q and k                                     */
+    int32_t mode;    /* e2s_score_mode                                           */
+    float scale;     /* logit scale of Eq. 1; 0 selects 1/sqrt(head_dim)         */
+    int32_t cells;   /* G: cells per side, 1 <= G <= min(grid_h, grid_w) (paper: 4) */
+    float lambda;    /* novelty weight of Eq. 22, finite, in [0, 1] (paper: 0.1) */
+    int32_t keep;    /* K of Eq. 23, 0 <= K <= N                                 */
+} e2s_params;
+
+/* Score stage (Sec. 3.1 Eq. 1; Sec. 4.1 Eq. 8-9).
+ *   q  [B, L, H,   N_T, d]  dtype per params->dtype
+ *   k  [B, L, Hkv, N,   d]  same dtype
+ *   support_c [B, L, H, N] f32 out: e = p - 1/2 with p = N r / (1 + N r)
+ *   r_opt     [B, L, H, N] f32 out or NULL: r, the normalized attention
+ * Uses params->dtype, mode and scale (cells, lambda, keep are not checked). */
+E2S_API e2s_status e2s_score_heads(const e2s_shape* shape, const e2s_params* params,
+                           const void* q, const void* k,
+                           float* support_c, float* r_opt, void* stream);
+
+/* Head reliability (Sec. 4.1 Eq. 10) from support_c [B, L, H, N]:
+ *   rho    [B, L, N] f32 out: (2/H)|sum_h e_h| * (1 - (2/H) sum_h |e_h - ebar|)
+ *   pbar_c [B, L, N] f32 out: ebar = mean_h e_h = pbar - 1/2                       */
+E2S_API e2s_status e2s_head_reliability(const e2s_shape* shape, const float* support_c,
+                                float* rho, float* pbar_c, void* stream);
+
+/* Layer masses (Sec. 4.1 Eq. 11) from rho, pbar_c [B, L, N]:
+ *   mass [B, L, N, 3] f32 out: (rho (1/2 + ebar), rho (1/2 - ebar), 1 - rho)  = (I, U, Theta) */
+E2S_API e2s_status e2s_head_masses(const e2s_shape* shape, const float* rho, const float* pbar_c,
+                           float* mass, void* stream);
+
+/* Dempster fusion across the L layers in index order (Sec. 4.2 Eq. 12-19).
+ *   mass     [B, L, N, 3] f32 in (each triple a mass function over {I}, {U}, Theta)
+ *   fused    [B, N, 3]    f32 out: m~ after the last layer
+ *   conflict [B, L, N]    f32 out: K^(l) of Eq. 13, row l = 0 is 0
+ *   prio_c   [B, N]       f32 out: c = 1 - q = m~(U) (1 - K^(L))
+ * Total conflict (1 - K <= 0) makes the running mass vacuous (0, 0, 1) and records
+ * K = 1, so q = 1 there (Eq. 19).  fused and conflict may be NULL (not written). */
+E2S_API e2s_status e2s_ds_combine_layers(const e2s_shape* shape, const float* mass, float* fused,
+                                 float* conflict, float* prio_c, void* stream);
+
+/* Reliability, masses and fusion in one pass over support_c (Eq. 10-19); the
+ * results are bit-identical to the three staged calls above.
+ *   support_c [B, L, H, N] in; fused [B, N, 3], conflict [B, L, N] (both may be NULL),
+ *   prio_c [B, N] out. */
+E2S_API e2s_status e2s_fuse_evidence(const e2s_shape* shape, const float* support_c, float* fused,
+                             float* conflict, float* prio_c, void* stream);
+
+/* Spatial novelty and top-K (Sec. 4.3 Eq. 20-23) from prio_c [B, N]:
+ *   cells: cell(n) = floor(row*G/grid_h)*G + floor(col*G/grid_w), row = n / grid_w,
+ *   col = n % grid_w; the representative of a cell is its token of lowest c (highest
+ *   q), lowest index on ties; adjusted complement c^ = (1-lambda) c + lambda (1-b),
+ *   evaluated in double precision; the K tokens of smallest (c^, index) are kept.
+ *   keep_idx   [B, K] int32 out, ascending token indices; may be NULL iff K == 0
+ *   adj_c_opt  [B, N] double out or NULL: c^ = 1 - q~
+ *   is_rep_opt [B, N] uint8 out or NULL: b of Eq. 21
+ * Uses params->cells, lambda and keep. */
+E2S_API e2s_status e2s_spatial_select(const e2s_shape* shape, const e2s_params* params,
+                              const float* prio_c, int32_t* keep_idx, double* adj_c_opt,
+                              uint8_t* is_rep_opt, void* stream);
+
+/* Bytes of device workspace e2s_prune needs for this shape (host-only query). */
+E2S_API e2s_status e2s_prune_workspace_size(const e2s_shape* shape, const e2s_params* params,
+                                    size_t* bytes);
+
+/* The whole path (Algorithm 1 with every source layer fused before one top-K):
+ * e2s_score_heads -> e2s_fuse_evidence -> e2s_spatial_select on `stream`, with the
+ * intermediates in `workspace` (256-byte aligned, >= e2s_prune_workspace_size bytes).
+ *   keep_idx [B, K] int32 out (NULL iff K == 0); fused_opt [B, N, 3] and
+ *   prio_c_opt [B, N] f32 out or NULL. */
+E2S_API e2s_status e2s_prune(const e2s_shape* shape, const e2s_params* params, const void* q,
+                     const void* k, void* workspace, size_t workspace_bytes,
+                     int32_t* keep_idx, float* fused_opt, float* prio_c_opt, void* stream);
+
+/* Static description of a status code (never NULL). */
+E2S_API const char* e2s_status_string(e2s_status status);
+
+/* E2S_ABI_VERSION of the built library. */
+E2S_API int32_t e2s_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* E2S_H */

@@ -1,0 +1,330 @@
+"""ctypes binding of libe2s.so (the C ABI declared in include/e2s.h).
+
+Argument marshalling only: every step of the scoring path runs in the library's
+HIP kernels.  Two layers are exposed:
+
+  * ``lib()``: the loaded ``ctypes.CDLL`` with argument and result types set, so
+    the C entry points can be called directly with raw pointers;
+  * functions with the C names minus the ``e2s_`` prefix (``score_heads``,
+    ``head_reliability``, ``head_masses``, ``ds_combine_layers``,
+    ``fuse_evidence``, ``spatial_select``, ``prune``) that take torch tensors on
+    the GPU, allocate the outputs with torch, pass raw device pointers and the
+    current torch stream, and raise ``E2SError`` on a non-zero status.
+
+There is no fallback: if the library has not been built, importing the binding
+raises ``ImportError``.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import math
+import os
+import re
+from typing import Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libe2s.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "e2s.h")
+
+# status codes (e2s_status)
+OK, ERR_NULL_POINTER, ERR_BAD_SHAPE, ERR_BAD_PARAM, ERR_UNSUPPORTED, ERR_MISALIGNED, \
+    ERR_WORKSPACE_TOO_SMALL, ERR_LAUNCH = range(8)
+DTYPE_F32, DTYPE_BF16 = 0, 1
+MEAN_LOGIT, MEAN_PROB = 0, 1
+MODES = {"mean_logit": MEAN_LOGIT, "mean_prob": MEAN_PROB}
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("num_layers", ctypes.c_int32),
+                ("num_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("num_text", ctypes.c_int32),
+                ("grid_h", ctypes.c_int32), ("grid_w", ctypes.c_int32)]
+
+
+class Params(ctypes.Structure):
+    _fields_ = [("dtype", ctypes.c_int32), ("mode", ctypes.c_int32), ("scale", ctypes.c_float),
+                ("cells", ctypes.c_int32), ("lam", ctypes.c_float), ("keep", ctypes.c_int32)]
+
+
+class E2SError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        msg = _LIB.e2s_status_string(status).decode() if _LIB is not None else str(status)
+        super().__init__(f"{where}: {msg}")
+
+
+_P = ctypes.c_void_p
+_SH = ctypes.POINTER(Shape)
+_PA = ctypes.POINTER(Params)
+_SIGNATURES = {
+    "e2s_score_heads": [_SH, _PA, _P, _P, _P, _P, _P],
+    "e2s_head_reliability": [_SH, _P, _P, _P, _P],
+    "e2s_head_masses": [_SH, _P, _P, _P, _P],
+    "e2s_ds_combine_layers": [_SH, _P, _P, _P, _P, _P],
+    "e2s_fuse_evidence": [_SH, _P, _P, _P, _P, _P],
+    "e2s_spatial_select": [_SH, _PA, _P, _P, _P, _P, _P],
+    "e2s_prune_workspace_size": [_SH, _PA, ctypes.POINTER(ctypes.c_size_t)],
+    "e2s_prune": [_SH, _PA, _P, _P, _P, ctypes.c_size_t, _P, _P, _P, _P],
+    "e2s_status_string": [ctypes.c_int],
+    "e2s_abi_version": [],
+}
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python -m paper_2608_23253_amd.build` (or __graft_entry__.build())")
+    so = ctypes.CDLL(LIB_PATH)
+    for name, args in _SIGNATURES.items():
+        fn = getattr(so, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    so.e2s_status_string.restype = ctypes.c_char_p
+    so.e2s_abi_version.restype = ctypes.c_int32
+    return so
+
+
+_LIB: Optional[ctypes.CDLL] = _load()
+
+
+def lib() -> ctypes.CDLL:
+    return _LIB
+
+
+def header_entry_points(path: str = HEADER) -> list:
+    """Names of the functions include/e2s.h declares."""
+    with open(path) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(e2s_[a-z_]+)\s*\(", text)))
+
+
+# ---------------------------------------------------------------------------
+# torch-facing wrappers
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class Geometry:
+    grid_h: int
+    grid_w: int
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _check(t, name, dtype=None, ndim=None):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions (got {t.dim()})")
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device=None) -> int:
+    return _torch().cuda.current_stream(device).cuda_stream
+
+
+def _raise(status: int, where: str):
+    if status != OK:
+        raise E2SError(status, where)
+
+
+def make_shape(batch, num_layers, num_heads, num_kv_heads, head_dim, num_text, grid_h,
+               grid_w) -> Shape:
+    return Shape(batch, num_layers, num_heads, num_kv_heads, head_dim, num_text, grid_h, grid_w)
+
+
+def make_params(dtype=DTYPE_BF16, mode="mean_logit", scale=0.0, cells=4, lam=0.1,
+                keep=0) -> Params:
+    m = MODES[mode] if isinstance(mode, str) else int(mode)
+    return Params(int(dtype), m, float(scale), int(cells), float(lam), int(keep))
+
+
+def shape_from(q, k, grid_h: int, grid_w: int) -> Shape:
+    """Shape of a call from Q [B,L,H,N_T,d] and K [B,L,Hkv,N,d]."""
+    if q.dim() != 5 or k.dim() != 5:
+        raise ValueError("q must be [B,L,H,N_T,d] and k [B,L,Hkv,N,d]")
+    B, L, H, NT, D = q.shape
+    if k.shape[0] != B or k.shape[1] != L or k.shape[4] != D:
+        raise ValueError(f"q {tuple(q.shape)} and k {tuple(k.shape)} disagree")
+    if k.shape[3] != grid_h * grid_w:
+        raise ValueError(f"k has {k.shape[3]} visual tokens, grid {grid_h}x{grid_w}")
+    return make_shape(B, L, H, k.shape[2], D, NT, grid_h, grid_w)
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return DTYPE_BF16
+    if t.dtype == torch.float32:
+        return DTYPE_F32
+    raise TypeError(f"q/k must be bfloat16 or float32 (got {t.dtype})")
+
+
+def score_heads(q, k, grid_h: int, grid_w: int, mode="mean_logit", scale: float = 0.0,
+                want_r: bool = False):
+    """Eq. 1, 8, 9: returns (support_c [B,L,H,N] = p - 1/2, r or None)."""
+    torch = _torch()
+    _check(q, "q", ndim=5)
+    _check(k, "k", dtype=q.dtype, ndim=5)
+    sh = shape_from(q, k, grid_h, grid_w)
+    pa = make_params(_dtype_code(q), mode, scale)
+    n = grid_h * grid_w
+    e = torch.empty((sh.batch, sh.num_layers, sh.num_heads, n), device=q.device,
+                    dtype=torch.float32)
+    r = torch.empty_like(e) if want_r else None
+    _raise(_LIB.e2s_score_heads(ctypes.byref(sh), ctypes.byref(pa), q.data_ptr(), k.data_ptr(),
+                                e.data_ptr(), _ptr(r), _stream(q.device)), "e2s_score_heads")
+    return e, r
+
+
+def _shape_from_support(e, grid_h, grid_w) -> Shape:
+    B, L, H, N = e.shape
+    if N != grid_h * grid_w:
+        raise ValueError("support_c's last dimension must be grid_h*grid_w")
+    # num_kv_heads, head_dim and num_text do not enter the evidence stages
+    return make_shape(B, L, H, 1, 128, 1, grid_h, grid_w)
+
+
+def head_reliability(support_c, grid_h: int, grid_w: int):
+    """Eq. 10: (rho, pbar_c) each [B, L, N]."""
+    torch = _torch()
+    _check(support_c, "support_c", dtype=torch.float32, ndim=4)
+    sh = _shape_from_support(support_c, grid_h, grid_w)
+    B, L, H, N = support_c.shape
+    rho = torch.empty((B, L, N), device=support_c.device, dtype=torch.float32)
+    pbar = torch.empty_like(rho)
+    _raise(_LIB.e2s_head_reliability(ctypes.byref(sh), support_c.data_ptr(), rho.data_ptr(),
+                                     pbar.data_ptr(), _stream(support_c.device)),
+           "e2s_head_reliability")
+    return rho, pbar
+
+
+def head_masses(rho, pbar_c, grid_h: int, grid_w: int):
+    """Eq. 11: mass [B, L, N, 3] (I, U, Theta)."""
+    torch = _torch()
+    _check(rho, "rho", dtype=torch.float32, ndim=3)
+    _check(pbar_c, "pbar_c", dtype=torch.float32, ndim=3)
+    B, L, N = rho.shape
+    sh = make_shape(B, L, 1, 1, 128, 1, grid_h, grid_w)
+    mass = torch.empty((B, L, N, 3), device=rho.device, dtype=torch.float32)
+    _raise(_LIB.e2s_head_masses(ctypes.byref(sh), rho.data_ptr(), pbar_c.data_ptr(),
+                                mass.data_ptr(), _stream(rho.device)), "e2s_head_masses")
+    return mass
+
+
+def ds_combine_layers(mass, grid_h: int, grid_w: int, want_fused=True, want_conflict=True):
+    """Eq. 12-19: (fused [B,N,3] or None, conflict [B,L,N] or None, prio_c [B,N])."""
+    torch = _torch()
+    _check(mass, "mass", dtype=torch.float32, ndim=4)
+    B, L, N, _ = mass.shape
+    sh = make_shape(B, L, 1, 1, 128, 1, grid_h, grid_w)
+    dev = mass.device
+    fused = torch.empty((B, N, 3), device=dev, dtype=torch.float32) if want_fused else None
+    conflict = torch.empty((B, L, N), device=dev, dtype=torch.float32) if want_conflict else None
+    prio = torch.empty((B, N), device=dev, dtype=torch.float32)
+    _raise(_LIB.e2s_ds_combine_layers(ctypes.byref(sh), mass.data_ptr(), _ptr(fused),
+                                      _ptr(conflict), prio.data_ptr(), _stream(dev)),
+           "e2s_ds_combine_layers")
+    return fused, conflict, prio
+
+
+def fuse_evidence(support_c, grid_h: int, grid_w: int, want_fused=True, want_conflict=True):
+    """Eq. 10-19 in one pass: (fused or None, conflict or None, prio_c)."""
+    torch = _torch()
+    _check(support_c, "support_c", dtype=torch.float32, ndim=4)
+    sh = _shape_from_support(support_c, grid_h, grid_w)
+    B, L, H, N = support_c.shape
+    dev = support_c.device
+    fused = torch.empty((B, N, 3), device=dev, dtype=torch.float32) if want_fused else None
+    conflict = torch.empty((B, L, N), device=dev, dtype=torch.float32) if want_conflict else None
+    prio = torch.empty((B, N), device=dev, dtype=torch.float32)
+    _raise(_LIB.e2s_fuse_evidence(ctypes.byref(sh), support_c.data_ptr(), _ptr(fused),
+                                  _ptr(conflict), prio.data_ptr(), _stream(dev)),
+           "e2s_fuse_evidence")
+    return fused, conflict, prio
+
+
+def spatial_select(prio_c, grid_h: int, grid_w: int, keep: int, cells: int = 4,
+                   lam: float = 0.1, want_adj=False, want_rep=False):
+    """Eq. 20-23: (keep_idx [B,K] int32 ascending, adj_c [B,N] f64 or None, is_rep or None)."""
+    torch = _torch()
+    _check(prio_c, "prio_c", dtype=torch.float32, ndim=2)
+    B, N = prio_c.shape
+    sh = make_shape(B, 1, 1, 1, 128, 1, grid_h, grid_w)
+    pa = make_params(cells=cells, lam=lam, keep=keep)
+    dev = prio_c.device
+    out = torch.empty((B, keep), device=dev, dtype=torch.int32)
+    adj = torch.empty((B, N), device=dev, dtype=torch.float64) if want_adj else None
+    rep = torch.empty((B, N), device=dev, dtype=torch.uint8) if want_rep else None
+    _raise(_LIB.e2s_spatial_select(ctypes.byref(sh), ctypes.byref(pa), prio_c.data_ptr(),
+                                   out.data_ptr() if keep > 0 else None, _ptr(adj), _ptr(rep),
+                                   _stream(dev)), "e2s_spatial_select")
+    return out, adj, rep
+
+
+def workspace_size(shape: Shape, params: Params) -> int:
+    n = ctypes.c_size_t(0)
+    _raise(_LIB.e2s_prune_workspace_size(ctypes.byref(shape), ctypes.byref(params),
+                                         ctypes.byref(n)), "e2s_prune_workspace_size")
+    return int(n.value)
+
+
+class Pruner:
+    """Holds the shape, params and workspace of repeated e2s_prune calls."""
+
+    def __init__(self, q, k, grid_h: int, grid_w: int, keep: int, cells: int = 4,
+                 lam: float = 0.1, mode="mean_logit", scale: float = 0.0):
+        torch = _torch()
+        _check(q, "q", ndim=5)
+        _check(k, "k", dtype=q.dtype, ndim=5)
+        self.shape = shape_from(q, k, grid_h, grid_w)
+        self.params = make_params(_dtype_code(q), mode, scale, cells, lam, keep)
+        self.device = q.device
+        self.workspace = torch.empty(workspace_size(self.shape, self.params), device=q.device,
+                                     dtype=torch.uint8)
+        self.keep_idx = torch.empty((self.shape.batch, keep), device=q.device, dtype=torch.int32)
+
+    def __call__(self, q, k, fused=None, prio_c=None, stream: Optional[int] = None):
+        if tuple(q.shape) != (self.shape.batch, self.shape.num_layers, self.shape.num_heads,
+                              self.shape.num_text, self.shape.head_dim):
+            raise ValueError("q does not match the Pruner's shape")
+        if tuple(k.shape) != (self.shape.batch, self.shape.num_layers, self.shape.num_kv_heads,
+                              self.shape.grid_h * self.shape.grid_w, self.shape.head_dim):
+            raise ValueError("k does not match the Pruner's shape")
+        if q.dtype != k.dtype or _dtype_code(q) != self.params.dtype:
+            raise TypeError("q/k dtype does not match the Pruner's")
+        st = _stream(self.device) if stream is None else stream
+        _raise(_LIB.e2s_prune(ctypes.byref(self.shape), ctypes.byref(self.params), q.data_ptr(),
+                              k.data_ptr(), self.workspace.data_ptr(), self.workspace.numel(),
+                              self.keep_idx.data_ptr() if self.params.keep > 0 else None,
+                              _ptr(fused), _ptr(prio_c), st), "e2s_prune")
+        return self.keep_idx
+
+
+def prune(q, k, grid_h: int, grid_w: int, keep: int, cells: int = 4, lam: float = 0.1,
+          mode="mean_logit", scale: float = 0.0, want_fused=False, want_prio=False):
+    """The whole path: (keep_idx [B,K], fused [B,N,3] or None, prio_c [B,N] or None)."""
+    torch = _torch()
+    p = Pruner(q, k, grid_h, grid_w, keep, cells, lam, mode, scale)
+    B, N = p.shape.batch, grid_h * grid_w
+    fused = torch.empty((B, N, 3), device=q.device, dtype=torch.float32) if want_fused else None
+    prio = torch.empty((B, N), device=q.device, dtype=torch.float32) if want_prio else None
+    idx = p(q, k, fused, prio)
+    return idx, fused, prio
+
+
+def default_scale(head_dim: int) -> float:
+    return 1.0 / math.sqrt(head_dim)

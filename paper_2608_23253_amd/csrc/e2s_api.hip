@@ -1,0 +1,198 @@
+// extern "C" entry points of libe2s.so (declared and documented in include/e2s.h).
+// Each call validates every argument on the host before it touches the HIP
+// runtime, then enqueues its kernels on the caller's stream.
+#include <cmath>
+
+#include "e2s.h"
+#include "e2s_kernels.h"
+#include "e2s_validate.h"
+
+namespace {
+
+using e2s::Dims;
+
+e2s_status from_hip(hipError_t err) {
+    if (err == hipSuccess) return E2S_OK;
+    if (err == hipErrorNotSupported) return E2S_ERR_UNSUPPORTED;
+    return E2S_ERR_LAUNCH;
+}
+
+#define E2S_TRY(expr)                          \
+    do {                                       \
+        const e2s_status st_ = (expr);         \
+        if (st_ != E2S_OK) return st_;         \
+    } while (0)
+
+e2s_status need(const void* p) { return p ? E2S_OK : E2S_ERR_NULL_POINTER; }
+e2s_status aligned_opt(const void* p, size_t a) { return p ? e2s::check_aligned(p, a) : E2S_OK; }
+
+float effective_scale(const e2s_params* p, const Dims& d) {
+    if (p->scale != 0.0f) return p->scale;
+    return static_cast<float>(1.0 / std::sqrt(static_cast<double>(d.D)));
+}
+
+e2s_status check_score_call(const e2s_shape* shape, const e2s_params* params, const void* q,
+                            const void* k, const float* support_c, const float* r_opt,
+                            Dims* d) {
+    E2S_TRY(e2s::check_shape(shape, d));
+    E2S_TRY(e2s::check_score_params(params));
+    E2S_TRY(need(q));
+    E2S_TRY(need(k));
+    E2S_TRY(need(support_c));
+    E2S_TRY(e2s::check_aligned(q, 16));
+    E2S_TRY(e2s::check_aligned(k, 16));
+    E2S_TRY(e2s::check_aligned(support_c, 4));
+    E2S_TRY(aligned_opt(r_opt, 4));
+    return E2S_OK;
+}
+
+e2s_status run_score(const Dims& d, const e2s_params* params, const void* q, const void* k,
+                     float* support_c, float* r_opt, hipStream_t st) {
+    const float scale = effective_scale(params, d);
+    if (params->mode == E2S_SCORE_MEAN_LOGIT)
+        return from_hip(e2s::launch_score_mean_logit(d, params->dtype, scale, q, k, support_c,
+                                                     r_opt, st));
+    return from_hip(
+        e2s::launch_score_mean_prob(d, params->dtype, scale, q, k, support_c, r_opt, st));
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t e2s_abi_version(void) { return E2S_ABI_VERSION; }
+
+const char* e2s_status_string(e2s_status status) {
+    switch (status) {
+        case E2S_OK: return "E2S_OK";
+        case E2S_ERR_NULL_POINTER: return "E2S_ERR_NULL_POINTER: a required pointer is NULL";
+        case E2S_ERR_BAD_SHAPE: return "E2S_ERR_BAD_SHAPE: a count is out of range or inconsistent";
+        case E2S_ERR_BAD_PARAM: return "E2S_ERR_BAD_PARAM: dtype, mode, scale, cells, lambda or keep";
+        case E2S_ERR_UNSUPPORTED: return "E2S_ERR_UNSUPPORTED: valid but not implemented by this build";
+        case E2S_ERR_MISALIGNED: return "E2S_ERR_MISALIGNED: a pointer violates the alignment rule";
+        case E2S_ERR_WORKSPACE_TOO_SMALL: return "E2S_ERR_WORKSPACE_TOO_SMALL: workspace below e2s_prune_workspace_size";
+        case E2S_ERR_LAUNCH: return "E2S_ERR_LAUNCH: the HIP runtime refused a kernel launch";
+    }
+    return "unknown e2s_status";
+}
+
+e2s_status e2s_score_heads(const e2s_shape* shape, const e2s_params* params, const void* q,
+                           const void* k, float* support_c, float* r_opt, void* stream) {
+    Dims d;
+    E2S_TRY(check_score_call(shape, params, q, k, support_c, r_opt, &d));
+    return run_score(d, params, q, k, support_c, r_opt, static_cast<hipStream_t>(stream));
+}
+
+e2s_status e2s_head_reliability(const e2s_shape* shape, const float* support_c, float* rho,
+                                float* pbar_c, void* stream) {
+    Dims d;
+    E2S_TRY(e2s::check_shape(shape, &d));
+    E2S_TRY(need(support_c));
+    E2S_TRY(need(rho));
+    E2S_TRY(need(pbar_c));
+    E2S_TRY(e2s::check_aligned(support_c, 4));
+    E2S_TRY(e2s::check_aligned(rho, 4));
+    E2S_TRY(e2s::check_aligned(pbar_c, 4));
+    return from_hip(e2s::launch_head_reliability(d, support_c, rho, pbar_c,
+                                                 static_cast<hipStream_t>(stream)));
+}
+
+e2s_status e2s_head_masses(const e2s_shape* shape, const float* rho, const float* pbar_c,
+                           float* mass, void* stream) {
+    Dims d;
+    E2S_TRY(e2s::check_shape(shape, &d));
+    E2S_TRY(need(rho));
+    E2S_TRY(need(pbar_c));
+    E2S_TRY(need(mass));
+    E2S_TRY(e2s::check_aligned(rho, 4));
+    E2S_TRY(e2s::check_aligned(pbar_c, 4));
+    E2S_TRY(e2s::check_aligned(mass, 4));
+    return from_hip(e2s::launch_head_masses(d, rho, pbar_c, mass, static_cast<hipStream_t>(stream)));
+}
+
+e2s_status e2s_ds_combine_layers(const e2s_shape* shape, const float* mass, float* fused,
+                                 float* conflict, float* prio_c, void* stream) {
+    Dims d;
+    E2S_TRY(e2s::check_shape(shape, &d));
+    E2S_TRY(need(mass));
+    E2S_TRY(need(prio_c));
+    E2S_TRY(e2s::check_aligned(mass, 4));
+    E2S_TRY(e2s::check_aligned(prio_c, 4));
+    E2S_TRY(aligned_opt(fused, 4));
+    E2S_TRY(aligned_opt(conflict, 4));
+    return from_hip(e2s::launch_ds_combine(d, mass, fused, conflict, prio_c,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+e2s_status e2s_fuse_evidence(const e2s_shape* shape, const float* support_c, float* fused,
+                             float* conflict, float* prio_c, void* stream) {
+    Dims d;
+    E2S_TRY(e2s::check_shape(shape, &d));
+    E2S_TRY(need(support_c));
+    E2S_TRY(need(prio_c));
+    E2S_TRY(e2s::check_aligned(support_c, 4));
+    E2S_TRY(e2s::check_aligned(prio_c, 4));
+    E2S_TRY(aligned_opt(fused, 4));
+    E2S_TRY(aligned_opt(conflict, 4));
+    return from_hip(e2s::launch_fuse_evidence(d, support_c, fused, conflict, prio_c,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+e2s_status e2s_spatial_select(const e2s_shape* shape, const e2s_params* params,
+                              const float* prio_c, int32_t* keep_idx, double* adj_c_opt,
+                              uint8_t* is_rep_opt, void* stream) {
+    Dims d;
+    E2S_TRY(e2s::check_shape(shape, &d));
+    E2S_TRY(e2s::check_select_params(params, d));
+    E2S_TRY(need(prio_c));
+    if (params->keep > 0) E2S_TRY(need(keep_idx));
+    E2S_TRY(e2s::check_aligned(prio_c, 4));
+    E2S_TRY(aligned_opt(keep_idx, 4));
+    E2S_TRY(aligned_opt(adj_c_opt, 8));
+    return from_hip(e2s::launch_spatial_select(d, params->cells, params->lambda, params->keep,
+                                               prio_c, keep_idx, adj_c_opt, is_rep_opt,
+                                               static_cast<hipStream_t>(stream)));
+}
+
+e2s_status e2s_prune_workspace_size(const e2s_shape* shape, const e2s_params* params,
+                                    size_t* bytes) {
+    Dims d;
+    E2S_TRY(e2s::check_shape(shape, &d));
+    E2S_TRY(need(params));
+    E2S_TRY(need(bytes));
+    *bytes = e2s::prune_workspace_bytes(d);
+    return E2S_OK;
+}
+
+e2s_status e2s_prune(const e2s_shape* shape, const e2s_params* params, const void* q,
+                     const void* k, void* workspace, size_t workspace_bytes, int32_t* keep_idx,
+                     float* fused_opt, float* prio_c_opt, void* stream) {
+    Dims d;
+    E2S_TRY(e2s::check_shape(shape, &d));
+    E2S_TRY(e2s::check_score_params(params));
+    E2S_TRY(e2s::check_select_params(params, d));
+    E2S_TRY(need(q));
+    E2S_TRY(need(k));
+    E2S_TRY(need(workspace));
+    if (params->keep > 0) E2S_TRY(need(keep_idx));
+    E2S_TRY(e2s::check_aligned(q, 16));
+    E2S_TRY(e2s::check_aligned(k, 16));
+    E2S_TRY(e2s::check_aligned(workspace, 256));
+    E2S_TRY(aligned_opt(keep_idx, 4));
+    E2S_TRY(aligned_opt(fused_opt, 4));
+    E2S_TRY(aligned_opt(prio_c_opt, 4));
+    if (workspace_bytes < e2s::prune_workspace_bytes(d)) return E2S_ERR_WORKSPACE_TOO_SMALL;
+
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    float* support_c = static_cast<float*>(workspace);
+    const size_t e_bytes =
+        e2s::align_up(static_cast<size_t>(d.B * d.L * d.H * d.N) * sizeof(float), 256);
+    float* prio_c = prio_c_opt ? prio_c_opt
+                               : reinterpret_cast<float*>(static_cast<char*>(workspace) + e_bytes);
+    E2S_TRY(run_score(d, params, q, k, support_c, nullptr, st));
+    E2S_TRY(from_hip(e2s::launch_fuse_evidence(d, support_c, fused_opt, nullptr, prio_c, st)));
+    return from_hip(e2s::launch_spatial_select(d, params->cells, params->lambda, params->keep,
+                                               prio_c, keep_idx, nullptr, nullptr, st));
+}
+
+}  // extern "C"

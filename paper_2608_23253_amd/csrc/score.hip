@@ -1,0 +1,212 @@
+// Score stage: text->visual attention per head, normalized over the visual tokens
+// and mapped to a centred support e = p - 1/2 (Sec. 3.1 Eq. 1; Sec. 4.1 Eq. 8-9).
+//
+// Mean-of-logits reading.  Eq. 1 averages Q_t.K_n / sqrt(d) over the text queries;
+// by linearity that equals (mean_t Q_t).K_n / sqrt(d), so the stage is a stream of
+// the key tensor against one query vector per head: an HBM-bound matrix-vector
+// product.  One workgroup owns one (image, layer, key head) unit (and a chunk of
+// at most 8 of the query heads that share that key head under grouped-query
+// attention), so every key row is read from HBM exactly once:
+//
+//   A  qbar_h = (scale / N_T) * sum_t Q[h, t, :]             (fp32, LDS)
+//   B  a[h, n] = qbar_h . K[n, :]                             (fp32, LDS)
+//      16 lanes (d = 128) or 8 lanes (d = 64) share one key row; each lane loads
+//      16 contiguous bytes, so a wave-wide load covers 1 KB of contiguous keys;
+//      the partial dot products are summed with DPP row operations.
+//   C  per head (one wave): m = max_n a, S = sum_n exp(a_n - m),
+//      E = sum_n expm1(a_n - m) = S - N, and L = log(S / N)
+//   D  u_n = N r_n - 1 = expm1(a_n - m - L),  e_n = u_n / (2 (2 + u_n)) = p_n - 1/2,
+//      r_n = exp(a_n - m - L) / N.
+//
+// Steps C-D carry the softmax in log-sum-exp-centred form.  Near uniform attention
+// (a_n - m = O(1e-3), the regime of Gaussian keys at the 1/sqrt(d) scale) the
+// naive N r - 1 loses ~10 bits to cancellation; expm1 of the centred logit keeps
+// full relative precision.  L itself is taken from whichever sum is exact in the
+// current regime: log1p(E / N) when S > N/2 (E, a sum of small non-positive
+// terms, has no cancellation), log(S / N) when attention is peaked (S is then a
+// sum dominated by a few O(1) positive terms).
+#include "e2s_device.h"
+#include "e2s_kernels.h"
+
+#include <cmath>
+
+namespace e2s {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kMaxChunk = 8;                  // query heads per workgroup
+constexpr int kLdsBudget = 96 * 1024;         // bytes of dynamic LDS per workgroup
+constexpr int kUnroll = 4;                    // key rows in flight per lane
+
+template <typename T, int D, int RC>
+__global__ __launch_bounds__(kThreads) void score_mean_logit_kernel(
+    const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
+    float* __restrict__ r_out, int H, int Hkv, int NT, int N, int group, int chunk,
+    int nchunks, float qscale) {
+    constexpr int LPR = D / 8;            // lanes per row (8 elements per lane)
+    constexpr int RPP = kThreads / LPR;   // rows per block-wide pass (phase A)
+    constexpr int RPW = kWave / LPR;      // rows per wave-wide load (phase B)
+    constexpr int STEP = kWaves * RPW;    // rows per block-wide load
+
+    extern __shared__ float smem[];
+    float* qbar = smem;                   // [RC][D]
+    float* part = qbar + RC * D;          // [RPP][D]
+    float* logits = part + RPP * D;       // [rc][N]
+
+    const int unit = blockIdx.x / nchunks;        // (b*L + l)*Hkv + g
+    const int ci = blockIdx.x - unit * nchunks;
+    const int g = unit % Hkv;
+    const int64_t bl = unit / Hkv;                // b*L + l
+    const int hq0 = g * group + ci * chunk;       // first query head of this chunk
+    const int rc = min(chunk, group - ci * chunk);
+    const int tid = threadIdx.x;
+
+    // ---- A: mean query per head --------------------------------------------
+    {
+        const int prow = tid / LPR, plane = tid % LPR;
+        for (int j = 0; j < rc; ++j) {
+            const T* qh = q + ((bl * H + hq0 + j) * NT) * D + plane * 8;
+            float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            for (int t = prow; t < NT; t += RPP) {
+                Packet<T> p;
+                load_packet(p, qh + static_cast<int64_t>(t) * D);
+                float x[8];
+                unpack(p, x);
+#pragma unroll
+                for (int m = 0; m < 8; ++m) acc[m] += x[m];
+            }
+#pragma unroll
+            for (int m = 0; m < 8; ++m) part[prow * D + plane * 8 + m] = acc[m];
+            __syncthreads();
+            if (tid < D) {
+                float s = 0.f;
+                for (int r = 0; r < RPP; ++r) s += part[r * D + tid];
+                qbar[j * D + tid] = s * qscale;
+            }
+            __syncthreads();
+        }
+    }
+
+    // ---- B: logits a[h, n] --------------------------------------------------
+    const int wave = tid / kWave, lane = tid % kWave;
+    const int wrow = lane / LPR, wl = lane % LPR;
+    float qb[RC][8];
+#pragma unroll
+    for (int j = 0; j < RC; ++j)
+#pragma unroll
+        for (int m = 0; m < 8; ++m) qb[j][m] = (j < rc) ? qbar[j * D + wl * 8 + m] : 0.f;
+
+    const T* kg = k + static_cast<int64_t>(unit) * N * D + wl * 8;
+    for (int base = wave * RPW; base < N; base += STEP * kUnroll) {
+        Packet<T> p[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int n = base + wrow + u * STEP;
+            if (n < N) {
+                load_packet(p[u], kg + static_cast<int64_t>(n) * D);
+            } else {
+                p[u] = Packet<T>{};
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int n = base + wrow + u * STEP;
+            float x[8];
+            unpack(p[u], x);
+#pragma unroll
+            for (int j = 0; j < RC; ++j) {
+                if (j < rc) {
+                    float s = qb[j][0] * x[0];
+#pragma unroll
+                    for (int m = 1; m < 8; ++m) s = fmaf(qb[j][m], x[m], s);
+                    s = group_sum<LPR>(s);
+                    if (wl == 0 && n < N) logits[j * N + n] = s;
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- C, D: centred softmax and support, one wave per head ---------------
+    const float fN = static_cast<float>(N);
+    for (int j = wave; j < rc; j += kWaves) {
+        float* a = logits + j * N;
+        float m = -INFINITY;
+        for (int n = lane; n < N; n += kWave) m = fmaxf(m, a[n]);
+        m = wave_max(m);
+        float E = 0.f, S = 0.f;
+        for (int n = lane; n < N; n += kWave) {
+            const float d = a[n] - m;
+            a[n] = d;
+            E += expm1f(d);
+            S += expf(d);
+        }
+        E = wave_sum(E);
+        S = wave_sum(S);
+        const float lse = log_mean_exp(E, S, fN);
+        const int64_t row = (bl * H + hq0 + j) * static_cast<int64_t>(N);
+        float* eo = e_out + row;
+        float* ro = r_out ? r_out + row : nullptr;
+        for (int n = lane; n < N; n += kWave) {
+            const float dc = a[n] - lse;
+            const float u = expm1f(dc);
+            eo[n] = u / (2.0f * (2.0f + u));
+            if (ro) ro[n] = expf(dc) / fN;
+        }
+    }
+}
+
+template <typename T, int D, int RC>
+hipError_t launch_ml(const Dims& d, float qscale, const void* q, const void* k, float* e,
+                     float* r, int chunk, int nchunks, hipStream_t st) {
+    constexpr int RPP = kThreads / (D / 8);
+    const size_t lds = (static_cast<size_t>(RC) * D + static_cast<size_t>(RPP) * D +
+                        static_cast<size_t>(chunk) * d.N) * sizeof(float);
+    auto kern = score_mean_logit_kernel<T, D, RC>;
+    if (lds > 64 * 1024) {
+        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             static_cast<int>(lds));
+        if (err != hipSuccess) return err;
+    }
+    const int64_t blocks = d.B * d.L * d.Hkv * nchunks;
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), lds, st,
+                       static_cast<const T*>(q), static_cast<const T*>(k), e, r,
+                       static_cast<int>(d.H), static_cast<int>(d.Hkv), static_cast<int>(d.NT),
+                       static_cast<int>(d.N), static_cast<int>(d.group), chunk, nchunks, qscale);
+    return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t dispatch_rc(const Dims& d, float qscale, const void* q, const void* k, float* e,
+                       float* r, hipStream_t st) {
+    constexpr int RPP = kThreads / (D / 8);
+    const int64_t fixed = (static_cast<int64_t>(kMaxChunk) * D + RPP * D) * 4;
+    int64_t fit = (kLdsBudget - fixed) / (d.N * 4);
+    if (fit < 1) fit = 1;
+    int chunk = static_cast<int>(std::min<int64_t>({d.group, kMaxChunk, fit}));
+    const int nchunks = static_cast<int>((d.group + chunk - 1) / chunk);
+    chunk = static_cast<int>((d.group + nchunks - 1) / nchunks);  // balance the chunks
+    if (chunk <= 1) return launch_ml<T, D, 1>(d, qscale, q, k, e, r, chunk, nchunks, st);
+    if (chunk <= 2) return launch_ml<T, D, 2>(d, qscale, q, k, e, r, chunk, nchunks, st);
+    if (chunk <= 4) return launch_ml<T, D, 4>(d, qscale, q, k, e, r, chunk, nchunks, st);
+    return launch_ml<T, D, 8>(d, qscale, q, k, e, r, chunk, nchunks, st);
+}
+
+}  // namespace
+
+hipError_t launch_score_mean_logit(const Dims& d, int dtype, float scale, const void* q,
+                                   const void* k, float* support_c, float* r_opt,
+                                   hipStream_t stream) {
+    const float qscale = static_cast<float>(static_cast<double>(scale) / static_cast<double>(d.NT));
+    if (dtype == E2S_DTYPE_BF16) {
+        if (d.D == 128)
+            return dispatch_rc<uint16_t, 128>(d, qscale, q, k, support_c, r_opt, stream);
+        return dispatch_rc<uint16_t, 64>(d, qscale, q, k, support_c, r_opt, stream);
+    }
+    if (d.D == 128) return dispatch_rc<float, 128>(d, qscale, q, k, support_c, r_opt, stream);
+    return dispatch_rc<float, 64>(d, qscale, q, k, support_c, r_opt, stream);
+}
+
+}  // namespace e2s

@@ -1,0 +1,146 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point the
+header declares, and rejects invalid calls on the host before any launch.
+
+Every call below is invalid in exactly one way, so it returns before it touches
+the HIP runtime; the fake device addresses are never dereferenced.
+"""
+import ctypes
+
+import pytest
+
+from paper_2608_23253_amd import _lib as L
+
+lib = L.lib()
+A = 1 << 20          # a fake, 256-byte aligned device address (never dereferenced)
+
+
+def good_shape(**kw):
+    s = dict(batch=2, num_layers=3, num_heads=4, num_kv_heads=2, head_dim=64, num_text=5,
+             grid_h=6, grid_w=7)
+    s.update(kw)
+    return L.make_shape(**s)
+
+
+def good_params(**kw):
+    p = dict(dtype=L.DTYPE_BF16, mode="mean_logit", scale=0.0, cells=3, lam=0.1, keep=10)
+    p.update(kw)
+    return L.make_params(**p)
+
+
+def score(shape, params, q=A, k=A, e=A, r=None):
+    return lib.e2s_score_heads(ctypes.byref(shape) if shape is not None else None,
+                               ctypes.byref(params) if params is not None else None,
+                               q, k, e, r, None)
+
+
+def select(shape, params, c=A, out=A, adj=None, rep=None):
+    return lib.e2s_spatial_select(ctypes.byref(shape), ctypes.byref(params), c, out, adj, rep,
+                                  None)
+
+
+def prune(shape, params, q=A, k=A, ws=A, ws_bytes=None, out=A):
+    if ws_bytes is None:
+        ws_bytes = L.workspace_size(shape, params)
+    return lib.e2s_prune(ctypes.byref(shape), ctypes.byref(params), q, k, ws, ws_bytes, out,
+                         None, None, None)
+
+
+def test_exports_every_declared_entry_point():
+    names = L.header_entry_points()
+    assert len(names) == 10
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.e2s_abi_version() == 1
+
+
+def test_status_strings():
+    for code in range(8):
+        s = lib.e2s_status_string(code).decode()
+        assert s.startswith("E2S_")
+    assert b"unknown" in lib.e2s_status_string(99)
+
+
+@pytest.mark.parametrize("field,value,expect", [
+    ("batch", 0, L.ERR_BAD_SHAPE), ("num_layers", 0, L.ERR_BAD_SHAPE),
+    ("num_heads", 0, L.ERR_BAD_SHAPE), ("num_kv_heads", 3, L.ERR_BAD_SHAPE),
+    ("num_kv_heads", 0, L.ERR_BAD_SHAPE), ("head_dim", 96, L.ERR_UNSUPPORTED),
+    ("head_dim", 0, L.ERR_BAD_SHAPE), ("num_text", 0, L.ERR_BAD_SHAPE),
+    ("grid_h", 0, L.ERR_BAD_SHAPE), ("grid_w", -1, L.ERR_BAD_SHAPE),
+    ("grid_h", 200, L.ERR_UNSUPPORTED),          # with grid_w = 100: N = 20000 > 16384
+])
+def test_bad_shapes(field, value, expect):
+    kw = {field: value}
+    if field == "grid_h" and value == 200:
+        kw["grid_w"] = 100                        # N = 20000 > 16384
+    assert score(good_shape(**kw), good_params()) == expect
+
+
+@pytest.mark.parametrize("field,value", [
+    ("dtype", 5), ("mode", 2), ("scale", -1.0), ("scale", float("nan")), ("scale", float("inf")),
+])
+def test_bad_score_params(field, value):
+    assert score(good_shape(), good_params(**{field: value})) == L.ERR_BAD_PARAM
+
+
+@pytest.mark.parametrize("field,value", [
+    ("cells", 0), ("cells", 7), ("lam", -0.01), ("lam", 1.5), ("lam", float("nan")),
+    ("keep", -1), ("keep", 43),
+])
+def test_bad_select_params(field, value):
+    # grid 6x7 = 42 tokens: cells <= 6, keep <= 42
+    assert select(good_shape(), good_params(**{field: value})) == L.ERR_BAD_PARAM
+    assert prune(good_shape(), good_params(**{field: value}), ws_bytes=1 << 30) == L.ERR_BAD_PARAM
+
+
+def test_null_pointers():
+    assert score(None, good_params()) == L.ERR_NULL_POINTER
+    assert score(good_shape(), None) == L.ERR_NULL_POINTER
+    assert score(good_shape(), good_params(), q=None) == L.ERR_NULL_POINTER
+    assert score(good_shape(), good_params(), k=None) == L.ERR_NULL_POINTER
+    assert score(good_shape(), good_params(), e=None) == L.ERR_NULL_POINTER
+    assert select(good_shape(), good_params(), c=None) == L.ERR_NULL_POINTER
+    assert select(good_shape(), good_params(), out=None) == L.ERR_NULL_POINTER
+    assert prune(good_shape(), good_params(), ws=None) == L.ERR_NULL_POINTER
+    assert prune(good_shape(), good_params(), out=None) == L.ERR_NULL_POINTER
+    sh = good_shape()
+    assert lib.e2s_head_reliability(ctypes.byref(sh), None, A, A, None) == L.ERR_NULL_POINTER
+    assert lib.e2s_head_masses(ctypes.byref(sh), A, None, A, None) == L.ERR_NULL_POINTER
+    assert lib.e2s_ds_combine_layers(ctypes.byref(sh), A, None, None, None, None) == \
+        L.ERR_NULL_POINTER
+    assert lib.e2s_fuse_evidence(ctypes.byref(sh), None, None, None, A, None) == \
+        L.ERR_NULL_POINTER
+    n = ctypes.c_size_t()
+    assert lib.e2s_prune_workspace_size(None, ctypes.byref(good_params()), ctypes.byref(n)) == \
+        L.ERR_NULL_POINTER
+
+
+def test_misaligned_pointers():
+    assert score(good_shape(), good_params(), q=A + 8) == L.ERR_MISALIGNED
+    assert score(good_shape(), good_params(), k=A + 2) == L.ERR_MISALIGNED
+    assert score(good_shape(), good_params(), e=A + 2) == L.ERR_MISALIGNED
+    assert select(good_shape(), good_params(), adj=A + 4) == L.ERR_MISALIGNED
+    assert prune(good_shape(), good_params(), ws=A + 16) == L.ERR_MISALIGNED
+
+
+def test_workspace_size_and_too_small():
+    sh, pa = good_shape(), good_params()
+    need = L.workspace_size(sh, pa)
+    e = 2 * 3 * 4 * 42 * 4
+    c = 2 * 42 * 4
+    assert need == -(-e // 256) * 256 + -(-c // 256) * 256
+    assert prune(sh, pa, ws_bytes=need - 1) == L.ERR_WORKSPACE_TOO_SMALL
+
+
+def test_keep_zero_allows_null_output():
+    """K = 0 (the paper's 20 -> 8 -> 0 schedule) is valid and needs no output buffer;
+    the call is only validated here: a misaligned score pointer, checked after the
+    output pointer, stops it before any launch."""
+    assert select(good_shape(), good_params(keep=0), c=A + 2, out=None) == L.ERR_MISALIGNED
+    assert select(good_shape(), good_params(keep=1), c=A + 2, out=None) == L.ERR_NULL_POINTER
+
+
+def test_binding_rejects_cpu_tensors():
+    torch = pytest.importorskip("torch")
+    q = torch.zeros((1, 1, 1, 1, 64), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        L.score_heads(q, q, 1, 1)

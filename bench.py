@@ -46,6 +46,8 @@ def parse():
                     help="minimum CPU time spent timing the oracle")
     ap.add_argument("--kernel-only", action="store_true")
     ap.add_argument("--copy-calibrate", type=int, default=0, metavar="N_MIB")
+    ap.add_argument("--hbm-probe", type=int, default=0, metavar="N_MIB",
+                    help="time a streaming read (torch sum) of N MiB: a practical read ceiling")
     return ap.parse_args()
 
 
@@ -97,6 +99,24 @@ def copy_calibrate(mib: int):
                       "ms": ms, "GBps": moved / ms / 1e6}))
 
 
+def hbm_probe(mib: int):
+    import torch
+    n = mib * (1 << 20) // 4
+    x = torch.ones(n, device="cuda", dtype=torch.float32)
+    out = torch.empty((), device="cuda", dtype=torch.float32)
+    for _ in range(3):
+        torch.sum(x, out=out)
+    torch.cuda.synchronize()
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record()
+    for _ in range(10):
+        torch.sum(x, out=out)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / 10
+    print(json.dumps({"read_mib": mib, "ms": ms, "GBps": n * 4 / ms / 1e6}))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -106,6 +126,9 @@ def main():
         sys.exit(2)
     if args.copy_calibrate:
         copy_calibrate(args.copy_calibrate)
+        return
+    if args.hbm_probe:
+        hbm_probe(args.hbm_probe)
         return
 
     import numpy as np

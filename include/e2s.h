@@ -76,7 +76,7 @@ typedef enum { E2S_SCORE_MEAN_LOGIT = 0, E2S_SCORE_MEAN_PROB = 1 } e2s_score_mod
 typedef struct {
     int32_t batch;         /* B >= 1                                   */
     int32_t num_layers;    /* L >= 1 source layers, fused in order      */
-    int32_t num_heads;     /* H >= 1                                   */
+    int32_t num_heads;     /* H >= 1, at most 128                      */
     int32_t num_kv_heads;  /* Hkv >= 1, H % Hkv == 0                   */
     int32_t head_dim;      /* d: 64 or 128                             */
     int32_t num_text;      /* N_T >= 1                                 */

@@ -30,6 +30,7 @@ e2s_status check_shape(const e2s_shape* s, Dims* out) {
     d.N = d.gh * d.gw;
     d.group = d.H / d.Hkv;
     if (d.N > kMaxVisual) return E2S_ERR_UNSUPPORTED;
+    if (d.H > kMaxHeads) return E2S_ERR_UNSUPPORTED;
     if (d.D != 64 && d.D != 128) return E2S_ERR_UNSUPPORTED;
     // Every tensor of the call must be indexable with 63-bit element offsets and
     // the grids must stay below 2^31 workgroups.

@@ -16,6 +16,7 @@ struct Dims {
 };
 
 constexpr int64_t kMaxVisual = 16384;  // one image's scores fit in a workgroup's LDS
+constexpr int64_t kMaxHeads = 128;     // per-token head supports held in registers
 
 e2s_status check_shape(const e2s_shape* s, Dims* out);
 e2s_status check_score_params(const e2s_params* p);

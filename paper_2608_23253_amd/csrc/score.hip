@@ -8,15 +8,22 @@
 // at most 8 of the query heads that share that key head under grouped-query
 // attention), so every key row is read from HBM exactly once:
 //
-//   A  qbar_h = (scale / N_T) * sum_t Q[h, t, :]             (fp32, LDS)
+//   A  qbar_h = (scale / N_T) * sum_t Q[h, t, :]             (fp32, LDS); the first
+//      key rows are already being loaded while this runs, and all heads of the
+//      workgroup are reduced before a single barrier
 //   B  a[h, n] = qbar_h . K[n, :]                             (fp32, LDS)
 //      16 lanes (d = 128) or 8 lanes (d = 64) share one key row; each lane loads
 //      16 contiguous bytes, so a wave-wide load covers 1 KB of contiguous keys;
 //      the partial dot products are summed with DPP row operations.
-//   C  per head (one wave): m = max_n a, S = sum_n exp(a_n - m),
+//   C  per head (one wave per head, or the whole workgroup when it owns a single
+//      head): m = max_n a, S = sum_n exp(a_n - m),
 //      E = sum_n expm1(a_n - m) = S - N, and L = log(S / N)
 //   D  u_n = N r_n - 1 = expm1(a_n - m - L),  e_n = u_n / (2 (2 + u_n)) = p_n - 1/2,
 //      r_n = exp(a_n - m - L) / N.
+//
+// The supports are written with non-temporal stores: the key stream reads at
+// ~7 TB/s on its own, and cached write-backs interleaved with it cost more
+// read bandwidth than the bytes they carry.
 //
 // Steps C-D carry the softmax in log-sum-exp-centred form.  Near uniform attention
 // (a_n - m = O(1e-3), the regime of Gaussian keys at the 1/sqrt(d) scale) the
@@ -37,7 +44,7 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kMaxChunk = 8;                  // query heads per workgroup
 constexpr int kLdsBudget = 96 * 1024;         // bytes of dynamic LDS per workgroup
-constexpr int kUnroll = 4;                    // key rows in flight per lane
+constexpr int kUnroll = 8;                    // key rows in flight per lane
 
 template <typename T, int D, int RC>
 __global__ __launch_bounds__(kThreads) void score_mean_logit_kernel(
@@ -45,14 +52,13 @@ __global__ __launch_bounds__(kThreads) void score_mean_logit_kernel(
     float* __restrict__ r_out, int H, int Hkv, int NT, int N, int group, int chunk,
     int nchunks, float qscale) {
     constexpr int LPR = D / 8;            // lanes per row (8 elements per lane)
-    constexpr int RPP = kThreads / LPR;   // rows per block-wide pass (phase A)
-    constexpr int RPW = kWave / LPR;      // rows per wave-wide load (phase B)
+    constexpr int RPW = kWave / LPR;      // rows per wave-wide load
     constexpr int STEP = kWaves * RPW;    // rows per block-wide load
 
     extern __shared__ float smem[];
     float* qbar = smem;                   // [RC][D]
-    float* part = qbar + RC * D;          // [RPP][D]
-    float* logits = part + RPP * D;       // [rc][N]
+    float* part = qbar + RC * D;          // [RC][kWaves][D]
+    float* logits = part + RC * kWaves * D;   // [rc][N]
 
     const int unit = blockIdx.x / nchunks;        // (b*L + l)*Hkv + g
     const int ci = blockIdx.x - unit * nchunks;
@@ -61,59 +67,77 @@ __global__ __launch_bounds__(kThreads) void score_mean_logit_kernel(
     const int hq0 = g * group + ci * chunk;       // first query head of this chunk
     const int rc = min(chunk, group - ci * chunk);
     const int tid = threadIdx.x;
+    const int wave = tid / kWave, lane = tid % kWave;
+    const int wrow = lane / LPR, wl = lane % LPR;
+    const T* kg = k + static_cast<int64_t>(unit) * N * D + wl * 8;
 
-    // ---- A: mean query per head --------------------------------------------
-    {
-        const int prow = tid / LPR, plane = tid % LPR;
-        for (int j = 0; j < rc; ++j) {
-            const T* qh = q + ((bl * H + hq0 + j) * NT) * D + plane * 8;
-            float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-            for (int t = prow; t < NT; t += RPP) {
-                Packet<T> p;
-                load_packet(p, qh + static_cast<int64_t>(t) * D);
-                float x[8];
-                unpack(p, x);
+    // Key rows past N are clamped to row N-1 (loads stay in bounds and branch-free);
+    // their products are discarded.
+    auto load_keys = [&](Packet<T> (&pk)[kUnroll], int base) {
 #pragma unroll
-                for (int m = 0; m < 8; ++m) acc[m] += x[m];
-            }
-#pragma unroll
-            for (int m = 0; m < 8; ++m) part[prow * D + plane * 8 + m] = acc[m];
-            __syncthreads();
-            if (tid < D) {
-                float s = 0.f;
-                for (int r = 0; r < RPP; ++r) s += part[r * D + tid];
-                qbar[j * D + tid] = s * qscale;
-            }
-            __syncthreads();
+        for (int u = 0; u < kUnroll; ++u) {
+            const int n = min(base + wrow + u * STEP, N - 1);
+            load_packet(pk[u], kg + static_cast<int64_t>(n) * D);
         }
+    };
+
+    // The first key rows do not depend on the query mean: start loading them now
+    // so that their latency overlaps phase A.
+    Packet<T> pk[kUnroll];
+    load_keys(pk, wave * RPW);
+
+    // ---- A: mean query per head (one barrier for all heads) -----------------
+    // Wave w sums rows w*RPW + wrow + i*STEP of every head, lane wl holding 8
+    // consecutive dims; the RPW row groups of a wave meet by shuffles, the waves
+    // in LDS.
+    {
+        constexpr int QU = 4;
+        for (int j = 0; j < rc; ++j) {
+            const T* qh = q + ((bl * H + hq0 + j) * NT) * D + wl * 8;
+            float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            for (int t = wave * RPW + wrow; t - wrow < NT; t += QU * STEP) {
+                Packet<T> p[QU];
+#pragma unroll
+                for (int u = 0; u < QU; ++u)
+                    load_packet(p[u], qh + static_cast<int64_t>(min(t + u * STEP, NT - 1)) * D);
+#pragma unroll
+                for (int u = 0; u < QU; ++u) {
+                    float x[8];
+                    unpack(p[u], x);
+                    const bool ok = t + u * STEP < NT;
+#pragma unroll
+                    for (int m = 0; m < 8; ++m) acc[m] += ok ? x[m] : 0.f;
+                }
+            }
+#pragma unroll
+            for (int m = 0; m < 8; ++m) {
+                for (int o = LPR; o < kWave; o <<= 1) acc[m] += __shfl_xor(acc[m], o);
+                if (wrow == 0) part[(j * kWaves + wave) * D + wl * 8 + m] = acc[m];
+            }
+        }
+        __syncthreads();
+        for (int i = tid; i < rc * D; i += kThreads) {
+            const int j = i / D, dd = i - j * D;
+            const float* pj = part + j * kWaves * D + dd;
+            qbar[i] = (((pj[0] + pj[D]) + pj[2 * D]) + pj[3 * D]) * qscale;
+        }
+        __syncthreads();
     }
 
     // ---- B: logits a[h, n] --------------------------------------------------
-    const int wave = tid / kWave, lane = tid % kWave;
-    const int wrow = lane / LPR, wl = lane % LPR;
     float qb[RC][8];
 #pragma unroll
     for (int j = 0; j < RC; ++j)
 #pragma unroll
         for (int m = 0; m < 8; ++m) qb[j][m] = (j < rc) ? qbar[j * D + wl * 8 + m] : 0.f;
 
-    const T* kg = k + static_cast<int64_t>(unit) * N * D + wl * 8;
     for (int base = wave * RPW; base < N; base += STEP * kUnroll) {
-        Packet<T> p[kUnroll];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const int n = base + wrow + u * STEP;
-            if (n < N) {
-                load_packet(p[u], kg + static_cast<int64_t>(n) * D);
-            } else {
-                p[u] = Packet<T>{};
-            }
-        }
+        if (base != wave * RPW) load_keys(pk, base);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             const int n = base + wrow + u * STEP;
             float x[8];
-            unpack(p[u], x);
+            unpack(pk[u], x);
 #pragma unroll
             for (int j = 0; j < RC; ++j) {
                 if (j < rc) {
@@ -128,8 +152,47 @@ __global__ __launch_bounds__(kThreads) void score_mean_logit_kernel(
     }
     __syncthreads();
 
-    // ---- C, D: centred softmax and support, one wave per head ---------------
+    // ---- C, D: centred softmax and support -----------------------------------
     const float fN = static_cast<float>(N);
+    if (rc == 1) {
+        // a single head: the whole workgroup shares it
+        float* a = logits;
+        __shared__ float red[3 * kWaves];
+        float m = -INFINITY;
+        for (int n = tid; n < N; n += kThreads) m = fmaxf(m, a[n]);
+        m = wave_max(m);
+        if (lane == 0) red[wave] = m;
+        __syncthreads();
+        m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+        float E = 0.f, S = 0.f;
+        for (int n = tid; n < N; n += kThreads) {
+            const float d = a[n] - m;
+            a[n] = d;
+            E += expm1f(d);
+            S += expf(d);
+        }
+        E = wave_sum(E);
+        S = wave_sum(S);
+        if (lane == 0) {
+            red[kWaves + wave] = E;
+            red[2 * kWaves + wave] = S;
+        }
+        __syncthreads();
+        E = ((red[kWaves] + red[kWaves + 1]) + red[kWaves + 2]) + red[kWaves + 3];
+        S = ((red[2 * kWaves] + red[2 * kWaves + 1]) + red[2 * kWaves + 2]) + red[2 * kWaves + 3];
+        const float lse = log_mean_exp(E, S, fN);
+        const int64_t row = (bl * H + hq0) * static_cast<int64_t>(N);
+        float* eo = e_out + row;
+        float* ro = r_out ? r_out + row : nullptr;
+        for (int n = tid; n < N; n += kThreads) {
+            const float dc = a[n] - lse;
+            const float u = expm1f(dc);
+            __builtin_nontemporal_store(u / (2.0f * (2.0f + u)), eo + n);
+            if (ro) ro[n] = expf(dc) / fN;
+        }
+        return;
+    }
+    // several heads: one wave per head
     for (int j = wave; j < rc; j += kWaves) {
         float* a = logits + j * N;
         float m = -INFINITY;
@@ -151,7 +214,7 @@ __global__ __launch_bounds__(kThreads) void score_mean_logit_kernel(
         for (int n = lane; n < N; n += kWave) {
             const float dc = a[n] - lse;
             const float u = expm1f(dc);
-            eo[n] = u / (2.0f * (2.0f + u));
+            __builtin_nontemporal_store(u / (2.0f * (2.0f + u)), eo + n);
             if (ro) ro[n] = expf(dc) / fN;
         }
     }
@@ -160,8 +223,7 @@ __global__ __launch_bounds__(kThreads) void score_mean_logit_kernel(
 template <typename T, int D, int RC>
 hipError_t launch_ml(const Dims& d, float qscale, const void* q, const void* k, float* e,
                      float* r, int chunk, int nchunks, hipStream_t st) {
-    constexpr int RPP = kThreads / (D / 8);
-    const size_t lds = (static_cast<size_t>(RC) * D + static_cast<size_t>(RPP) * D +
+    const size_t lds = (static_cast<size_t>(RC) * D * (1 + kWaves) +
                         static_cast<size_t>(chunk) * d.N) * sizeof(float);
     auto kern = score_mean_logit_kernel<T, D, RC>;
     if (lds > 64 * 1024) {
@@ -181,8 +243,7 @@ hipError_t launch_ml(const Dims& d, float qscale, const void* q, const void* k, 
 template <typename T, int D>
 hipError_t dispatch_rc(const Dims& d, float qscale, const void* q, const void* k, float* e,
                        float* r, hipStream_t st) {
-    constexpr int RPP = kThreads / (D / 8);
-    const int64_t fixed = (static_cast<int64_t>(kMaxChunk) * D + RPP * D) * 4;
+    const int64_t fixed = static_cast<int64_t>(kMaxChunk) * D * (1 + kWaves) * 4;
     int64_t fit = (kLdsBudget - fixed) / (d.N * 4);
     if (fit < 1) fit = 1;
     int chunk = static_cast<int>(std::min<int64_t>({d.group, kMaxChunk, fit}));

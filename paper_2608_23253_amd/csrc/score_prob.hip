@@ -317,7 +317,7 @@ __global__ __launch_bounds__(kThreads) void score_mean_prob_kernel(
     const float inv_nt = 1.0f / static_cast<float>(NT);
     for (int n = tid; n < N; n += kThreads) {
         const float u = colsum[n] * inv_nt;
-        e_out[row + n] = u / (2.0f * (2.0f + u));
+        __builtin_nontemporal_store(u / (2.0f * (2.0f + u)), e_out + row + n);
         if (r_out) r_out[row + n] = (1.0f + u) / fN;
     }
 }

@@ -8,9 +8,11 @@
 //  3. adjusted complement c^ = (1 - lambda) c + lambda (1 - b) = 1 - q~ (Eq. 22),
 //     evaluated in double precision with explicitly rounded operations; its
 //     order-preserving 64-bit image is the ranking key;
-//  4. the K-th smallest key T is found by an 8-round radix select over 8-bit
-//     digits (LDS histogram + one wave's prefix scan per round), together with
-//     how many tokens equal to T must still be taken;
+//  4. the K-th smallest key T is found by a radix select over 8-bit digits (LDS
+//     histogram + one wave's prefix scan per round, at most 8 rounds, fewer once
+//     T's bin holds a single key), together with how many tokens equal to T must
+//     still be taken; lanes of a wave that fall in the same bin are added with one
+//     atomic;
 //  5. tokens with key < T, plus the lowest-index tokens with key == T, are kept
 //     (Eq. 23); two block-wide scans in token order write them in ascending order.
 //
@@ -76,6 +78,8 @@ __global__ __launch_bounds__(THREADS) void spatial_select_kernel(
     uint8_t* rep = reinterpret_cast<uint8_t*>(scan + 32);       // [N]
     __shared__ uint64_t s_prefix;
     __shared__ uint32_t s_rank;
+    __shared__ uint32_t s_unique;
+    __shared__ uint64_t s_found;
 
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     const int64_t b = blockIdx.x;
@@ -123,16 +127,41 @@ __global__ __launch_bounds__(THREADS) void spatial_select_kernel(
     if (tid == 0) {
         s_prefix = 0;
         s_rank = static_cast<uint32_t>(K);
+        s_unique = 0;
     }
     uint64_t mask = 0;
     for (int shift = 56; shift >= 0; shift -= 8) {
         for (int i = tid; i < 256; i += THREADS) hist[i] = 0;
         __syncthreads();
         const uint64_t prefix = s_prefix;
-        for (int n = tid; n < N; n += THREADS) {
-            const uint64_t kk = ordered_bits(adj(n));
-            if ((kk & mask) == prefix)
-                atomicAdd(&hist[static_cast<uint32_t>(kk >> shift) & 255u], 1u);
+        if (s_unique) {
+            // the previous round left one key with this prefix: it is the K-th key
+            for (int n = tid; n < N; n += THREADS) {
+                const uint64_t kk = ordered_bits(adj(n));
+                if ((kk & mask) == prefix) s_found = kk;
+            }
+            __syncthreads();
+            if (tid == 0) s_prefix = s_found;
+            __syncthreads();
+            break;
+        }
+        for (int base = 0; base < N; base += THREADS) {
+            const int n = base + tid;
+            const uint64_t kk = n < N ? ordered_bits(adj(n)) : 0ull;
+            const bool match = n < N && (kk & mask) == prefix;
+            const uint32_t digit = static_cast<uint32_t>(kk >> shift) & 255u;
+            // early rounds put most keys of a wave in one bin: add them with one atomic
+            const uint64_t mb = __ballot(match);
+            if (mb) {
+                const int leader = __ffsll(static_cast<unsigned long long>(mb)) - 1;
+                const uint32_t d0 = __shfl(digit, leader);
+                const uint64_t same = __ballot(match && digit == d0);
+                if (same == mb) {
+                    if (lane == leader) atomicAdd(&hist[d0], static_cast<uint32_t>(__popcll(mb)));
+                } else if (match) {
+                    atomicAdd(&hist[digit], 1u);
+                }
+            }
         }
         __syncthreads();
         if (wave == 0) {
@@ -160,6 +189,7 @@ __global__ __launch_bounds__(THREADS) void spatial_select_kernel(
                 }
                 s_prefix = prefix | (static_cast<uint64_t>(digit) << shift);
                 s_rank = rank - cum;
+                s_unique = hist[digit] == 1u;
             }
         }
         mask |= 0xFFull << shift;

@@ -67,6 +67,7 @@ def test_status_strings():
     ("head_dim", 0, L.ERR_BAD_SHAPE), ("num_text", 0, L.ERR_BAD_SHAPE),
     ("grid_h", 0, L.ERR_BAD_SHAPE), ("grid_w", -1, L.ERR_BAD_SHAPE),
     ("grid_h", 200, L.ERR_UNSUPPORTED),          # with grid_w = 100: N = 20000 > 16384
+    ("num_heads", 130, L.ERR_UNSUPPORTED),       # with num_kv_heads = 2: H > 128
 ])
 def test_bad_shapes(field, value, expect):
     kw = {field: value}

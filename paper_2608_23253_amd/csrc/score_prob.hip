@@ -4,23 +4,31 @@
 //
 // Unlike the mean-of-logits reading this is a genuine dense contraction
 // (N_T x N_V logits per head), computed on the matrix cores with
-// v_mfma_f32_16x16x32_bf16 (bf16 storage) or v_mfma_f32_16x16x4_f32 (fp32 storage),
-// fp32 accumulation.  One workgroup owns one (image, layer, query head); its text
-// queries (in chunks of up to 128 rows) are staged in LDS, and the key tiles of 16
-// rows are loaded straight into MFMA operand registers.  Two passes over the keys:
+// v_mfma_f32_16x16x32_bf16 (bf16 storage) or v_mfma_f32_16x16x4_f32 (fp32
+// storage), fp32 accumulation.  One workgroup owns one (image, layer, query head).
+// Its text queries (chunks of up to 128 rows) are staged in LDS as the B operand;
+// key tiles of 16 rows are loaded from HBM straight into A-operand registers, so a
+// 16x16 result tile holds 16 keys (4 per lane) x 16 queries (one per lane).  Two
+// passes over the keys:
 //
-//   pass 1  online row statistics per query: m_t = max_n z, S_t = sum exp(z - m_t)
-//           and E_t = sum expm1(z - m_t), merged across lanes and waves, then the
-//           centring constant L_t = log(S_t / N)            (as in the other reading)
-//   pass 2  per key column: sum over queries of  N P[t,n] - 1 = expm1(z - m_t - L_t)
+//   pass 1  online row statistics of the lane's query: m_t = max_n z,
+//           S_t = sum exp(z - m_t), E_t = sum expm1(z - m_t); merged across the
+//           lanes and waves that saw other keys, then the centring constant
+//           L_t = log(S_t / N)                               (as in the other reading)
+//   pass 2  per key: sum over queries of  N P[t,n] - 1 = expm1(z - m_t - L_t),
+//           accumulated in-lane over all query blocks, then summed across the 16
+//           query lanes of a DPP row
 //
 // so u_n = N r_n - 1 = (1/N_T) sum_t expm1(z[t,n] - m_t - L_t) is accumulated in
-// centred form, e_n = u_n / (2 (2 + u_n)), r_n = (1 + u_n) / N.
+// centred form; e_n = u_n / (2 (2 + u_n)), r_n = (1 + u_n) / N.
+//
+// expm1 of the small centred logits uses a short Taylor series; the library's
+// expf takes over only in waves where some |x| exceeds 1/2 (peaked attention).
 //
 // Query heads that share a key head (grouped-query attention) run in workgroups
 // with consecutive logical ids; the ids are remapped so that those workgroups land
-// on the same XCD (blocks are dispatched round-robin over the 8 XCDs) and the
-// second pass re-reads the keys from that XCD's L2.
+// on the same XCD (blocks are dispatched round-robin over the 8 XCDs) and re-read
+// the shared keys from that XCD's L2.
 #include <type_traits>
 
 #include "e2s_device.h"
@@ -41,75 +49,110 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
     return x * q + min(x, r) + i;
 }
 
-// Per-type tiling: bf16 keeps 4 key tiles in flight, fp32 (wider operands) 2.
+// expm1 on [-1/2, 1/2]: Taylor series to degree 8 (truncation below 6e-9 there).
+__device__ __forceinline__ float expm1_series(float x) {
+    float p = 1.0f / 40320.0f;
+    p = fmaf(p, x, 1.0f / 5040.0f);
+    p = fmaf(p, x, 1.0f / 720.0f);
+    p = fmaf(p, x, 1.0f / 120.0f);
+    p = fmaf(p, x, 1.0f / 24.0f);
+    p = fmaf(p, x, 1.0f / 6.0f);
+    p = fmaf(p, x, 0.5f);
+    p = fmaf(p, x, 1.0f);
+    return p * x;
+}
+
+// t = expm1(x) and w = exp(x); outside [-1/2, 1/2] both come from expf (then
+// exp(x) - 1 loses at most ~1.5 bits).  Called with every lane of the wave active.
+__device__ __forceinline__ void exp_pair(float x, float& t, float& w) {
+    t = expm1_series(x);
+    w = 1.0f + t;
+    const bool far = fabsf(x) > 0.5f;
+    if (__any(far)) {
+        if (far) {
+            w = expf(x);
+            t = w - 1.0f;
+        }
+    }
+}
+__device__ __forceinline__ float expm1_fast(float x) {
+    float t = expm1_series(x);
+    const bool far = fabsf(x) > 0.5f;
+    if (__any(far)) {
+        if (far) t = expf(x) - 1.0f;
+    }
+    return t;
+}
+
 template <typename T, int D> struct ProbCfg;
 template <int D> struct ProbCfg<uint16_t, D> {
     static constexpr int QC = 128;           // query rows per LDS chunk
-    static constexpr int TG = 4;             // key tiles per statistics update
+    static constexpr int TG = 4;             // key tiles per wave iteration
     static constexpr int QS = D + 8;         // padded LDS row (elements)
+    static constexpr int NA = D / 32;        // A registers (bf16x8) per key tile
+    using AFrag = bf16x8;
 };
 template <int D> struct ProbCfg<float, D> {
     static constexpr int QC = 64;
     static constexpr int TG = 2;
     static constexpr int QS = D + 4;
+    static constexpr int NA = D / 4;
+    using AFrag = float;
 };
 
-// B operand (keys) of one 16-key tile for all k steps.
+// A operand (keys) of one 16-key tile for all k steps.
 //   bf16: lane (lr, lg) holds key lr, elements 32 s + 8 lg .. +7 of step s.
 //   fp32: lane holds key lr, element d(s, lg) = 16 (s/4) + 4 lg + s%4 of step s.
-// The A operand (queries) uses the same element mapping, so every product pairs
-// Q[t, d] with K[n, d].
+// The B operand (queries, from LDS) uses the same element mapping.
 template <int NS>
-__device__ __forceinline__ void load_b(bf16x8 (&b)[NS], const uint16_t* row, bool valid) {
+__device__ __forceinline__ void load_keys(bf16x8 (&a)[NS], const uint16_t* row, bool valid) {
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-        if (valid) {
-            b[s] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(row + 32 * s));
-        } else {
-            b[s] = bf16x8{};
-        }
-    }
+    for (int s = 0; s < NS; ++s)
+        a[s] = valid ? __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(row + 32 * s))
+                     : bf16x8{};
 }
 template <int NS>
-__device__ __forceinline__ void load_b_f32(float (&b)[NS], const float* row, bool valid) {
+__device__ __forceinline__ void load_keys(float (&a)[NS], const float* row, bool valid) {
 #pragma unroll
     for (int t = 0; t < NS / 4; ++t) {
-        f32x4v v = valid ? __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(row + 16 * t))
-                         : f32x4v{0.f, 0.f, 0.f, 0.f};
-        b[4 * t + 0] = v.x;
-        b[4 * t + 1] = v.y;
-        b[4 * t + 2] = v.z;
-        b[4 * t + 3] = v.w;
+        const f32x4v v = valid
+            ? __builtin_nontemporal_load(reinterpret_cast<const f32x4v*>(row + 16 * t))
+            : f32x4v{0.f, 0.f, 0.f, 0.f};
+        a[4 * t + 0] = v.x;
+        a[4 * t + 1] = v.y;
+        a[4 * t + 2] = v.z;
+        a[4 * t + 3] = v.w;
     }
 }
 
-// One 16x16 logit tile (16 queries of block qb x 16 keys) into acc.
+// 16 keys x 16 queries of query block qrow..qrow+15: lane (lr, lg) gets the
+// logits of keys 4 lg + r (r = 0..3) against query qrow + lr.
 template <int D>
-__device__ __forceinline__ f32x4v tile_mma(const uint16_t* qs, int qrow, int lg,
-                                           const bf16x8 (&b)[D / 32]) {
+__device__ __forceinline__ f32x4v tile_mma(const bf16x8 (&a)[D / 32], const uint16_t* qs,
+                                           int qrow, int lr, int lg) {
     constexpr int QS = D + 8;
     f32x4v acc = {0.f, 0.f, 0.f, 0.f};
-    const uint16_t* arow = qs + qrow * QS + 8 * lg;
+    const uint16_t* brow = qs + (qrow + lr) * QS + 8 * lg;
 #pragma unroll
     for (int s = 0; s < D / 32; ++s) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(arow + 32 * s);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[s], acc, 0, 0, 0);
+        const bf16x8 b = *reinterpret_cast<const bf16x8*>(brow + 32 * s);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s], b, acc, 0, 0, 0);
     }
     return acc;
 }
 template <int D>
-__device__ __forceinline__ f32x4v tile_mma(const float* qs, int qrow, int lg,
-                                           const float (&b)[D / 4]) {
+__device__ __forceinline__ f32x4v tile_mma(const float (&a)[D / 4], const float* qs, int qrow,
+                                           int lr, int lg) {
     constexpr int QS = D + 4;
     f32x4v acc = {0.f, 0.f, 0.f, 0.f};
-    const float* arow = qs + qrow * QS + 4 * lg;
+    const float* brow = qs + (qrow + lr) * QS + 4 * lg;
 #pragma unroll
     for (int t = 0; t < D / 16; ++t) {
-        const f32x4v a = *reinterpret_cast<const f32x4v*>(arow + 16 * t);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b[4 * t + 0], acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b[4 * t + 1], acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b[4 * t + 2], acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b[4 * t + 3], acc, 0, 0, 0);
+        const f32x4v b = *reinterpret_cast<const f32x4v*>(brow + 16 * t);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[4 * t + 0], b.x, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[4 * t + 1], b.y, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[4 * t + 2], b.z, acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[4 * t + 3], b.w, acc, 0, 0, 0);
     }
     return acc;
 }
@@ -120,9 +163,8 @@ __global__ __launch_bounds__(kThreads) void score_mean_prob_kernel(
     float* __restrict__ r_out, int H, int NT, int N, int group, int Hkv, float scale,
     int nblocks) {
     using C = ProbCfg<T, D>;
-    constexpr int QC = C::QC, TG = C::TG, QS = C::QS, QBM = QC / 16;
-    constexpr int NB = std::is_same<T, float>::value ? D / 4 : D / 32;  // B regs per tile
-    using BFrag = typename std::conditional<std::is_same<T, float>::value, float, bf16x8>::type;
+    constexpr int QC = C::QC, TG = C::TG, QS = C::QS, QBM = QC / 16, NA = C::NA;
+    using AFrag = typename C::AFrag;
 
     extern __shared__ __align__(16) unsigned char smem[];
     T* qs = reinterpret_cast<T*>(smem);                          // [QC][QS]
@@ -142,6 +184,7 @@ __global__ __launch_bounds__(kThreads) void score_mean_prob_kernel(
     const int ntiles = (N + 15) / 16;
     const int ngroups = (ntiles + TG - 1) / TG;
     const float fN = static_cast<float>(N);
+    const int koff = std::is_same<T, float>::value ? 4 * lg : 8 * lg;
 
     for (int n = tid; n < N; n += kThreads) colsum[n] = 0.f;
 
@@ -161,94 +204,95 @@ __global__ __launch_bounds__(kThreads) void score_mean_prob_kernel(
         }
         __syncthreads();
 
-        // ---- pass 1: online statistics of each query row --------------------
-        float m[QBM][4], E[QBM][4], S[QBM][4];
+        // ---- pass 1: online statistics of this lane's query in each block ----
+        float m[QBM], E[QBM], S[QBM];
 #pragma unroll
-        for (int i = 0; i < QBM; ++i)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                m[i][r] = -INFINITY;
-                E[i][r] = 0.f;
-                S[i][r] = 0.f;
-            }
+        for (int i = 0; i < QBM; ++i) {
+            m[i] = -INFINITY;
+            E[i] = 0.f;
+            S[i] = 0.f;
+        }
         float cnt = 0.f;                                          // valid keys seen by this lane
         for (int gi = wave; gi < ngroups; gi += kWaves) {
-            BFrag b[TG][NB];
-            bool valid[TG];
+            AFrag a[TG][NA];
+            bool kval[TG][4];
 #pragma unroll
             for (int tt = 0; tt < TG; ++tt) {
-                const int key = (gi * TG + tt) * 16 + lr;
-                valid[tt] = key < N;
-                if constexpr (std::is_same<T, float>::value)
-                    load_b_f32<NB>(b[tt], kg + static_cast<int64_t>(key) * D + 4 * lg, valid[tt]);
-                else
-                    load_b<NB>(b[tt], kg + static_cast<int64_t>(key) * D + 8 * lg, valid[tt]);
+                const int tile = gi * TG + tt;
+                const int key = tile * 16 + lr;
+                load_keys<NA>(a[tt], kg + static_cast<int64_t>(min(key, N - 1)) * D + koff,
+                              key < N);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) kval[tt][r] = tile * 16 + 4 * lg + r < N;
             }
 #pragma unroll
             for (int qb = 0; qb < QBM; ++qb) {
                 if (qb < QB) {
-                    f32x4v z[TG];
+                    float v[TG][4];
+                    float mx = m[qb];
 #pragma unroll
-                    for (int tt = 0; tt < TG; ++tt) z[tt] = tile_mma<D>(qs, qb * 16 + lr, lg, b[tt]);
+                    for (int tt = 0; tt < TG; ++tt) {
+                        const f32x4v z = tile_mma<D>(a[tt], qs, qb * 16, lr, lg);
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        float v[TG];
-                        float mx = m[qb][r];
-#pragma unroll
-                        for (int tt = 0; tt < TG; ++tt) {
-                            v[tt] = valid[tt] ? z[tt][r] * scale : -INFINITY;
-                            mx = fmaxf(mx, v[tt]);
-                        }
-                        if (__any(mx > m[qb][r])) {
-                            // rescale the sums to the new maximum (exact no-op where unchanged)
-                            const float dm = (mx > m[qb][r]) ? m[qb][r] - mx : 0.f;
-                            const float sc = expf(dm);
-                            const float em = (cnt > 0.f) ? expm1f(dm) : 0.f;
-                            E[qb][r] = fmaf(cnt, em, E[qb][r] * sc);
-                            S[qb][r] = S[qb][r] * sc;
-                            m[qb][r] = mx;
-                        }
-#pragma unroll
-                        for (int tt = 0; tt < TG; ++tt) {
-                            if (valid[tt]) {
-                                const float d = v[tt] - mx;
-                                E[qb][r] += expm1f(d);
-                                S[qb][r] += expf(d);
-                            }
+                        for (int r = 0; r < 4; ++r) {
+                            v[tt][r] = kval[tt][r] ? z[r] * scale : -INFINITY;
+                            mx = fmaxf(mx, v[tt][r]);
                         }
                     }
+                    if (__any(mx > m[qb])) {
+                        // rescale the sums to the new maximum (exact no-op where unchanged)
+                        const float dm = (mx > m[qb]) ? m[qb] - mx : 0.f;
+                        const float sc = expf(dm);
+                        const float em = (cnt > 0.f) ? expm1f(dm) : 0.f;
+                        E[qb] = fmaf(cnt, em, E[qb] * sc);
+                        S[qb] = S[qb] * sc;
+                        m[qb] = mx;
+                    }
+#pragma unroll
+                    for (int tt = 0; tt < TG; ++tt)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            float t, w;
+                            exp_pair(kval[tt][r] ? v[tt][r] - mx : 0.f, t, w);
+                            if (kval[tt][r]) {
+                                E[qb] += t;
+                                S[qb] += w;
+                            }
+                        }
                 }
             }
 #pragma unroll
-            for (int tt = 0; tt < TG; ++tt) cnt += valid[tt] ? 1.f : 0.f;
+            for (int tt = 0; tt < TG; ++tt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) cnt += kval[tt][r] ? 1.f : 0.f;
         }
 
-        // ---- merge statistics: 16 lanes per row group, then the 4 waves ----
+        // ---- merge statistics: the 4 lane groups of a wave, then the waves ----
 #pragma unroll
         for (int qb = 0; qb < QBM; ++qb) {
             if (qb < QB) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    float M = m[qb][r];
-                    for (int o = 1; o < 16; o <<= 1) M = fmaxf(M, __shfl_xor(M, o));
-                    float e = 0.f, s = 0.f, c = cnt;
-                    if (cnt > 0.f) {
-                        const float dm = m[qb][r] - M;
-                        e = fmaf(cnt, expm1f(dm), E[qb][r] * expf(dm));
-                        s = S[qb][r] * expf(dm);
-                    }
-                    for (int o = 1; o < 16; o <<= 1) {
-                        e += __shfl_xor(e, o);
-                        s += __shfl_xor(s, o);
-                        c += __shfl_xor(c, o);
-                    }
-                    if (lr == 0) {
-                        float* w = wpart + (wave * QC + qb * 16 + 4 * lg + r) * 4;
-                        w[0] = (c > 0.f) ? M : -INFINITY;
-                        w[1] = e;
-                        w[2] = s;
-                        w[3] = c;
-                    }
+                float M = m[qb];
+                M = fmaxf(M, __shfl_xor(M, 16));
+                M = fmaxf(M, __shfl_xor(M, 32));
+                float e = 0.f, s = 0.f;
+                if (cnt > 0.f) {
+                    const float dm = m[qb] - M;
+                    e = fmaf(cnt, expm1f(dm), E[qb] * expf(dm));
+                    s = S[qb] * expf(dm);
+                }
+                float c = cnt;
+                e += __shfl_xor(e, 16);
+                s += __shfl_xor(s, 16);
+                c += __shfl_xor(c, 16);
+                e += __shfl_xor(e, 32);
+                s += __shfl_xor(s, 32);
+                c += __shfl_xor(c, 32);
+                if (lg == 0) {
+                    float* w = wpart + (wave * QC + qb * 16 + lr) * 4;
+                    w[0] = (c > 0.f) ? M : -INFINITY;
+                    w[1] = e;
+                    w[2] = s;
+                    w[3] = c;
                 }
             }
         }
@@ -269,46 +313,50 @@ __global__ __launch_bounds__(kThreads) void score_mean_prob_kernel(
         }
         __syncthreads();
 
-        // ---- pass 2: column sums of N P - 1 = expm1(z - m - L) --------------
+        // ---- pass 2: per key, sum over queries of expm1(z - m - L) ----------
+        float qm[QBM], ql[QBM];
+        bool qval[QBM];
+#pragma unroll
+        for (int qb = 0; qb < QBM; ++qb) {
+            qm[qb] = st_m[qb * 16 + lr];
+            ql[qb] = st_l[qb * 16 + lr];
+            qval[qb] = qb * 16 + lr < rows;
+        }
         for (int gi = wave; gi < ngroups; gi += kWaves) {
-            BFrag b[TG][NB];
-            bool valid[TG];
+            AFrag a[TG][NA];
 #pragma unroll
             for (int tt = 0; tt < TG; ++tt) {
                 const int key = (gi * TG + tt) * 16 + lr;
-                valid[tt] = key < N;
-                if constexpr (std::is_same<T, float>::value)
-                    load_b_f32<NB>(b[tt], kg + static_cast<int64_t>(key) * D + 4 * lg, valid[tt]);
-                else
-                    load_b<NB>(b[tt], kg + static_cast<int64_t>(key) * D + 8 * lg, valid[tt]);
+                load_keys<NA>(a[tt], kg + static_cast<int64_t>(min(key, N - 1)) * D + koff,
+                              key < N);
             }
-            float col[TG];
+            float col[TG][4];
 #pragma unroll
-            for (int tt = 0; tt < TG; ++tt) col[tt] = 0.f;
+            for (int tt = 0; tt < TG; ++tt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) col[tt][r] = 0.f;
 #pragma unroll
             for (int qb = 0; qb < QBM; ++qb) {
                 if (qb < QB) {
-                    const int row0 = qb * 16 + 4 * lg;
-                    const f32x4v mm = *reinterpret_cast<const f32x4v*>(st_m + row0);
-                    const f32x4v ll = *reinterpret_cast<const f32x4v*>(st_l + row0);
 #pragma unroll
                     for (int tt = 0; tt < TG; ++tt) {
-                        const f32x4v z = tile_mma<D>(qs, qb * 16 + lr, lg, b[tt]);
+                        const f32x4v z = tile_mma<D>(a[tt], qs, qb * 16, lr, lg);
 #pragma unroll
                         for (int r = 0; r < 4; ++r) {
-                            if (row0 + r < rows)
-                                col[tt] += expm1f((z[r] * scale - mm[r]) - ll[r]);
+                            const float t = expm1_fast((z[r] * scale - qm[qb]) - ql[qb]);
+                            col[tt][r] += qval[qb] ? t : 0.f;
                         }
                     }
                 }
             }
 #pragma unroll
-            for (int tt = 0; tt < TG; ++tt) {
-                col[tt] += __shfl_xor(col[tt], 16);
-                col[tt] += __shfl_xor(col[tt], 32);
-                const int key = (gi * TG + tt) * 16 + lr;
-                if (lg == 0 && valid[tt]) colsum[key] += col[tt];
-            }
+            for (int tt = 0; tt < TG; ++tt)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float sum = group_sum<16>(col[tt][r]);
+                    const int key = (gi * TG + tt) * 16 + 4 * lg + r;
+                    if (lr == 0 && key < N) colsum[key] += sum;
+                }
         }
     }
     __syncthreads();

@@ -22,8 +22,11 @@
 // so u_n = N r_n - 1 = (1/N_T) sum_t expm1(z[t,n] - m_t - L_t) is accumulated in
 // centred form; e_n = u_n / (2 (2 + u_n)), r_n = (1 + u_n) / N.
 //
-// expm1 of the small centred logits uses a short Taylor series; the library's
-// expf takes over only in waves where some |x| exceeds 1/2 (peaked attention).
+// expm1 of the small centred logits uses a degree-5 Taylor series on |x| <= 1/8;
+// the library's expm1f / expf take over for a batch of 16 logits only when some
+// lane of the wave has one outside that range (peaked attention).
+// The query-block loops are not unrolled (the per-lane statistics live in LDS),
+// which keeps the kernel's code within the instruction cache.
 //
 // Query heads that share a key head (grouped-query attention) run in workgroups
 // with consecutive logical ids; the ids are remapped so that those workgroups land
@@ -49,39 +52,16 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
     return x * q + min(x, r) + i;
 }
 
-// expm1 on [-1/2, 1/2]: Taylor series to degree 8 (truncation below 6e-9 there).
+// expm1 on [-1/8, 1/8]: Taylor series to degree 5 (truncation below 6e-9, i.e.
+// under one float32 ulp of the result, there).
+constexpr float kSeriesRange = 0.125f;
 __device__ __forceinline__ float expm1_series(float x) {
-    float p = 1.0f / 40320.0f;
-    p = fmaf(p, x, 1.0f / 5040.0f);
-    p = fmaf(p, x, 1.0f / 720.0f);
-    p = fmaf(p, x, 1.0f / 120.0f);
+    float p = 1.0f / 120.0f;
     p = fmaf(p, x, 1.0f / 24.0f);
     p = fmaf(p, x, 1.0f / 6.0f);
     p = fmaf(p, x, 0.5f);
     p = fmaf(p, x, 1.0f);
     return p * x;
-}
-
-// t = expm1(x) and w = exp(x); outside [-1/2, 1/2] both come from expf (then
-// exp(x) - 1 loses at most ~1.5 bits).  Called with every lane of the wave active.
-__device__ __forceinline__ void exp_pair(float x, float& t, float& w) {
-    t = expm1_series(x);
-    w = 1.0f + t;
-    const bool far = fabsf(x) > 0.5f;
-    if (__any(far)) {
-        if (far) {
-            w = expf(x);
-            t = w - 1.0f;
-        }
-    }
-}
-__device__ __forceinline__ float expm1_fast(float x) {
-    float t = expm1_series(x);
-    const bool far = fabsf(x) > 0.5f;
-    if (__any(far)) {
-        if (far) t = expf(x) - 1.0f;
-    }
-    return t;
 }
 
 template <typename T, int D> struct ProbCfg;
@@ -125,35 +105,43 @@ __device__ __forceinline__ void load_keys(float (&a)[NS], const float* row, bool
     }
 }
 
-// 16 keys x 16 queries of query block qrow..qrow+15: lane (lr, lg) gets the
-// logits of keys 4 lg + r (r = 0..3) against query qrow + lr.
+// Query operand (B) of one 16-query block, all k steps, read from LDS once and
+// reused for every key tile.  Same element mapping as the keys.
 template <int D>
-__device__ __forceinline__ f32x4v tile_mma(const bf16x8 (&a)[D / 32], const uint16_t* qs,
-                                           int qrow, int lr, int lg) {
-    constexpr int QS = D + 8;
-    f32x4v acc = {0.f, 0.f, 0.f, 0.f};
-    const uint16_t* brow = qs + (qrow + lr) * QS + 8 * lg;
+__device__ __forceinline__ void load_queries(bf16x8 (&b)[D / 32], const uint16_t* qs, int qrow,
+                                             int lr, int lg) {
+    const uint16_t* brow = qs + (qrow + lr) * (D + 8) + 8 * lg;
 #pragma unroll
-    for (int s = 0; s < D / 32; ++s) {
-        const bf16x8 b = *reinterpret_cast<const bf16x8*>(brow + 32 * s);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s], b, acc, 0, 0, 0);
-    }
-    return acc;
+    for (int s = 0; s < D / 32; ++s) b[s] = *reinterpret_cast<const bf16x8*>(brow + 32 * s);
 }
 template <int D>
-__device__ __forceinline__ f32x4v tile_mma(const float (&a)[D / 4], const float* qs, int qrow,
-                                           int lr, int lg) {
-    constexpr int QS = D + 4;
-    f32x4v acc = {0.f, 0.f, 0.f, 0.f};
-    const float* brow = qs + (qrow + lr) * QS + 4 * lg;
+__device__ __forceinline__ void load_queries(float (&b)[D / 4], const float* qs, int qrow, int lr,
+                                             int lg) {
+    const float* brow = qs + (qrow + lr) * (D + 4) + 4 * lg;
 #pragma unroll
     for (int t = 0; t < D / 16; ++t) {
-        const f32x4v b = *reinterpret_cast<const f32x4v*>(brow + 16 * t);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[4 * t + 0], b.x, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[4 * t + 1], b.y, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[4 * t + 2], b.z, acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[4 * t + 3], b.w, acc, 0, 0, 0);
+        const f32x4v v = *reinterpret_cast<const f32x4v*>(brow + 16 * t);
+        b[4 * t + 0] = v.x;
+        b[4 * t + 1] = v.y;
+        b[4 * t + 2] = v.z;
+        b[4 * t + 3] = v.w;
     }
+}
+
+// 16 keys x 16 queries: lane (lr, lg) gets the logits of keys 4 lg + r (r = 0..3)
+// against query lr of the block.
+template <int NA>
+__device__ __forceinline__ f32x4v tile_mma(const bf16x8 (&a)[NA], const bf16x8 (&b)[NA]) {
+    f32x4v acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < NA; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s], b[s], acc, 0, 0, 0);
+    return acc;
+}
+template <int NA>
+__device__ __forceinline__ f32x4v tile_mma(const float (&a)[NA], const float (&b)[NA]) {
+    f32x4v acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < NA; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s], acc, 0, 0, 0);
     return acc;
 }
 
@@ -161,17 +149,19 @@ template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void score_mean_prob_kernel(
     const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
     float* __restrict__ r_out, int H, int NT, int N, int group, int Hkv, float scale,
-    int nblocks) {
+    int nblocks, int qcap) {
     using C = ProbCfg<T, D>;
-    constexpr int QC = C::QC, TG = C::TG, QS = C::QS, QBM = QC / 16, NA = C::NA;
+    constexpr int TG = C::TG, QS = C::QS, NA = C::NA;
     using AFrag = typename C::AFrag;
 
     extern __shared__ __align__(16) unsigned char smem[];
-    T* qs = reinterpret_cast<T*>(smem);                          // [QC][QS]
-    float* st_m = reinterpret_cast<float*>(qs + QC * QS);        // [QC] row max
-    float* st_l = st_m + QC;                                     // [QC] log(S/N)
-    float* wpart = st_l + QC;                                    // [kWaves][QC][4]
-    float* colsum = wpart + kWaves * QC * 4;                     // [N]
+    // qcap = min(QC, N_T rounded up to 16) query rows per chunk
+    const int qbcap = qcap / 16;
+    T* qs = reinterpret_cast<T*>(smem);                          // [qcap][QS]
+    float* st_m = reinterpret_cast<float*>(qs + qcap * QS);      // [qcap] m + L per query
+    float* wpart = st_m + qcap;                                  // [kWaves][qcap][4]
+    float* lstat = wpart + kWaves * qcap * 4;                    // [3][qbcap][kThreads]
+    float* colsum = lstat + 3 * qbcap * kThreads;                // [N]
 
     const int bid = xcd_remap(blockIdx.x, nblocks);              // (b*L + l)*H + h
     const int h = bid % H;
@@ -185,11 +175,15 @@ __global__ __launch_bounds__(kThreads) void score_mean_prob_kernel(
     const int ngroups = (ntiles + TG - 1) / TG;
     const float fN = static_cast<float>(N);
     const int koff = std::is_same<T, float>::value ? 4 * lg : 8 * lg;
+    // this lane's online statistics (max, sum expm1, sum exp) of query block qb
+    float* lm = lstat + tid;
+    float* lE = lstat + qbcap * kThreads + tid;
+    float* lS = lstat + 2 * qbcap * kThreads + tid;
 
     for (int n = tid; n < N; n += kThreads) colsum[n] = 0.f;
 
-    for (int t0 = 0; t0 < NT; t0 += QC) {
-        const int rows = min(QC, NT - t0);
+    for (int t0 = 0; t0 < NT; t0 += qcap) {
+        const int rows = min(qcap, NT - t0);
         const int QB = (rows + 15) / 16;
         __syncthreads();
         // ---- stage this chunk of queries (rows past NT are zero) ----
@@ -202,16 +196,14 @@ __global__ __launch_bounds__(kThreads) void score_mean_prob_kernel(
                                                      c * EPV);
             *reinterpret_cast<f32x4v*>(qs + row * QS + c * EPV) = v;
         }
+        for (int qb = 0; qb < QB; ++qb) {
+            lm[qb * kThreads] = -INFINITY;
+            lE[qb * kThreads] = 0.f;
+            lS[qb * kThreads] = 0.f;
+        }
         __syncthreads();
 
         // ---- pass 1: online statistics of this lane's query in each block ----
-        float m[QBM], E[QBM], S[QBM];
-#pragma unroll
-        for (int i = 0; i < QBM; ++i) {
-            m[i] = -INFINITY;
-            E[i] = 0.f;
-            S[i] = 0.f;
-        }
         float cnt = 0.f;                                          // valid keys seen by this lane
         for (int gi = wave; gi < ngroups; gi += kWaves) {
             AFrag a[TG][NA];
@@ -225,103 +217,113 @@ __global__ __launch_bounds__(kThreads) void score_mean_prob_kernel(
 #pragma unroll
                 for (int r = 0; r < 4; ++r) kval[tt][r] = tile * 16 + 4 * lg + r < N;
             }
-#pragma unroll
-            for (int qb = 0; qb < QBM; ++qb) {
-                if (qb < QB) {
-                    float v[TG][4];
-                    float mx = m[qb];
-#pragma unroll
-                    for (int tt = 0; tt < TG; ++tt) {
-                        const f32x4v z = tile_mma<D>(a[tt], qs, qb * 16, lr, lg);
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            v[tt][r] = kval[tt][r] ? z[r] * scale : -INFINITY;
-                            mx = fmaxf(mx, v[tt][r]);
-                        }
-                    }
-                    if (__any(mx > m[qb])) {
-                        // rescale the sums to the new maximum (exact no-op where unchanged)
-                        const float dm = (mx > m[qb]) ? m[qb] - mx : 0.f;
-                        const float sc = expf(dm);
-                        const float em = (cnt > 0.f) ? expm1f(dm) : 0.f;
-                        E[qb] = fmaf(cnt, em, E[qb] * sc);
-                        S[qb] = S[qb] * sc;
-                        m[qb] = mx;
-                    }
-#pragma unroll
-                    for (int tt = 0; tt < TG; ++tt)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            float t, w;
-                            exp_pair(kval[tt][r] ? v[tt][r] - mx : 0.f, t, w);
-                            if (kval[tt][r]) {
-                                E[qb] += t;
-                                S[qb] += w;
-                            }
-                        }
-                }
-            }
+            const bool full = (gi + 1) * TG * 16 <= N;            // no key past N
+            float cntg = 0.f;                                     // valid keys of this lane here
 #pragma unroll
             for (int tt = 0; tt < TG; ++tt)
 #pragma unroll
-                for (int r = 0; r < 4; ++r) cnt += kval[tt][r] ? 1.f : 0.f;
+                for (int r = 0; r < 4; ++r) cntg += kval[tt][r] ? 1.f : 0.f;
+            for (int qb = 0; qb < QB; ++qb) {
+                AFrag bq[NA];
+                load_queries<D>(bq, qs, qb * 16, lr, lg);
+                float z[TG * 4];
+#pragma unroll
+                for (int tt = 0; tt < TG; ++tt) {
+                    const f32x4v zt = tile_mma<NA>(a[tt], bq);
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) z[tt * 4 + r] = zt[r];
+                }
+                float zmax = -INFINITY, zmin = INFINITY;
+#pragma unroll
+                for (int i = 0; i < TG * 4; ++i) {
+                    const bool ok = full || kval[i / 4][i % 4];
+                    zmax = fmaxf(zmax, ok ? z[i] : -INFINITY);
+                    zmin = fminf(zmin, ok ? z[i] : INFINITY);
+                }
+                float m = lm[qb * kThreads], E = lE[qb * kThreads], S = lS[qb * kThreads];
+                const float mx = fmaxf(m, zmax * scale);          // scale > 0
+                if (__any(mx > m)) {
+                    // rescale the sums to the new maximum (exact no-op where unchanged)
+                    const float dm = (mx > m) ? m - mx : 0.f;
+                    const float sc = expf(dm);
+                    const float em = (cnt > 0.f) ? expm1f(dm) : 0.f;
+                    E = fmaf(cnt, em, E * sc);
+                    S = S * sc;
+                    m = mx;
+                }
+                // every x = z * scale - mx lies in [zmin * scale - mx, 0]
+                const bool near = cntg == 0.f || fmaf(zmin, scale, -mx) >= -kSeriesRange;
+                if (__all(near)) {
+                    float el = 0.f;
+#pragma unroll
+                    for (int i = 0; i < TG * 4; ++i) {
+                        const float t = expm1_series(fmaf(z[i], scale, -mx));
+                        el += (full || kval[i / 4][i % 4]) ? t : 0.f;
+                    }
+                    E += el;
+                    S += cntg + el;
+                } else {
+#pragma unroll
+                    for (int i = 0; i < TG * 4; ++i) {
+                        if (full || kval[i / 4][i % 4]) {
+                            const float x = fmaf(z[i], scale, -mx);
+                            const float t = expm1f(x);
+                            E += t;
+                            S += (x < -0.5f) ? expf(x) : 1.0f + t;
+                        }
+                    }
+                }
+                lm[qb * kThreads] = m;
+                lE[qb * kThreads] = E;
+                lS[qb * kThreads] = S;
+            }
+            cnt += cntg;
         }
 
         // ---- merge statistics: the 4 lane groups of a wave, then the waves ----
-#pragma unroll
-        for (int qb = 0; qb < QBM; ++qb) {
-            if (qb < QB) {
-                float M = m[qb];
-                M = fmaxf(M, __shfl_xor(M, 16));
-                M = fmaxf(M, __shfl_xor(M, 32));
-                float e = 0.f, s = 0.f;
-                if (cnt > 0.f) {
-                    const float dm = m[qb] - M;
-                    e = fmaf(cnt, expm1f(dm), E[qb] * expf(dm));
-                    s = S[qb] * expf(dm);
-                }
-                float c = cnt;
-                e += __shfl_xor(e, 16);
-                s += __shfl_xor(s, 16);
-                c += __shfl_xor(c, 16);
-                e += __shfl_xor(e, 32);
-                s += __shfl_xor(s, 32);
-                c += __shfl_xor(c, 32);
-                if (lg == 0) {
-                    float* w = wpart + (wave * QC + qb * 16 + lr) * 4;
-                    w[0] = (c > 0.f) ? M : -INFINITY;
-                    w[1] = e;
-                    w[2] = s;
-                    w[3] = c;
-                }
+        for (int qb = 0; qb < QB; ++qb) {
+            const float m = lm[qb * kThreads];
+            float M = fmaxf(m, __shfl_xor(m, 16));
+            M = fmaxf(M, __shfl_xor(M, 32));
+            float e = 0.f, s = 0.f;
+            if (cnt > 0.f) {
+                const float dm = m - M;
+                e = fmaf(cnt, expm1f(dm), lE[qb * kThreads] * expf(dm));
+                s = lS[qb * kThreads] * expf(dm);
+            }
+            float c = cnt;
+            e += __shfl_xor(e, 16);
+            s += __shfl_xor(s, 16);
+            c += __shfl_xor(c, 16);
+            e += __shfl_xor(e, 32);
+            s += __shfl_xor(s, 32);
+            c += __shfl_xor(c, 32);
+            if (lg == 0) {
+                float* wp = wpart + (wave * qcap + qb * 16 + lr) * 4;
+                wp[0] = (c > 0.f) ? M : -INFINITY;
+                wp[1] = e;
+                wp[2] = s;
+                wp[3] = c;
             }
         }
         __syncthreads();
         if (tid < QB * 16) {
             float M = -INFINITY;
-            for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wpart[(w * QC + tid) * 4]);
+            for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wpart[(w * qcap + tid) * 4]);
             float e = 0.f, s = 0.f;
             for (int w = 0; w < kWaves; ++w) {
-                const float* p = wpart + (w * QC + tid) * 4;
+                const float* p = wpart + (w * qcap + tid) * 4;
                 if (p[0] == -INFINITY) continue;     // this wave saw no key
                 const float dm = p[0] - M;
                 e += fmaf(p[3], expm1f(dm), p[1] * expf(dm));
                 s += p[2] * expf(dm);
             }
-            st_m[tid] = (tid < rows) ? M : 0.f;
-            st_l[tid] = (tid < rows) ? log_mean_exp(e, s, fN) : 0.f;
+            // one shift per query: z * scale - (m + L) is the centred logit
+            st_m[tid] = (tid < rows) ? M + log_mean_exp(e, s, fN) : 0.f;
         }
         __syncthreads();
 
         // ---- pass 2: per key, sum over queries of expm1(z - m - L) ----------
-        float qm[QBM], ql[QBM];
-        bool qval[QBM];
-#pragma unroll
-        for (int qb = 0; qb < QBM; ++qb) {
-            qm[qb] = st_m[qb * 16 + lr];
-            ql[qb] = st_l[qb * 16 + lr];
-            qval[qb] = qb * 16 + lr < rows;
-        }
         for (int gi = wave; gi < ngroups; gi += kWaves) {
             AFrag a[TG][NA];
 #pragma unroll
@@ -330,33 +332,40 @@ __global__ __launch_bounds__(kThreads) void score_mean_prob_kernel(
                 load_keys<NA>(a[tt], kg + static_cast<int64_t>(min(key, N - 1)) * D + koff,
                               key < N);
             }
-            float col[TG][4];
+            float col[TG * 4];
 #pragma unroll
-            for (int tt = 0; tt < TG; ++tt)
+            for (int i = 0; i < TG * 4; ++i) col[i] = 0.f;
+            for (int qb = 0; qb < QB; ++qb) {
+                AFrag bq[NA];
+                load_queries<D>(bq, qs, qb * 16, lr, lg);
+                const float shift = st_m[qb * 16 + lr];
+                const bool qval = qb * 16 + lr < rows;
+                float x[TG * 4];
+                float xmin = INFINITY, xmax = -INFINITY;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) col[tt][r] = 0.f;
+                for (int tt = 0; tt < TG; ++tt) {
+                    const f32x4v z = tile_mma<NA>(a[tt], bq);
 #pragma unroll
-            for (int qb = 0; qb < QBM; ++qb) {
-                if (qb < QB) {
-#pragma unroll
-                    for (int tt = 0; tt < TG; ++tt) {
-                        const f32x4v z = tile_mma<D>(a[tt], qs, qb * 16, lr, lg);
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const float t = expm1_fast((z[r] * scale - qm[qb]) - ql[qb]);
-                            col[tt][r] += qval[qb] ? t : 0.f;
-                        }
+                    for (int r = 0; r < 4; ++r) {
+                        x[tt * 4 + r] = fmaf(z[r], scale, -shift);
+                        xmin = fminf(xmin, x[tt * 4 + r]);
+                        xmax = fmaxf(xmax, x[tt * 4 + r]);
                     }
+                }
+                if (__all(fmaxf(-xmin, xmax) <= kSeriesRange)) {
+#pragma unroll
+                    for (int i = 0; i < TG * 4; ++i) col[i] += qval ? expm1_series(x[i]) : 0.f;
+                } else {
+#pragma unroll
+                    for (int i = 0; i < TG * 4; ++i) col[i] += qval ? expm1f(x[i]) : 0.f;
                 }
             }
 #pragma unroll
-            for (int tt = 0; tt < TG; ++tt)
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const float sum = group_sum<16>(col[tt][r]);
-                    const int key = (gi * TG + tt) * 16 + 4 * lg + r;
-                    if (lr == 0 && key < N) colsum[key] += sum;
-                }
+            for (int i = 0; i < TG * 4; ++i) {
+                const float sum = group_sum<16>(col[i]);
+                const int key = (gi * TG + i / 4) * 16 + 4 * lg + i % 4;
+                if (lr == 0 && key < N) colsum[key] += sum;
+            }
         }
     }
     __syncthreads();
@@ -374,8 +383,9 @@ template <typename T, int D>
 hipError_t launch_mp(const Dims& d, float scale, const void* q, const void* k, float* e,
                      float* r, hipStream_t st) {
     using C = ProbCfg<T, D>;
-    const size_t lds = static_cast<size_t>(C::QC) * C::QS * sizeof(T) +
-                       (2 * C::QC + kWaves * C::QC * 4) * sizeof(float) +
+    const int qcap = static_cast<int>(std::min<int64_t>(C::QC, (d.NT + 15) / 16 * 16));
+    const size_t lds = static_cast<size_t>(qcap) * C::QS * sizeof(T) +
+                       (qcap + kWaves * qcap * 4 + 3 * (qcap / 16) * kThreads) * sizeof(float) +
                        static_cast<size_t>(d.N) * sizeof(float);
     auto kern = score_mean_prob_kernel<T, D>;
     if (lds > 64 * 1024) {
@@ -389,7 +399,7 @@ hipError_t launch_mp(const Dims& d, float scale, const void* q, const void* k, f
                        static_cast<const T*>(q), static_cast<const T*>(k), e, r,
                        static_cast<int>(d.H), static_cast<int>(d.NT), static_cast<int>(d.N),
                        static_cast<int>(d.group), static_cast<int>(d.Hkv), scale,
-                       static_cast<int>(blocks));
+                       static_cast<int>(blocks), qcap);
     return hipGetLastError();
 }
 

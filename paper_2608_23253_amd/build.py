@@ -21,8 +21,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libe2s.so")
 
-SOURCES = ["e2s_validate.cpp", "e2s_api.hip", "score.hip", "score_prob.hip", "fuse.hip",
-           "select.hip"]
+SOURCES = ["e2s_validate.cpp", "e2s_api.hip", "score.hip", "score_prob.hip", "layer.hip",
+           "fuse.hip", "select.hip"]
 
 ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-Wno-unused-parameter",

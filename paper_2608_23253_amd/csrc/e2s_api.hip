@@ -184,9 +184,17 @@ e2s_status e2s_prune(const e2s_shape* shape, const e2s_params* params, const voi
     if (workspace_bytes < e2s::prune_workspace_bytes(d)) return E2S_ERR_WORKSPACE_TOO_SMALL;
 
     const hipStream_t st = static_cast<hipStream_t>(stream);
+    if (params->mode == E2S_SCORE_MEAN_LOGIT && e2s::layer_evidence_fits(d)) {
+        // one workgroup per layer keeps the supports in LDS: rho, pbar_c in the workspace
+        float* rho = static_cast<float*>(workspace);
+        float* pbar = rho + d.B * d.L * d.N;
+        E2S_TRY(from_hip(e2s::launch_layer_evidence(d, params->dtype, effective_scale(params, d),
+                                                    q, k, rho, pbar, st)));
+        return from_hip(e2s::launch_ds_select(d, params->cells, params->lambda, params->keep, rho,
+                                              pbar, keep_idx, fused_opt, prio_c_opt, st));
+    }
     float* support_c = static_cast<float*>(workspace);
-    const size_t e_bytes =
-        e2s::align_up(static_cast<size_t>(d.B * d.L * d.H * d.N) * sizeof(float), 256);
+    const size_t e_bytes = e2s::prune_region_bytes(d);
     float* prio_c = prio_c_opt ? prio_c_opt
                                : reinterpret_cast<float*>(static_cast<char*>(workspace) + e_bytes);
     E2S_TRY(run_score(d, params, q, k, support_c, nullptr, st));

@@ -36,4 +36,15 @@ hipError_t launch_spatial_select(const Dims& d, int cells, float lambda, int kee
                                  const float* prio_c, int32_t* keep_idx, double* adj_c,
                                  uint8_t* is_rep, hipStream_t stream);
 
+// Score + reliability of a whole layer per workgroup (mean-of-logits reading, one
+// query head per key head), writing rho and pbar_c [B, L, N]; applicable when
+// layer_evidence_fits(d).
+bool layer_evidence_fits(const Dims& d);
+hipError_t launch_layer_evidence(const Dims& d, int dtype, float scale, const void* q,
+                                 const void* k, float* rho, float* pbar_c, hipStream_t stream);
+// Eq. 11-19 from rho, pbar_c, then Eq. 20-23; fused and prio_c may be null.
+hipError_t launch_ds_select(const Dims& d, int cells, float lambda, int keep, const float* rho,
+                            const float* pbar_c, int32_t* keep_idx, float* fused, float* prio_c,
+                            hipStream_t stream);
+
 }  // namespace e2s

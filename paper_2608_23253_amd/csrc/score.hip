@@ -4,9 +4,16 @@
 // Mean-of-logits reading.  Eq. 1 averages Q_t.K_n / sqrt(d) over the text queries;
 // by linearity that equals (mean_t Q_t).K_n / sqrt(d), so the stage is a stream of
 // the key tensor against one query vector per head: an HBM-bound matrix-vector
-// product.  One workgroup owns one (image, layer, key head) unit (and a chunk of
-// at most 8 of the query heads that share that key head under grouped-query
-// attention), so every key row is read from HBM exactly once:
+// product.
+//
+// One query head per key head (multi-head attention): one wave owns one (image,
+// layer, head) unit and runs all steps below on its own, without workgroup
+// barriers (wave_head: the query mean in registers, the key rows streamed with
+// the next batch in flight, the softmax reduced across the wave).
+//
+// Grouped-query attention: one workgroup owns one (image, layer, key head) unit
+// (and a chunk of at most 8 of the query heads that share that key head), so every
+// key row is read from HBM exactly once:
 //
 //   A  qbar_h = (scale / N_T) * sum_t Q[h, t, :]             (fp32, LDS); the first
 //      key rows are already being loaded while this runs, and all heads of the
@@ -34,14 +41,16 @@
 // sum dominated by a few O(1) positive terms).
 #include "e2s_device.h"
 #include "e2s_kernels.h"
+#include "score_common.h"
 
+#include <algorithm>
 #include <cmath>
 
 namespace e2s {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / kWave;
+constexpr int kThreads = kGroupThreads;     // one 4-wave reduction group
+constexpr int kWaves = kGroupWaves;
 constexpr int kMaxChunk = 8;                  // query heads per workgroup
 constexpr int kLdsBudget = 96 * 1024;         // bytes of dynamic LDS per workgroup
 constexpr int kUnroll = 8;                    // key rows in flight per lane
@@ -91,35 +100,18 @@ __global__ __launch_bounds__(kThreads) void score_mean_logit_kernel(
     // consecutive dims; the RPW row groups of a wave meet by shuffles, the waves
     // in LDS.
     {
-        constexpr int QU = 4;
         for (int j = 0; j < rc; ++j) {
-            const T* qh = q + ((bl * H + hq0 + j) * NT) * D + wl * 8;
-            float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-            for (int t = wave * RPW + wrow; t - wrow < NT; t += QU * STEP) {
-                Packet<T> p[QU];
+            float acc[8];
+            query_partial<T, D>(q + ((bl * H + hq0 + j) * NT) * D + wl * 8, NT, wave, wrow, acc);
+            if (wrow == 0) {
 #pragma unroll
-                for (int u = 0; u < QU; ++u)
-                    load_packet(p[u], qh + static_cast<int64_t>(min(t + u * STEP, NT - 1)) * D);
-#pragma unroll
-                for (int u = 0; u < QU; ++u) {
-                    float x[8];
-                    unpack(p[u], x);
-                    const bool ok = t + u * STEP < NT;
-#pragma unroll
-                    for (int m = 0; m < 8; ++m) acc[m] += ok ? x[m] : 0.f;
-                }
-            }
-#pragma unroll
-            for (int m = 0; m < 8; ++m) {
-                for (int o = LPR; o < kWave; o <<= 1) acc[m] += __shfl_xor(acc[m], o);
-                if (wrow == 0) part[(j * kWaves + wave) * D + wl * 8 + m] = acc[m];
+                for (int m = 0; m < 8; ++m) part[(j * kWaves + wave) * D + wl * 8 + m] = acc[m];
             }
         }
         __syncthreads();
         for (int i = tid; i < rc * D; i += kThreads) {
             const int j = i / D, dd = i - j * D;
-            const float* pj = part + j * kWaves * D + dd;
-            qbar[i] = (((pj[0] + pj[D]) + pj[2 * D]) + pj[3 * D]) * qscale;
+            qbar[i] = query_mean(part + j * kWaves * D + dd, D, qscale);
         }
         __syncthreads();
     }
@@ -141,10 +133,7 @@ __global__ __launch_bounds__(kThreads) void score_mean_logit_kernel(
 #pragma unroll
             for (int j = 0; j < RC; ++j) {
                 if (j < rc) {
-                    float s = qb[j][0] * x[0];
-#pragma unroll
-                    for (int m = 1; m < 8; ++m) s = fmaf(qb[j][m], x[m], s);
-                    s = group_sum<LPR>(s);
+                    const float s = row_logit<LPR>(qb[j], x);
                     if (wl == 0 && n < N) logits[j * N + n] = s;
                 }
             }
@@ -156,38 +145,16 @@ __global__ __launch_bounds__(kThreads) void score_mean_logit_kernel(
     const float fN = static_cast<float>(N);
     if (rc == 1) {
         // a single head: the whole workgroup shares it
+        __shared__ float red[16];
         float* a = logits;
-        __shared__ float red[3 * kWaves];
-        float m = -INFINITY;
-        for (int n = tid; n < N; n += kThreads) m = fmaxf(m, a[n]);
-        m = wave_max(m);
-        if (lane == 0) red[wave] = m;
-        __syncthreads();
-        m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-        float E = 0.f, S = 0.f;
-        for (int n = tid; n < N; n += kThreads) {
-            const float d = a[n] - m;
-            a[n] = d;
-            E += expm1f(d);
-            S += expf(d);
-        }
-        E = wave_sum(E);
-        S = wave_sum(S);
-        if (lane == 0) {
-            red[kWaves + wave] = E;
-            red[2 * kWaves + wave] = S;
-        }
-        __syncthreads();
-        E = ((red[kWaves] + red[kWaves + 1]) + red[kWaves + 2]) + red[kWaves + 3];
-        S = ((red[2 * kWaves] + red[2 * kWaves + 1]) + red[2 * kWaves + 2]) + red[2 * kWaves + 3];
-        const float lse = log_mean_exp(E, S, fN);
+        bool near;
+        const float lse = softmax_centre(a, N, tid, red, true, near);
         const int64_t row = (bl * H + hq0) * static_cast<int64_t>(N);
         float* eo = e_out + row;
         float* ro = r_out ? r_out + row : nullptr;
         for (int n = tid; n < N; n += kThreads) {
             const float dc = a[n] - lse;
-            const float u = expm1f(dc);
-            __builtin_nontemporal_store(u / (2.0f * (2.0f + u)), eo + n);
+            __builtin_nontemporal_store(support_from_centred(dc, near), eo + n);
             if (ro) ro[n] = expf(dc) / fN;
         }
         return;
@@ -213,8 +180,7 @@ __global__ __launch_bounds__(kThreads) void score_mean_logit_kernel(
         float* ro = r_out ? r_out + row : nullptr;
         for (int n = lane; n < N; n += kWave) {
             const float dc = a[n] - lse;
-            const float u = expm1f(dc);
-            __builtin_nontemporal_store(u / (2.0f * (2.0f + u)), eo + n);
+            __builtin_nontemporal_store(support_from_centred(dc, false), eo + n);
             if (ro) ro[n] = expf(dc) / fN;
         }
     }
@@ -240,9 +206,53 @@ hipError_t launch_ml(const Dims& d, float qscale, const void* q, const void* k, 
     return hipGetLastError();
 }
 
+// One query head per key head: one wave per (image, layer, head) unit, no
+// workgroup barrier (wave_head); the workgroup only packs up to 4 independent
+// waves together.
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void score_wave_kernel(
+    const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
+    float* __restrict__ r_out, int64_t units, int NT, int N, float qscale) {
+    extern __shared__ float smem[];
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int64_t unit = static_cast<int64_t>(blockIdx.x) * (blockDim.x / kWave) + wave;
+    if (unit >= units) return;
+    float* a = smem + wave * N;
+    float* eo = e_out + unit * N;
+    float* ro = r_out ? r_out + unit * N : nullptr;
+    const float fN = static_cast<float>(N);
+    wave_head<T, D>(q + unit * NT * D, k + unit * N * D, NT, N, qscale, a, lane,
+                    [&](int n, float dc, bool near) {
+                        __builtin_nontemporal_store(support_from_centred(dc, near), eo + n);
+                        if (ro) ro[n] = expf(dc) / fN;
+                    });
+}
+
+template <typename T, int D>
+hipError_t launch_wave(const Dims& d, float qscale, const void* q, const void* k, float* e,
+                       float* r, hipStream_t st) {
+    const int64_t per_wave = d.N * static_cast<int64_t>(sizeof(float));
+    const int wpg = static_cast<int>(std::clamp<int64_t>(kLdsBudget / per_wave, 1, kWaves));
+    const int64_t units = d.B * d.L * d.H;
+    const int64_t blocks = (units + wpg - 1) / wpg;
+    const size_t lds = static_cast<size_t>(wpg * per_wave);
+    auto kern = score_wave_kernel<T, D>;
+    if (lds > 64 * 1024) {
+        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             static_cast<int>(lds));
+        if (err != hipSuccess) return err;
+    }
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(blocks)), dim3(wpg * kWave), lds, st,
+                       static_cast<const T*>(q), static_cast<const T*>(k), e, r, units,
+                       static_cast<int>(d.NT), static_cast<int>(d.N), qscale);
+    return hipGetLastError();
+}
+
 template <typename T, int D>
 hipError_t dispatch_rc(const Dims& d, float qscale, const void* q, const void* k, float* e,
                        float* r, hipStream_t st) {
+    if (d.group == 1) return launch_wave<T, D>(d, qscale, q, k, e, r, st);
     const int64_t fixed = static_cast<int64_t>(kMaxChunk) * D * (1 + kWaves) * 4;
     int64_t fit = (kLdsBudget - fixed) / (d.N * 4);
     if (fit < 1) fit = 1;

@@ -1,0 +1,296 @@
+// Arithmetic of the mean-of-logits score stage shared by the per-head score kernels
+// (score.hip) and the per-layer evidence kernel (layer.hip).  Callers run these
+// functions with the same thread-to-data mapping, so they produce the same bits
+// (the library is compiled without floating-point contraction).
+#pragma once
+
+#include "e2s_device.h"
+
+namespace e2s {
+
+constexpr int kGroupWaves = 4;                       // waves of one reduction group
+constexpr int kGroupThreads = kGroupWaves * kWave;   // 256
+
+// Phase A for one query head: wave lw of a 4-wave group sums rows
+// lw*RPW + wrow + i*STEP (RPW = 64/(D/8) rows per wave load, STEP = 4*RPW) of the
+// head's [N_T, d] queries, lane wl holding dims 8*wl .. 8*wl+7; the RPW row groups
+// of the wave are then combined by shuffles, so lanes with wrow == 0 hold the
+// wave's partial sums.  qh points at the head's row 0, offset by 8*wl elements.
+template <typename T, int D>
+__device__ __forceinline__ void query_partial(const T* __restrict__ qh, int NT, int lw, int wrow,
+                                              float (&acc)[8]) {
+    constexpr int LPR = D / 8, RPW = kWave / LPR, STEP = kGroupWaves * RPW, QU = 4;
+#pragma unroll
+    for (int m = 0; m < 8; ++m) acc[m] = 0.f;
+    for (int t = lw * RPW + wrow; t - wrow < NT; t += QU * STEP) {
+        Packet<T> p[QU];
+#pragma unroll
+        for (int u = 0; u < QU; ++u)
+            load_packet(p[u], qh + static_cast<int64_t>(min(t + u * STEP, NT - 1)) * D);
+#pragma unroll
+        for (int u = 0; u < QU; ++u) {
+            float x[8];
+            unpack(p[u], x);
+            const bool ok = t + u * STEP < NT;
+#pragma unroll
+            for (int m = 0; m < 8; ++m) acc[m] += ok ? x[m] : 0.f;
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < 8; ++m)
+        for (int o = LPR; o < kWave; o <<= 1) acc[m] += __shfl_xor(acc[m], o);
+}
+
+// The four wave partials p[0], p[D], p[2D], p[3D] of one query-mean element,
+// combined left to right and scaled by scale / N_T.
+__device__ __forceinline__ float query_mean(const float* p, int D, float qscale) {
+    return (((p[0] + p[D]) + p[2 * D]) + p[3 * D]) * qscale;
+}
+
+// Logit of one key row: lane wl's 8-element dot product, summed over the LPR lanes
+// that share the row.
+template <int LPR>
+__device__ __forceinline__ float row_logit(const float (&qb)[8], const float (&x)[8]) {
+    float s = qb[0] * x[0];
+#pragma unroll
+    for (int m = 1; m < 8; ++m) s = fmaf(qb[m], x[m], s);
+    return group_sum<LPR>(s);
+}
+
+// expm1 on [-1/8, 1/8]: Taylor series to degree 5 (truncation below 6e-9, under
+// one float32 ulp of the result, there).
+constexpr float kSeriesRange = 0.125f;
+__device__ __forceinline__ float expm1_series(float x) {
+    float p = 1.0f / 120.0f;
+    p = fmaf(p, x, 1.0f / 24.0f);
+    p = fmaf(p, x, 1.0f / 6.0f);
+    p = fmaf(p, x, 0.5f);
+    p = fmaf(p, x, 1.0f);
+    return p * x;
+}
+
+// Softmax statistics of one head's N logits a[] (LDS) over a group of 256 threads
+// (lt = index within the group): a[n] is replaced by a[n] - max and the return
+// value is L = log(S / N) (see log_mean_exp).  near reports whether the head's
+// logits span at most kSeriesRange, in which case every a - max and every
+// a - max - L lies in [-kSeriesRange, kSeriesRange] (L lies between the smallest
+// a - max and 0) and expm1 is evaluated by the short series; otherwise by the
+// library.  red: 16 floats of LDS owned by the group.  Contains two block-wide
+// barriers, so every thread of the workgroup calls it the same number of times;
+// threads of an inactive group pass active = false.
+__device__ __forceinline__ float softmax_centre(float* a, int N, int lt, float* red, bool active,
+                                                bool& near) {
+    const int lw = lt / kWave, lane = lt % kWave;
+    float m = -INFINITY, lo = INFINITY;
+    if (active) {
+        for (int n = lt; n < N; n += kGroupThreads) {
+            m = fmaxf(m, a[n]);
+            lo = fminf(lo, a[n]);
+        }
+    }
+    m = wave_max(m);
+    lo = -wave_max(-lo);
+    if (lane == 0) {
+        red[lw] = m;
+        red[12 + lw] = lo;
+    }
+    __syncthreads();
+    m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    lo = fminf(fminf(red[12], red[13]), fminf(red[14], red[15]));
+    near = m - lo <= kSeriesRange;
+    float E = 0.f, S = 0.f;
+    if (active) {
+        if (near) {
+            for (int n = lt; n < N; n += kGroupThreads) {
+                const float d = a[n] - m;
+                a[n] = d;
+                const float t = expm1_series(d);
+                E += t;
+                S += 1.0f + t;
+            }
+        } else {
+            for (int n = lt; n < N; n += kGroupThreads) {
+                const float d = a[n] - m;
+                a[n] = d;
+                E += expm1f(d);
+                S += expf(d);
+            }
+        }
+    }
+    E = wave_sum(E);
+    S = wave_sum(S);
+    if (lane == 0) {
+        red[4 + lw] = E;
+        red[8 + lw] = S;
+    }
+    __syncthreads();
+    E = ((red[4] + red[5]) + red[6]) + red[7];
+    S = ((red[8] + red[9]) + red[10]) + red[11];
+    return log_mean_exp(E, S, static_cast<float>(N));
+}
+
+// Support e = p - 1/2 of a centred logit dc = a - max - L (Eq. 8-9).
+__device__ __forceinline__ float support_from_centred(float dc, bool near) {
+    const float u = near ? expm1_series(dc) : expm1f(dc);
+    return u / (2.0f * (2.0f + u));
+}
+
+// Orders one wave's LDS stores before its later LDS loads of other lanes' data
+// (LDS requests of a wave are served in issue order; this keeps the compiler from
+// moving loads above the stores).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Lane geometry of the per-wave score stage: 8 elements per lane, LPR lanes per
+// row, RPW rows per wave-wide load, KU rows per lane in flight (16 B per lane per
+// row for bf16, 32 B for fp32).
+template <typename T, int D>
+struct WaveRows {
+    static constexpr int LPR = D / 8, RPW = kWave / LPR, KU = 16 / sizeof(T);
+    static constexpr int BATCH = KU * RPW;   // rows per wave-wide batch
+};
+
+// KU key rows base + wrow + u * RPW of one head (kh offset by 8*wl elements);
+// rows past the end are clamped to the last row (in bounds) and discarded later.
+template <typename T, int D, int KU>
+__device__ __forceinline__ void load_key_batch(Packet<T> (&p)[KU], const T* __restrict__ kh,
+                                               int base, int wrow, int N) {
+    constexpr int RPW = WaveRows<T, D>::RPW;
+#pragma unroll
+    for (int u = 0; u < KU; ++u)
+        load_packet(p[u], kh + static_cast<int64_t>(min(base + wrow + u * RPW, N - 1)) * D);
+}
+
+// Logits of one batch: a[n] = qbar . K[n] for the rows of load_key_batch.
+template <typename T, int D, int KU>
+__device__ __forceinline__ void key_batch_logits(const Packet<T> (&p)[KU], const float (&qb)[8],
+                                                 float* a, int base, int wrow, int wl,
+                                                 int n_end) {
+    constexpr int LPR = WaveRows<T, D>::LPR, RPW = WaveRows<T, D>::RPW;
+#pragma unroll
+    for (int u = 0; u < KU; ++u) {
+        float x[8];
+        unpack(p[u], x);
+        const float s = row_logit<LPR>(qb, x);
+        const int n = base + wrow + u * RPW;
+        if (wl == 0 && n < n_end) a[n] = s;
+    }
+}
+
+// Query mean of one head by one wave: lane (wrow, wl) sums rows wrow, wrow + RPW,
+// ... of dims 8*wl .. 8*wl+7 in increasing row order; the RPW row sums are then
+// combined by a butterfly, so every lane holds the same qbar (times qscale).  qh is
+// offset by 8*wl elements.
+template <typename T, int D>
+__device__ __forceinline__ void wave_query_mean(const T* __restrict__ qh, int NT, int wrow,
+                                                float qscale, float (&qb)[8]) {
+    constexpr int LPR = WaveRows<T, D>::LPR, RPW = WaveRows<T, D>::RPW;
+    constexpr int QU = WaveRows<T, D>::KU;
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int t0 = 0; t0 < NT; t0 += QU * RPW) {
+        Packet<T> p[QU];
+#pragma unroll
+        for (int u = 0; u < QU; ++u)
+            load_packet(p[u], qh + static_cast<int64_t>(min(t0 + wrow + u * RPW, NT - 1)) * D);
+#pragma unroll
+        for (int u = 0; u < QU; ++u) {
+            float x[8];
+            unpack(p[u], x);
+            const bool ok = t0 + wrow + u * RPW < NT;
+#pragma unroll
+            for (int m = 0; m < 8; ++m) acc[m] += ok ? x[m] : 0.f;
+        }
+    }
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+        for (int o = LPR; o < kWave; o <<= 1) acc[m] += __shfl_xor(acc[m], o);
+        qb[m] = acc[m] * qscale;
+    }
+}
+
+// Eq. 8-9 for one head's N logits a[] (LDS, complete and visible to the wave): per
+// lane max / min / sums over n = lane, lane + 64, ... in increasing order, then
+// butterflies across the wave.  Calls emit(n, dc, near) once per token, from lane
+// n % 64, with the centred logit dc = a_n - max - L (u = N r - 1 = expm1(dc));
+// near as in softmax_centre.
+template <typename Emit>
+__device__ __forceinline__ void wave_softmax(float* a, int N, int lane, Emit&& emit) {
+    float mx = -INFINITY, lo = INFINITY;
+    for (int n = lane; n < N; n += kWave) {
+        mx = fmaxf(mx, a[n]);
+        lo = fminf(lo, a[n]);
+    }
+    mx = wave_max(mx);
+    lo = -wave_max(-lo);
+    const bool near = mx - lo <= kSeriesRange;
+    float E = 0.f, S = 0.f;
+    if (near) {
+        for (int n = lane; n < N; n += kWave) {
+            const float d = a[n] - mx;
+            a[n] = d;
+            const float t = expm1_series(d);
+            E += t;
+            S += 1.0f + t;
+        }
+    } else {
+        for (int n = lane; n < N; n += kWave) {
+            const float d = a[n] - mx;
+            a[n] = d;
+            E += expm1f(d);
+            S += expf(d);
+        }
+    }
+    E = wave_sum(E);
+    S = wave_sum(S);
+    const float L = log_mean_exp(E, S, static_cast<float>(N));
+    for (int n = lane; n < N; n += kWave) emit(n, a[n] - L, near);
+}
+
+// Eq. 1, 8 and 9 for one query head, computed by one wave with no workgroup
+// barrier.  qh: the head's [N_T, d] queries; kh: its key head's [N, d] keys; a: N
+// floats of LDS owned by the wave.  The first key batch is requested before the
+// query mean, and each later batch before the previous one is used.
+template <typename T, int D, typename Emit>
+__device__ __forceinline__ void wave_head(const T* __restrict__ qh, const T* __restrict__ kh,
+                                          int NT, int N, float qscale, float* a, int lane,
+                                          Emit&& emit) {
+    using G = WaveRows<T, D>;
+    const int wrow = lane / G::LPR, wl = lane % G::LPR;
+    qh += wl * 8;
+    kh += wl * 8;
+    Packet<T> ka[G::KU], kb[G::KU];
+    load_key_batch<T, D>(ka, kh, 0, wrow, N);
+    float qb[8];
+    wave_query_mean<T, D>(qh, NT, wrow, qscale, qb);
+    for (int base = 0; base < N; base += 2 * G::BATCH) {
+        if (base + G::BATCH < N) load_key_batch<T, D>(kb, kh, base + G::BATCH, wrow, N);
+        key_batch_logits<T, D>(ka, qb, a, base, wrow, wl, N);
+        if (base + G::BATCH >= N) break;
+        if (base + 2 * G::BATCH < N) load_key_batch<T, D>(ka, kh, base + 2 * G::BATCH, wrow, N);
+        key_batch_logits<T, D>(kb, qb, a, base + G::BATCH, wrow, wl, N);
+    }
+    wave_lds_sync();
+    wave_softmax(a, N, lane, emit);
+}
+
+// Eq. 10 for one token from its H supports e[h * stride], in the order of the
+// evidence kernels: head group g = 0..3 sums heads g, g+4, ... in increasing order
+// and the four partial sums are combined left to right.
+__device__ __forceinline__ void reliability_token(const float* e, int stride, int H, float& rho,
+                                                  float& ebar) {
+    float p[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int g = 0; g < 4; ++g)
+        for (int h = g; h < H; h += 4) p[g] += e[h * stride];
+    const float s1 = ((p[0] + p[1]) + p[2]) + p[3];
+    ebar = s1 / static_cast<float>(H);
+    float a[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int g = 0; g < 4; ++g)
+        for (int h = g; h < H; h += 4) a[g] += fabsf(e[h * stride] - ebar);
+    const float s2 = ((a[0] + a[1]) + a[2]) + a[3];
+    rho = reliability_from_sums(s1, s2, 2.0f / static_cast<float>(H));
+}
+
+}  // namespace e2s

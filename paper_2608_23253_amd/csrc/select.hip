@@ -1,253 +1,475 @@
-// Spatial novelty and global top-K (Sec. 4.3 Eq. 20-23), one workgroup per image.
+// Spatial novelty and global top-K (Sec. 4.3 Eq. 20-23), one workgroup of 1024
+// threads per image.
 //
-//  1. the image's complements c = 1 - q are staged in LDS (N <= 16384 floats);
-//  2. cell representatives (Eq. 20-21): one wave per cell scans the cell's
-//     row/column ranges and takes the minimum of the 64-bit key
-//     (order-preserving bits of c) << 32 | index, i.e. the highest q with the
-//     lowest index on ties;
-//  3. adjusted complement c^ = (1 - lambda) c + lambda (1 - b) = 1 - q~ (Eq. 22),
+// Thread t owns the consecutive tokens n0 = t * chunk .. n0 + chunk - 1
+// (chunk = ceil(N / 1024), one token for N <= 1024) and keeps their values in
+// registers throughout.  The work per image is a few KB, so the kernel is bound
+// by latency: every step below is shaped to need few dependent LDS round trips
+// and workgroup barriers.
+//
+//  1. cell representatives (Eq. 20-21): the 64-bit key
+//     (order-preserving bits of c) << 32 | index is minimised per cell, i.e. the
+//     highest q with the lowest index on ties.  Lanes holding tokens of one cell
+//     first combine their keys with DPP row shifts (a segmented minimum inside
+//     each 16-lane row); the last lane of each run folds it into the cell's LDS
+//     slot with an atomic minimum;
+//  2. adjusted complement c^ = (1 - lambda) c + lambda (1 - b) = 1 - q~ (Eq. 22),
 //     evaluated in double precision with explicitly rounded operations; its
 //     order-preserving 64-bit image is the ranking key;
-//  4. the K-th smallest key T is found by a radix select over 8-bit digits (LDS
-//     histogram + one wave's prefix scan per round, at most 8 rounds, fewer once
-//     T's bin holds a single key), together with how many tokens equal to T must
-//     still be taken; lanes of a wave that fall in the same bin are added with one
-//     atomic;
-//  5. tokens with key < T, plus the lowest-index tokens with key == T, are kept
-//     (Eq. 23); two block-wide scans in token order write them in ascending order.
+//  3. the K-th smallest key T is found by a radix select over 8-bit digits,
+//     starting at the highest bit in which the image's smallest and largest keys
+//     differ, together with how many tokens equal to T must still be taken.  Each
+//     round adds the matching keys into an LDS histogram (lanes of a wave that
+//     share a bin with one atomic, since same-word LDS atomics serialise), then
+//     after one barrier every wave scans the histogram itself and takes the same
+//     digit; three histograms in rotation let a round clear the next round's
+//     buffer without a second barrier.  The rounds stop once T's bin holds a
+//     single key;
+//  4. tokens with key < T, plus the lowest-index tokens with key == T, are kept
+//     (Eq. 23); one block-wide scan of the per-thread counts places them in
+//     ascending token order.
 //
 // Ranking by (c^, index) ascending is ranking by (q~ descending, index ascending).
 // The greedy formulation (take the best remaining token K times) returns the same
-// set; the radix select needs 8 rounds instead of K serial argmax steps.
+// set; the radix select needs a handful of rounds instead of K argmax steps.
 #include "e2s_device.h"
 #include "e2s_kernels.h"
 
 namespace e2s {
 namespace {
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int o) {
-    const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), o);
-    const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), o);
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / kWave;
+constexpr int kMaxChunk = 16;          // tokens per thread: N <= 16384
+constexpr int kRowShl1 = 0x101;
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v, uint32_t fill) {
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(
+        static_cast<int>(fill), static_cast<int>(v), CTRL, 0xF, 0xF, false));
+}
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v, uint64_t fill) {
+    const uint32_t hi = dpp_u32<CTRL>(static_cast<uint32_t>(v >> 32), static_cast<uint32_t>(fill >> 32));
+    const uint32_t lo = dpp_u32<CTRL>(static_cast<uint32_t>(v), static_cast<uint32_t>(fill));
     return (static_cast<uint64_t>(hi) << 32) | lo;
 }
-
-__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint64_t w = shfl_xor_u64(v, o);
-        v = w < v ? w : v;
-    }
-    return v;
+__device__ __forceinline__ uint32_t readlane_u32(uint32_t v, int l) {
+    return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), l));
+}
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int l) {
+    return (static_cast<uint64_t>(readlane_u32(static_cast<uint32_t>(v >> 32), l)) << 32) |
+           readlane_u32(static_cast<uint32_t>(v), l);
 }
 
+constexpr int kRowShr1 = 0x111, kRowShr2 = 0x112, kRowShr4 = 0x114, kRowShr8 = 0x118;
+
+// Inclusive prefix sum across the wave: shifts by 1, 2, 4, 8 lanes inside each
+// 16-lane DPP row (lanes shifted in from outside the row add 0), then the totals
+// of the earlier rows, read from lanes 15, 31 and 47, are added.
 __device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x, int lane) {
-    for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t y = __shfl_up(x, o);
-        if (lane >= o) x += y;
-    }
-    return x;
+    x += dpp_u32<kRowShr1>(x, 0u);
+    x += dpp_u32<kRowShr2>(x, 0u);
+    x += dpp_u32<kRowShr4>(x, 0u);
+    x += dpp_u32<kRowShr8>(x, 0u);
+    const uint32_t t0 = readlane_u32(x, 15), t1 = readlane_u32(x, 31), t2 = readlane_u32(x, 47);
+    const int row = lane >> 4;
+    return x + (row >= 1 ? t0 : 0u) + (row >= 2 ? t1 : 0u) + (row >= 3 ? t2 : 0u);
 }
 
-// Exclusive prefix sum of x over the block in thread order.  buf holds >= waves words.
-template <int THREADS>
-__device__ uint32_t block_exclusive_scan(uint32_t x, uint32_t* buf) {
-    constexpr int kW = THREADS / kWave;
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    const uint32_t incl = wave_inclusive_scan(x, lane);
-    if (lane == kWave - 1) buf[wave] = incl;
-    __syncthreads();
-    if (wave == 0) {
-        const uint32_t v = lane < kW ? buf[lane] : 0u;
-        const uint32_t vi = wave_inclusive_scan(v, lane);
-        if (lane < kW) buf[lane] = vi - v;
-    }
-    __syncthreads();
-    const uint32_t r = buf[wave] + incl - x;
-    __syncthreads();
-    return r;
+// One step of the segmented minimum: take the key of the lane S places lower in
+// the row when it belongs to the same cell (lanes shifted in from outside the row
+// carry cell -1 and the largest key).
+template <int CTRL>
+__device__ __forceinline__ void seg_min_step(uint64_t& key, int cell) {
+    const uint64_t k2 = dpp_u64<CTRL>(key, ~0ull);
+    const int c2 = static_cast<int>(dpp_u32<CTRL>(static_cast<uint32_t>(cell), 0xFFFFFFFFu));
+    key = (c2 == cell && k2 < key) ? k2 : key;
 }
 
-template <int THREADS>
-__global__ __launch_bounds__(THREADS) void spatial_select_kernel(
-    const float* __restrict__ prio_c, int32_t* __restrict__ keep_idx, double* __restrict__ adj_out,
-    uint8_t* __restrict__ rep_out, int N, int gh, int gw, int G, float lambda, int K) {
-    constexpr int kW = THREADS / kWave;
-    extern __shared__ unsigned char smem[];
-    float* cs = reinterpret_cast<float*>(smem);                 // [N]
-    uint32_t* hist = reinterpret_cast<uint32_t*>(cs + N);       // [256]
-    uint32_t* scan = hist + 256;                                // [32]
-    uint8_t* rep = reinterpret_cast<uint8_t*>(scan + 32);       // [N]
-    __shared__ uint64_t s_prefix;
-    __shared__ uint32_t s_rank;
-    __shared__ uint32_t s_unique;
-    __shared__ uint64_t s_found;
+// Wave-wide minimum and maximum of 64-bit values, in every lane: quad swaps and
+// half-row / row mirrors inside each 16-lane row, then the four row results.
+template <int CTRL>
+__device__ __forceinline__ void minmax_step(uint64_t& mn, uint64_t& mx) {
+    const uint64_t a = dpp_u64<CTRL>(mn, 0ull), b = dpp_u64<CTRL>(mx, 0ull);
+    mn = a < mn ? a : mn;
+    mx = b > mx ? b : mx;
+}
+__device__ __forceinline__ void wave_minmax_u64(uint64_t& mn, uint64_t& mx) {
+    minmax_step<kQuadSwap1>(mn, mx);
+    minmax_step<kQuadSwap2>(mn, mx);
+    minmax_step<kRowHalfMirror>(mn, mx);
+    minmax_step<kRowMirror>(mn, mx);
+    uint64_t a = readlane_u64(mn, 0), b = readlane_u64(mx, 0);
+#pragma unroll
+    for (int r = 16; r < kWave; r += 16) {
+        const uint64_t ar = readlane_u64(mn, r), br = readlane_u64(mx, r);
+        a = ar < a ? ar : a;
+        b = br > b ? br : b;
+    }
+    mn = a;
+    mx = b;
+}
 
+// Workgroup-shared state of a selection besides the per-cell slots.
+struct SelectShared {
+    uint32_t hist[3][256];
+    uint32_t scan[kWaves];
+    uint64_t wlo[kWaves], whi[kWaves];
+    uint64_t found;
+};
+
+// Selection of one image (Eq. 20-23).  cv[j] = c of token n0 + j for j < cnt
+// (registers of the calling thread, tokens owned as described above); best: G*G
+// words of LDS.  All threads of the workgroup call it.
+template <int MAXC>
+__device__ void select_image(const float (&cv)[MAXC], int n0, int cnt, int chunk,
+                             uint64_t* best, SelectShared& sh, int64_t b,
+                             int32_t* __restrict__ keep_idx, double* __restrict__ adj_out,
+                             uint8_t* __restrict__ rep_out, int N, int gh, int gw, int G,
+                             float lambda, int K) {
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
-    const int64_t b = blockIdx.x;
-    const float* cb = prio_c + b * N;
-    for (int n = tid; n < N; n += THREADS) {
-        cs[n] = cb[n];
-        rep[n] = 0;
+
+    for (int i = tid; i < G * G; i += kThreads) best[i] = ~0ull;
+    if (tid < 256) sh.hist[0][tid] = 0u;
+    __syncthreads();
+
+    // ---- cell representatives (Eq. 20) -----------------------------------
+    int cell[MAXC];
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        if (j >= chunk) break;
+        const int n = n0 + j;
+        const int row = n / gw, col = n - (n / gw) * gw;
+        cell[j] = j < cnt ? (row * G / gh) * G + col * G / gw : -1 - lane;
+        uint64_t key = j < cnt ? (static_cast<uint64_t>(ordered_bits(cv[j])) << 32) |
+                                     static_cast<uint32_t>(n)
+                               : ~0ull;
+        seg_min_step<kRowShr1>(key, cell[j]);
+        seg_min_step<kRowShr2>(key, cell[j]);
+        seg_min_step<kRowShr4>(key, cell[j]);
+        seg_min_step<kRowShr8>(key, cell[j]);
+        // the last lane of each run inside the row holds the run's minimum
+        const int next = static_cast<int>(
+            __builtin_amdgcn_update_dpp(-1, cell[j], kRowShl1, 0xF, 0xF, false));
+        const bool last = next != cell[j];   // lane 15 of a row reads -1
+        if (j < cnt && last)
+            atomicMin(reinterpret_cast<unsigned long long*>(best + cell[j]),
+                      static_cast<unsigned long long>(key));
     }
     __syncthreads();
 
-    // ---- cell representatives ---------------------------------------------
-    for (int cell = wave; cell < G * G; cell += kW) {
-        const int gr = cell / G, gc = cell - gr * G;
-        const int r0 = (gr * gh + G - 1) / G, r1 = ((gr + 1) * gh + G - 1) / G;
-        const int c0 = (gc * gw + G - 1) / G, c1 = ((gc + 1) * gw + G - 1) / G;
-        const int cw = c1 - c0, cnt = (r1 - r0) * cw;
-        uint64_t best = ~0ull;
-        for (int j = lane; j < cnt; j += kWave) {
-            const int row = r0 + j / cw;
-            const int n = row * gw + c0 + (j - (j / cw) * cw);
-            const uint64_t key = (static_cast<uint64_t>(ordered_bits(cs[n])) << 32) |
-                                 static_cast<uint32_t>(n);
-            best = key < best ? key : best;
-        }
-        best = wave_min_u64(best);
-        if (lane == 0 && cnt > 0) rep[static_cast<uint32_t>(best)] = 1;
-    }
-    __syncthreads();
-
+    // ---- ranking keys (Eq. 21-22) ------------------------------------------
     const double lam = static_cast<double>(lambda);
     const double oml = 1.0 - lam;
-    auto adj = [&](int n) -> double {
-        const double t = __dmul_rn(oml, static_cast<double>(cs[n]));
-        return rep[n] ? t : __dadd_rn(t, lam);
-    };
-    if (adj_out || rep_out) {
-        for (int n = tid; n < N; n += THREADS) {
-            if (adj_out) adj_out[b * N + n] = adj(n);
-            if (rep_out) rep_out[b * N + n] = rep[n];
+    uint64_t kk[MAXC];
+    uint64_t kmin = ~0ull, kmax = 0ull;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        kk[j] = ~0ull;
+        if (j >= chunk) break;
+        if (j < cnt) {
+            const int n = n0 + j;
+            const bool rep = static_cast<uint32_t>(best[cell[j]]) == static_cast<uint32_t>(n);
+            const double t = __dmul_rn(oml, static_cast<double>(cv[j]));
+            const double adj = rep ? t : __dadd_rn(t, lam);
+            kk[j] = ordered_bits(adj);
+            kmin = kk[j] < kmin ? kk[j] : kmin;
+            kmax = kk[j] > kmax ? kk[j] : kmax;
+            if (adj_out) adj_out[b * N + n] = adj;
+            if (rep_out) rep_out[b * N + n] = rep ? 1 : 0;
         }
     }
     if (K <= 0) return;
-
-    // ---- radix select of the K-th smallest key ----------------------------
-    if (tid == 0) {
-        s_prefix = 0;
-        s_rank = static_cast<uint32_t>(K);
-        s_unique = 0;
+    wave_minmax_u64(kmin, kmax);
+    if (lane == 0) {
+        sh.wlo[wave] = kmin;
+        sh.whi[wave] = kmax;
     }
-    uint64_t mask = 0;
-    for (int shift = 56; shift >= 0; shift -= 8) {
-        for (int i = tid; i < 256; i += THREADS) hist[i] = 0;
-        __syncthreads();
-        const uint64_t prefix = s_prefix;
-        if (s_unique) {
-            // the previous round left one key with this prefix: it is the K-th key
-            for (int n = tid; n < N; n += THREADS) {
-                const uint64_t kk = ordered_bits(adj(n));
-                if ((kk & mask) == prefix) s_found = kk;
-            }
-            __syncthreads();
-            if (tid == 0) s_prefix = s_found;
-            __syncthreads();
-            break;
-        }
-        for (int base = 0; base < N; base += THREADS) {
-            const int n = base + tid;
-            const uint64_t kk = n < N ? ordered_bits(adj(n)) : 0ull;
-            const bool match = n < N && (kk & mask) == prefix;
-            const uint32_t digit = static_cast<uint32_t>(kk >> shift) & 255u;
-            // early rounds put most keys of a wave in one bin: add them with one atomic
-            const uint64_t mb = __ballot(match);
-            if (mb) {
-                const int leader = __ffsll(static_cast<unsigned long long>(mb)) - 1;
-                const uint32_t d0 = __shfl(digit, leader);
-                const uint64_t same = __ballot(match && digit == d0);
-                if (same == mb) {
-                    if (lane == leader) atomicAdd(&hist[d0], static_cast<uint32_t>(__popcll(mb)));
-                } else if (match) {
-                    atomicAdd(&hist[digit], 1u);
+    __syncthreads();
+    uint64_t lo = sh.wlo[0], hi = sh.whi[0];
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w) {
+        lo = sh.wlo[w] < lo ? sh.wlo[w] : lo;
+        hi = sh.whi[w] > hi ? sh.whi[w] : hi;
+    }
+
+    // ---- radix select of the K-th smallest key (Eq. 23) -----------------------
+    uint64_t T = lo;                        // all keys equal: T = lo, take K of them
+    uint32_t need_eq = static_cast<uint32_t>(K);
+    if (lo != hi) {
+        const int top = 63 - __clzll(static_cast<long long>(lo ^ hi));
+        uint64_t mask = top == 63 ? 0ull : (~0ull << (top + 1));
+        uint64_t prefix = lo & mask;        // bits above top: common to every key
+        uint32_t rank = static_cast<uint32_t>(K);
+        int shift = top >= 7 ? top - 7 : 0;
+        for (int round = 0;; ++round) {
+            uint32_t* h = sh.hist[round % 3];
+            // the buffer after this one was last read before the previous barrier
+            if (tid < 256) sh.hist[(round + 1) % 3][tid] = 0u;
+#pragma unroll
+            for (int j = 0; j < MAXC; ++j) {
+                if (j >= chunk) break;
+                const bool match = j < cnt && (kk[j] & mask) == prefix;
+                const uint32_t digit = static_cast<uint32_t>(kk[j] >> shift) & 255u;
+                uint64_t mb = __ballot(match);
+                for (int it = 0; it < 2 && mb; ++it) {
+                    const int leader = __ffsll(static_cast<unsigned long long>(mb)) - 1;
+                    const uint32_t d0 = readlane_u32(digit, leader);
+                    const uint64_t same = __ballot(match && digit == d0);
+                    if (lane == leader) atomicAdd(&h[d0], static_cast<uint32_t>(__popcll(same)));
+                    mb &= ~same;
                 }
+                if ((mb >> lane) & 1ull) atomicAdd(&h[digit], 1u);
             }
-        }
-        __syncthreads();
-        if (wave == 0) {
-            const uint32_t h0 = hist[4 * lane], h1 = hist[4 * lane + 1];
-            const uint32_t h2 = hist[4 * lane + 2], h3 = hist[4 * lane + 3];
+            __syncthreads();
+            // every wave finds the bin that holds the rank-th matching key
+            const uint32_t h0 = h[4 * lane], h1 = h[4 * lane + 1];
+            const uint32_t h2 = h[4 * lane + 2], h3 = h[4 * lane + 3];
             const uint32_t local = h0 + h1 + h2 + h3;
             const uint32_t incl = wave_inclusive_scan(local, lane);
-            const uint32_t rank = s_rank;
-            const uint64_t hit = __ballot(incl >= rank);
-            const int first = __ffsll(static_cast<unsigned long long>(hit)) - 1;
-            if (lane == first) {
-                uint32_t cum = incl - local;
-                int digit = 4 * lane;
-                if (cum + h0 < rank) {
-                    cum += h0;
+            const int first = __ffsll(static_cast<unsigned long long>(__ballot(incl >= rank))) - 1;
+            uint32_t cum = readlane_u32(incl - local, first);
+            const uint32_t g0 = readlane_u32(h0, first), g1 = readlane_u32(h1, first);
+            const uint32_t g2 = readlane_u32(h2, first), g3 = readlane_u32(h3, first);
+            uint32_t digit = 4 * first, cnt_d = g0;
+            if (cum + g0 < rank) {
+                cum += g0;
+                ++digit;
+                cnt_d = g1;
+                if (cum + g1 < rank) {
+                    cum += g1;
                     ++digit;
-                    if (cum + h1 < rank) {
-                        cum += h1;
+                    cnt_d = g2;
+                    if (cum + g2 < rank) {
+                        cum += g2;
                         ++digit;
-                        if (cum + h2 < rank) {
-                            cum += h2;
-                            ++digit;
-                        }
+                        cnt_d = g3;
                     }
                 }
-                s_prefix = prefix | (static_cast<uint64_t>(digit) << shift);
-                s_rank = rank - cum;
-                s_unique = hist[digit] == 1u;
             }
+            prefix |= static_cast<uint64_t>(digit) << shift;
+            rank -= cum;
+            mask |= 0xFFull << shift;
+            if (cnt_d == 1u) {
+                // one key carries this prefix: it is the K-th key
+#pragma unroll
+                for (int j = 0; j < MAXC; ++j) {
+                    if (j >= chunk) break;
+                    if (j < cnt && (kk[j] & mask) == prefix) sh.found = kk[j];
+                }
+                __syncthreads();
+                T = sh.found;
+                need_eq = 1u;
+                break;
+            }
+            if (shift == 0) {
+                T = prefix;                 // every bit is fixed
+                need_eq = rank;
+                break;
+            }
+            shift = shift >= 8 ? shift - 8 : 0;
         }
-        mask |= 0xFFull << shift;
-        __syncthreads();
     }
-    const uint64_t T = s_prefix;
-    const uint32_t need_eq = s_rank;   // tokens equal to T still to take, >= 1
 
-    // ---- ordered compaction --------------------------------------------------
-    const int chunk = (N + THREADS - 1) / THREADS;
-    const int n0 = min(N, tid * chunk), n1 = min(N, n0 + chunk);
-    uint32_t eq_local = 0;
-    for (int n = n0; n < n1; ++n) eq_local += ordered_bits(adj(n)) == T;
-    const uint32_t eq_before = block_exclusive_scan<THREADS>(eq_local, scan);
-    uint32_t sel_local = 0, eqr = eq_before;
-    for (int n = n0; n < n1; ++n) {
-        const uint64_t kk = ordered_bits(adj(n));
-        const bool take = kk < T || (kk == T && eqr < need_eq);
-        eqr += kk == T;
-        sel_local += take;
+    // ---- ordered compaction ----------------------------------------------------
+    // counts below 2^16 (N <= 16384): both prefix sums ride in one word
+    uint32_t lt = 0, eq = 0;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        if (j >= chunk) break;
+        if (j < cnt) {
+            lt += kk[j] < T;
+            eq += kk[j] == T;
+        }
     }
-    uint32_t pos = block_exclusive_scan<THREADS>(sel_local, scan);
-    eqr = eq_before;
+    const uint32_t packed = (lt << 16) | eq;
+    const uint32_t incl = wave_inclusive_scan(packed, lane);
+    if (lane == kWave - 1) sh.scan[wave] = incl;
+    __syncthreads();
+    uint32_t before = incl - packed;
+    for (int w = 0; w < wave; ++w) before += sh.scan[w];
+    uint32_t lt_run = before >> 16, eq_run = before & 0xFFFFu;
     int32_t* out = keep_idx + b * K;
-    for (int n = n0; n < n1; ++n) {
-        const uint64_t kk = ordered_bits(adj(n));
-        const bool take = kk < T || (kk == T && eqr < need_eq);
-        eqr += kk == T;
-        if (take && pos < static_cast<uint32_t>(K)) out[pos++] = n;
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        if (j >= chunk) break;
+        if (j < cnt) {
+            uint32_t pos = static_cast<uint32_t>(K);
+            if (kk[j] < T) {
+                pos = lt_run + (eq_run < need_eq ? eq_run : need_eq);
+                ++lt_run;
+            } else if (kk[j] == T) {
+                if (eq_run < need_eq) pos = lt_run + eq_run;
+                ++eq_run;
+            }
+            if (pos < static_cast<uint32_t>(K)) out[pos] = n0 + j;
+        }
     }
 }
 
-template <int THREADS>
-hipError_t launch_sel(const Dims& d, int cells, float lambda, int keep, const float* c,
-                      int32_t* keep_idx, double* adj, uint8_t* rep, hipStream_t st) {
-    const size_t lds = static_cast<size_t>(d.N) * sizeof(float) + (256 + 32) * sizeof(uint32_t) +
-                       align_up(static_cast<size_t>(d.N), 16);
-    auto kern = spatial_select_kernel<THREADS>;
-    if (lds > 64 * 1024) {
-        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             static_cast<int>(lds));
-        if (err != hipSuccess) return err;
+template <int MAXC>
+__global__ __launch_bounds__(kThreads) void spatial_select_kernel(
+    const float* __restrict__ prio_c, int32_t* __restrict__ keep_idx, double* __restrict__ adj_out,
+    uint8_t* __restrict__ rep_out, int N, int gh, int gw, int G, float lambda, int K) {
+    extern __shared__ uint64_t best[];
+    __shared__ SelectShared sh;
+    const int64_t b = blockIdx.x;
+    const int chunk = (N + kThreads - 1) / kThreads;
+    const int n0 = min(N, static_cast<int>(threadIdx.x) * chunk);
+    const int cnt = min(N - n0, chunk);
+    const float* cb = prio_c + b * N;
+    float cv[MAXC];
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        if (j >= chunk) break;
+        cv[j] = cb[min(n0 + j, N - 1)];     // in bounds; unused past cnt
     }
-    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(THREADS), lds, st, c,
-                       keep_idx, adj, rep, static_cast<int>(d.N), static_cast<int>(d.gh),
+    select_image<MAXC>(cv, n0, cnt, chunk, best, sh, b, keep_idx, adj_out, rep_out, N, gh, gw, G,
+                       lambda, K);
+}
+
+// Dempster fusion across the layers (Eq. 11-19) from per-layer reliability and
+// mean support, then the selection: the tail of e2s_prune after the per-layer
+// evidence kernel.  The per-token arithmetic is that of the staged mass and
+// Dempster kernels.  Each layer's inputs are requested together (and, with up to
+// 4 tokens per thread, before the previous layer is combined).
+template <int MAXC>
+__global__ __launch_bounds__(kThreads) void ds_select_kernel(
+    const float* __restrict__ rho, const float* __restrict__ pbar_c, float* __restrict__ fused,
+    float* __restrict__ prio_c, int32_t* __restrict__ keep_idx, int L, int N, int gh, int gw,
+    int G, float lambda, int K) {
+    extern __shared__ uint64_t best[];
+    __shared__ SelectShared sh;
+    const int64_t b = blockIdx.x;
+    const int chunk = (N + kThreads - 1) / kThreads;
+    const int n0 = min(N, static_cast<int>(threadIdx.x) * chunk);
+    const int cnt = min(N - n0, chunk);
+
+    float r[MAXC], e[MAXC];      // current layer's inputs
+    float aI[MAXC], aU[MAXC], aT[MAXC], kl[MAXC];
+    auto load_layer = [&](int l, float (&rr)[MAXC], float (&ee)[MAXC]) {
+        const int64_t base = (b * L + l) * N;
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= chunk) break;
+            const int64_t i = base + min(n0 + j, N - 1);   // in bounds; unused past cnt
+            rr[j] = rho[i];
+            ee[j] = pbar_c[i];
+        }
+    };
+    load_layer(0, r, e);
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        if (j >= chunk) break;
+        masses_from_reliability(r[j], e[j], aI[j], aU[j], aT[j]);
+        kl[j] = 0.f;
+    }
+    // with many tokens per thread the prefetch would not fit in registers
+    constexpr bool kPrefetch = MAXC <= 4;
+    if (kPrefetch && L > 1) load_layer(1, r, e);
+    for (int l = 1; l < L; ++l) {
+        float r2[MAXC], e2[MAXC];
+        if (!kPrefetch) load_layer(l, r, e);
+        else if (l + 1 < L) load_layer(l + 1, r2, e2);
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= chunk) break;
+            float mI, mU, mT;
+            masses_from_reliability(r[j], e[j], mI, mU, mT);
+            kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
+            if (kPrefetch && l + 1 < L) {
+                r[j] = r2[j];
+                e[j] = e2[j];
+            }
+        }
+    }
+    float cv[MAXC];
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        if (j >= chunk) break;
+        cv[j] = priority_complement(aU[j], kl[j]);
+        if (j < cnt) {
+            const int64_t i = b * N + n0 + j;
+            if (fused) {
+                fused[3 * i + 0] = aI[j];
+                fused[3 * i + 1] = aU[j];
+                fused[3 * i + 2] = aT[j];
+            }
+            if (prio_c) prio_c[i] = cv[j];
+        }
+    }
+    select_image<MAXC>(cv, n0, cnt, chunk, best, sh, b, keep_idx, nullptr, nullptr, N, gh, gw, G,
+                       lambda, K);
+}
+
+template <typename Kern>
+hipError_t allow_lds(Kern kern, size_t lds) {
+    if (lds <= 64 * 1024) return hipSuccess;
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+}
+
+template <int MAXC>
+hipError_t launch_dssel(const Dims& d, int cells, float lambda, int keep, const float* rho,
+                        const float* pbar_c, int32_t* keep_idx, float* fused, float* prio_c,
+                        hipStream_t st) {
+    const size_t lds = static_cast<size_t>(cells) * cells * sizeof(uint64_t);
+    auto kern = ds_select_kernel<MAXC>;
+    hipError_t err = allow_lds(kern, lds);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(kThreads), lds, st, rho, pbar_c,
+                       fused, prio_c, keep_idx, static_cast<int>(d.L), static_cast<int>(d.N),
+                       static_cast<int>(d.gh), static_cast<int>(d.gw), cells, lambda, keep);
+    return hipGetLastError();
+}
+
+template <int MAXC>
+hipError_t launch_sel(const Dims& d, int cells, float lambda, int keep, const float* prio_c,
+                      int32_t* keep_idx, double* adj_c, uint8_t* is_rep, hipStream_t st) {
+    const size_t lds = static_cast<size_t>(cells) * cells * sizeof(uint64_t);
+    auto kern = spatial_select_kernel<MAXC>;
+    hipError_t err = allow_lds(kern, lds);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(kThreads), lds, st, prio_c,
+                       keep_idx, adj_c, is_rep, static_cast<int>(d.N), static_cast<int>(d.gh),
                        static_cast<int>(d.gw), cells, lambda, keep);
     return hipGetLastError();
 }
 
+// Tokens per thread, rounded up to the kernel variant's register budget.
+int chunk_class(const Dims& d) {
+    const int64_t chunk = (d.N + kThreads - 1) / kThreads;
+    return chunk <= 1 ? 1 : chunk <= 2 ? 2 : chunk <= 4 ? 4 : chunk <= 8 ? 8 : kMaxChunk;
+}
+
 }  // namespace
+
+hipError_t launch_ds_select(const Dims& d, int cells, float lambda, int keep, const float* rho,
+                            const float* pbar_c, int32_t* keep_idx, float* fused, float* prio_c,
+                            hipStream_t st) {
+    switch (chunk_class(d)) {
+        case 1: return launch_dssel<1>(d, cells, lambda, keep, rho, pbar_c, keep_idx, fused, prio_c, st);
+        case 2: return launch_dssel<2>(d, cells, lambda, keep, rho, pbar_c, keep_idx, fused, prio_c, st);
+        case 4: return launch_dssel<4>(d, cells, lambda, keep, rho, pbar_c, keep_idx, fused, prio_c, st);
+        case 8: return launch_dssel<8>(d, cells, lambda, keep, rho, pbar_c, keep_idx, fused, prio_c, st);
+        default:
+            return launch_dssel<kMaxChunk>(d, cells, lambda, keep, rho, pbar_c, keep_idx, fused,
+                                           prio_c, st);
+    }
+}
 
 hipError_t launch_spatial_select(const Dims& d, int cells, float lambda, int keep,
                                  const float* prio_c, int32_t* keep_idx, double* adj_c,
                                  uint8_t* is_rep, hipStream_t st) {
-    if (d.N <= 2048)
-        return launch_sel<256>(d, cells, lambda, keep, prio_c, keep_idx, adj_c, is_rep, st);
-    return launch_sel<1024>(d, cells, lambda, keep, prio_c, keep_idx, adj_c, is_rep, st);
+    switch (chunk_class(d)) {
+        case 1: return launch_sel<1>(d, cells, lambda, keep, prio_c, keep_idx, adj_c, is_rep, st);
+        case 2: return launch_sel<2>(d, cells, lambda, keep, prio_c, keep_idx, adj_c, is_rep, st);
+        case 4: return launch_sel<4>(d, cells, lambda, keep, prio_c, keep_idx, adj_c, is_rep, st);
+        case 8: return launch_sel<8>(d, cells, lambda, keep, prio_c, keep_idx, adj_c, is_rep, st);
+        default:
+            return launch_sel<kMaxChunk>(d, cells, lambda, keep, prio_c, keep_idx, adj_c, is_rep, st);
+    }
 }
 
 }  // namespace e2s

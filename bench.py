@@ -3,10 +3,13 @@
 
     python bench.py [--steps K] [--warmup W] [--workload llava] [--mode mean_logit]
 
-One step is one e2s_prune call over the whole batch: the score kernel, the
-fused evidence kernel and the selection kernel, with Q and K already resident
-in HBM.  Prints ONE JSON line with images/s, a roofline object for the
-dominant (score) kernel and the CPU oracle's throughput on a bounded sample.
+One step is one e2s_prune call over the whole batch with Q and K already resident
+in HBM: e2s_layer_reliability (score and head reliability, Eq. 1, 8-10) then
+e2s_fuse_select (masses, fusion and selection, Eq. 11-23).  Prints ONE JSON line
+with images/s, a roofline object for the dominant kernel (the score and
+reliability stage, timed alone with HIP events on the launch stream), per-stage
+times of the staged entry points, and the CPU oracle's throughput on a bounded
+sample.
 
 Other modes (used by the profiling commands kept with the results):
     --kernel-only   run only the timed e2s_prune steps (no CPU baseline)
@@ -27,8 +30,11 @@ sys.path.insert(0, ROOT)
 METRIC = "images pruned/sec (score+fuse+select) at LLaVA shape; % MFMA / % HBM peak"
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_mean_logit_llava_traffic.txt")
-SCORE_SOURCES = ("score.hip", "score_prob.hip", "e2s_device.h")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "layer_evidence_llava_traffic.txt")
+# the sources of the score and reliability stage: a counter summary taken on other
+# versions of them is not used
+STAGE_SOURCES = ("layer.hip", "score.hip", "score_prob.hip", "score_common.h", "fuse.hip",
+                 "e2s_device.h")
 
 
 def log(*a):
@@ -54,15 +60,15 @@ def parse():
 def source_digest() -> str:
     import hashlib
     h = hashlib.sha256()
-    for name in SCORE_SOURCES:
+    for name in STAGE_SOURCES:
         with open(os.path.join(ROOT, "paper_2608_23253_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
 def read_traffic(mode: str):
-    """HBM bytes per score launch from the committed counter summary, or None when
-    it is missing or was taken on a different version of the score kernel."""
+    """HBM bytes per launch of the score and reliability stage from the committed
+    counter summary, or None when it is missing or was taken on other sources."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     vals = {}
@@ -71,7 +77,7 @@ def read_traffic(mode: str):
             if ":" in line and not line.startswith("#"):
                 key, val = line.split(":", 1)
                 vals[key.strip()] = val.strip()
-    if vals.get("score_source_sha256_16") != source_digest() or vals.get("mode") != mode:
+    if vals.get("stage_source_sha256_16") != source_digest() or vals.get("mode") != mode:
         return None
     try:
         return float(vals["hbm_bytes_per_launch"])
@@ -103,14 +109,13 @@ def hbm_probe(mib: int):
     import torch
     n = mib * (1 << 20) // 4
     x = torch.ones(n, device="cuda", dtype=torch.float32)
-    out = torch.empty((), device="cuda", dtype=torch.float32)
     for _ in range(3):
-        torch.sum(x, out=out)
+        x.sum()
     torch.cuda.synchronize()
     s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     s.record()
     for _ in range(10):
-        torch.sum(x, out=out)
+        x.sum()
     e.record()
     torch.cuda.synchronize()
     ms = s.elapsed_time(e) / 10
@@ -176,49 +181,80 @@ def main():
         print(json.dumps({"ms_per_step": ms_step, "value": value}))
         return
 
-    # ---- region B: per-kernel durations (the same three kernels, staged) ------
+    # ---- region B: the two kernels of e2s_prune, each timed alone ---------------
     lib = L.lib()
     sh = pr.shape
     pa = L.make_params(pr.params.dtype, args.mode, 0.0, cfg.cells, cfg.lam, cfg.keep)
-    e_buf = torch.empty((B, cfg.num_layers, cfg.num_heads, N), device="cuda", dtype=torch.float32)
-    c_buf = torch.empty((B, N), device="cuda", dtype=torch.float32)
+    L_, H_ = cfg.num_layers, cfg.num_heads
+    rho = torch.empty((B, L_, N), device="cuda", dtype=torch.float32)
+    pbar = torch.empty_like(rho)
     keep_buf = torch.empty((B, cfg.keep), device="cuda", dtype=torch.int32)
     st = stream.cuda_stream
     shp, pap = ctypes.byref(sh), ctypes.byref(pa)
+    ws, ws_n = pr.workspace.data_ptr(), pr.workspace.numel()
     n_ev = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n_ev)]
-    for _ in range(args.warmup):
-        lib.e2s_score_heads(shp, pap, qd.data_ptr(), kd.data_ptr(), e_buf.data_ptr(), None, st)
-        lib.e2s_fuse_evidence(shp, e_buf.data_ptr(), None, None, c_buf.data_ptr(), st)
-        lib.e2s_spatial_select(shp, pap, c_buf.data_ptr(), keep_buf.data_ptr(), None, None, st)
-    torch.cuda.synchronize()
-    for i in range(n_ev):
-        ev[i][0].record(stream)
-        rc = lib.e2s_score_heads(shp, pap, qd.data_ptr(), kd.data_ptr(), e_buf.data_ptr(), None, st)
-        ev[i][1].record(stream)
-        rc |= lib.e2s_fuse_evidence(shp, e_buf.data_ptr(), None, None, c_buf.data_ptr(), st)
-        ev[i][2].record(stream)
-        rc |= lib.e2s_spatial_select(shp, pap, c_buf.data_ptr(), keep_buf.data_ptr(), None, None,
-                                     st)
-        ev[i][3].record(stream)
-        if rc:
-            raise RuntimeError(f"staged call failed with status {rc}")
-    torch.cuda.synchronize()
-    t_score = np.array([ev[i][0].elapsed_time(ev[i][1]) for i in range(n_ev)])
-    t_fuse = np.array([ev[i][1].elapsed_time(ev[i][2]) for i in range(n_ev)])
-    t_sel = np.array([ev[i][2].elapsed_time(ev[i][3]) for i in range(n_ev)])
+
+    def layer_rel():
+        return lib.e2s_layer_reliability(shp, pap, qd.data_ptr(), kd.data_ptr(), ws, ws_n,
+                                         rho.data_ptr(), pbar.data_ptr(), st)
+
+    def fuse_sel():
+        return lib.e2s_fuse_select(shp, pap, rho.data_ptr(), pbar.data_ptr(), keep_buf.data_ptr(),
+                                   None, None, st)
+
+    def timed(calls, n):
+        """Per-call durations (ms) of each function in `calls`, run in order n times,
+        from HIP events recorded on the launch stream between the calls."""
+        for _ in range(args.warmup):
+            for c in calls:
+                c()
+        torch.cuda.synchronize()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
+              for _ in range(n)]
+        for i in range(n):
+            ev[i][0].record(stream)
+            for j, c in enumerate(calls):
+                rc = c()
+                if rc:
+                    raise RuntimeError(f"{c.__name__} failed with status {rc}")
+                ev[i][j + 1].record(stream)
+        torch.cuda.synchronize()
+        return [np.array([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(n)])
+                for j in range(len(calls))]
+
+    t_lr, t_fs = timed([layer_rel, fuse_sel], n_ev)
+    assert torch.equal(keep_buf, pr.keep_idx), "two-call and e2s_prune results differ"
+
+    # ---- region C: the staged entry points (score, fused evidence, select) -----
+    e_buf = torch.empty((B, L_, H_, N), device="cuda", dtype=torch.float32)
+    c_buf = torch.empty((B, N), device="cuda", dtype=torch.float32)
+
+    def score():
+        return lib.e2s_score_heads(shp, pap, qd.data_ptr(), kd.data_ptr(), e_buf.data_ptr(),
+                                   None, st)
+
+    def fuse():
+        return lib.e2s_fuse_evidence(shp, e_buf.data_ptr(), None, None, c_buf.data_ptr(), st)
+
+    def select():
+        return lib.e2s_spatial_select(shp, pap, c_buf.data_ptr(), keep_buf.data_ptr(), None,
+                                      None, st)
+
+    t_score, t_fuse, t_sel = timed([score, fuse, select], n_ev)
     assert torch.equal(keep_buf, pr.keep_idx), "staged and fused paths disagree"
 
     per_img_qk = cfg.bytes_per_image()
-    per_img_e = 4 * cfg.num_layers * cfg.num_heads * N
-    algo_bytes = B * (per_img_qk + per_img_e)
-    score_ms = float(t_score.mean())
-    achieved = algo_bytes / (score_ms * 1e-3) / 1e9
+    # algorithmic bytes of the score and reliability stage: Q and K read once,
+    # rho and pbar_c [B, L, N] f32 written
+    algo_bytes = B * per_img_qk + 2 * 4 * B * L_ * N
+    lr_ms = float(t_lr.mean())
+    achieved = algo_bytes / (lr_ms * 1e-3) / 1e9
     traffic = read_traffic(args.mode)
-    flops_eq1 = 2.0 * B * cfg.num_layers * cfg.num_heads * cfg.num_text * N * cfg.head_dim
-    log(f"[bench] score {score_ms * 1e3:.1f} us (p10 {np.percentile(t_score, 10) * 1e3:.1f}, "
-        f"p90 {np.percentile(t_score, 90) * 1e3:.1f}), fuse {t_fuse.mean() * 1e3:.1f} us, "
-        f"select {t_sel.mean() * 1e3:.1f} us; score {achieved:.0f} GB/s")
+    flops_eq1 = 2.0 * B * L_ * H_ * cfg.num_text * N * cfg.head_dim
+    log(f"[bench] layer_reliability {lr_ms * 1e3:.1f} us (p10 {np.percentile(t_lr, 10) * 1e3:.1f},"
+        f" p90 {np.percentile(t_lr, 90) * 1e3:.1f}) {achieved:.0f} GB/s; fuse_select "
+        f"{t_fs.mean() * 1e3:.1f} us | staged: score {t_score.mean() * 1e3:.1f} us, fuse "
+        f"{t_fuse.mean() * 1e3:.1f} us, select {t_sel.mean() * 1e3:.1f} us")
 
     # ---- CPU oracle baseline ----------------------------------------------------
     import oracle as O
@@ -265,20 +301,23 @@ def main():
         },
         "roofline": {
             "bound": "hbm",
-            "kernel": "score (e2s_score_heads)",
+            "kernel": "score + head reliability (e2s_layer_reliability)",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
             "algorithmic_bytes_per_launch": algo_bytes,
-            "launch_us": round(score_ms * 1e3, 2),
-            "mfma_frac_if_eq1_flops": round(flops_eq1 / (score_ms * 1e-3) / 1e12
+            "launch_us": round(lr_ms * 1e3, 2),
+            "mfma_frac_if_eq1_flops": round(flops_eq1 / (lr_ms * 1e-3) / 1e12
                                             / MFMA_BF16_PEAK_TFLOPS, 4),
         },
-        "stages_us": {"score": round(score_ms * 1e3, 2), "fuse": round(float(t_fuse.mean()) * 1e3, 2),
-                      "select": round(float(t_sel.mean()) * 1e3, 2)},
-        "path_hbm_frac": round(B * (per_img_qk) / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "stages_us": {"layer_reliability": round(lr_ms * 1e3, 2),
+                      "fuse_select": round(float(t_fs.mean()) * 1e3, 2),
+                      "staged_score": round(float(t_score.mean()) * 1e3, 2),
+                      "staged_fuse": round(float(t_fuse.mean()) * 1e3, 2),
+                      "staged_select": round(float(t_sel.mean()) * 1e3, 2)},
+        "path_hbm_frac": round(B * per_img_qk / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
         "cpu_baseline": {
             "value": round(cpu_value, 2),
             "unit": "images/s",

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define E2S_ABI_VERSION 1
+#define E2S_ABI_VERSION 2
 
 #if defined(__GNUC__) || defined(__clang__)
 #define E2S_API __attribute__((visibility("default")))
@@ -144,13 +144,41 @@ E2S_API e2s_status e2s_spatial_select(const e2s_shape* shape, const e2s_params* 
                               const float* prio_c, int32_t* keep_idx, double* adj_c_opt,
                               uint8_t* is_rep_opt, void* stream);
 
-/* Bytes of device workspace e2s_prune needs for this shape (host-only query). */
+/* Score and head reliability in one call (Sec. 3.1 Eq. 1; Sec. 4.1 Eq. 8-10):
+ *   rho, pbar_c [B, L, N] f32 out, bit-identical to e2s_score_heads followed by
+ *   e2s_head_reliability.
+ * With the MEAN_LOGIT reading, H == Hkv and one layer's supports on chip
+ * (H * (N + d) * 4 <= 153600 bytes), one workgroup per (image, layer) keeps the
+ * supports in local memory and only rho and pbar_c reach device memory; otherwise
+ * the two staged kernels run with the supports in `workspace`.
+ *   workspace: 256-byte aligned, >= e2s_prune_workspace_size bytes, contents
+ *   undefined on return.
+ * Uses params->dtype, mode and scale. */
+E2S_API e2s_status e2s_layer_reliability(const e2s_shape* shape, const e2s_params* params,
+                                 const void* q, const void* k, void* workspace,
+                                 size_t workspace_bytes, float* rho, float* pbar_c,
+                                 void* stream);
+
+/* Masses, fusion and selection in one call (Sec. 4.1 Eq. 11; Sec. 4.2 Eq. 12-19;
+ * Sec. 4.3 Eq. 20-23) from rho, pbar_c [B, L, N]; one workgroup per image.  The
+ * results are bit-identical to e2s_head_masses -> e2s_ds_combine_layers ->
+ * e2s_spatial_select.
+ *   keep_idx [B, K] int32 out (NULL iff K == 0); fused_opt [B, N, 3] and
+ *   prio_c_opt [B, N] f32 out or NULL.
+ * Uses params->cells, lambda and keep. */
+E2S_API e2s_status e2s_fuse_select(const e2s_shape* shape, const e2s_params* params,
+                           const float* rho, const float* pbar_c, int32_t* keep_idx,
+                           float* fused_opt, float* prio_c_opt, void* stream);
+
+/* Bytes of device workspace e2s_prune and e2s_layer_reliability need for this
+ * shape (host-only query). */
 E2S_API e2s_status e2s_prune_workspace_size(const e2s_shape* shape, const e2s_params* params,
                                     size_t* bytes);
 
 /* The whole path (Algorithm 1 with every source layer fused before one top-K):
- * e2s_score_heads -> e2s_fuse_evidence -> e2s_spatial_select on `stream`, with the
- * intermediates in `workspace` (256-byte aligned, >= e2s_prune_workspace_size bytes).
+ * e2s_layer_reliability -> e2s_fuse_select on `stream`, with the intermediates in
+ * `workspace` (256-byte aligned, >= e2s_prune_workspace_size bytes, contents
+ * undefined on return); the result equals the staged calls bit for bit.
  *   keep_idx [B, K] int32 out (NULL iff K == 0); fused_opt [B, N, 3] and
  *   prio_c_opt [B, N] f32 out or NULL. */
 E2S_API e2s_status e2s_prune(const e2s_shape* shape, const e2s_params* params, const void* q,

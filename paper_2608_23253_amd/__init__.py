@@ -5,9 +5,11 @@ include/e2s.h); this package only builds and binds it.  Importing it without a
 built library raises ImportError: there is no CPU fallback.
 """
 from ._lib import (E2SError, Params, Pruner, Shape, default_scale, ds_combine_layers,
-                   fuse_evidence, head_masses, head_reliability, lib, make_params, make_shape,
-                   prune, score_heads, spatial_select, workspace_size)
+                   fuse_evidence, fuse_select, head_masses, head_reliability, layer_reliability,
+                   lib, make_params, make_shape, prune, score_heads, spatial_select,
+                   workspace_size)
 
 __all__ = ["E2SError", "Params", "Pruner", "Shape", "default_scale", "ds_combine_layers",
-           "fuse_evidence", "head_masses", "head_reliability", "lib", "make_params", "make_shape",
-           "prune", "score_heads", "spatial_select", "workspace_size"]
+           "fuse_evidence", "fuse_select", "head_masses", "head_reliability",
+           "layer_reliability", "lib", "make_params", "make_shape", "prune", "score_heads",
+           "spatial_select", "workspace_size"]

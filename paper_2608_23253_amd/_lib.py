@@ -64,6 +64,8 @@ _SIGNATURES = {
     "e2s_ds_combine_layers": [_SH, _P, _P, _P, _P, _P],
     "e2s_fuse_evidence": [_SH, _P, _P, _P, _P, _P],
     "e2s_spatial_select": [_SH, _PA, _P, _P, _P, _P, _P],
+    "e2s_layer_reliability": [_SH, _PA, _P, _P, _P, ctypes.c_size_t, _P, _P, _P],
+    "e2s_fuse_select": [_SH, _PA, _P, _P, _P, _P, _P, _P],
     "e2s_prune_workspace_size": [_SH, _PA, ctypes.POINTER(ctypes.c_size_t)],
     "e2s_prune": [_SH, _PA, _P, _P, _P, ctypes.c_size_t, _P, _P, _P, _P],
     "e2s_status_string": [ctypes.c_int],
@@ -273,6 +275,46 @@ def spatial_select(prio_c, grid_h: int, grid_w: int, keep: int, cells: int = 4,
                                    out.data_ptr() if keep > 0 else None, _ptr(adj), _ptr(rep),
                                    _stream(dev)), "e2s_spatial_select")
     return out, adj, rep
+
+
+def layer_reliability(q, k, grid_h: int, grid_w: int, mode="mean_logit", scale: float = 0.0,
+                      workspace=None):
+    """Eq. 1, 8-10 in one call: (rho, pbar_c) each [B, L, N].  workspace: a uint8
+    device tensor of at least workspace_size() bytes (allocated here if None)."""
+    torch = _torch()
+    _check(q, "q", ndim=5)
+    _check(k, "k", dtype=q.dtype, ndim=5)
+    sh = shape_from(q, k, grid_h, grid_w)
+    pa = make_params(_dtype_code(q), mode, scale)
+    if workspace is None:
+        workspace = torch.empty(workspace_size(sh, pa), device=q.device, dtype=torch.uint8)
+    B, L, N = sh.batch, sh.num_layers, grid_h * grid_w
+    rho = torch.empty((B, L, N), device=q.device, dtype=torch.float32)
+    pbar = torch.empty_like(rho)
+    _raise(_LIB.e2s_layer_reliability(ctypes.byref(sh), ctypes.byref(pa), q.data_ptr(),
+                                      k.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                                      rho.data_ptr(), pbar.data_ptr(), _stream(q.device)),
+           "e2s_layer_reliability")
+    return rho, pbar
+
+
+def fuse_select(rho, pbar_c, grid_h: int, grid_w: int, keep: int, cells: int = 4,
+                lam: float = 0.1, want_fused=False, want_prio=False):
+    """Eq. 11-23 in one call: (keep_idx [B,K], fused [B,N,3] or None, prio_c [B,N] or None)."""
+    torch = _torch()
+    _check(rho, "rho", dtype=torch.float32, ndim=3)
+    _check(pbar_c, "pbar_c", dtype=torch.float32, ndim=3)
+    B, L, N = rho.shape
+    sh = make_shape(B, L, 1, 1, 128, 1, grid_h, grid_w)
+    pa = make_params(cells=cells, lam=lam, keep=keep)
+    dev = rho.device
+    out = torch.empty((B, keep), device=dev, dtype=torch.int32)
+    fused = torch.empty((B, N, 3), device=dev, dtype=torch.float32) if want_fused else None
+    prio = torch.empty((B, N), device=dev, dtype=torch.float32) if want_prio else None
+    _raise(_LIB.e2s_fuse_select(ctypes.byref(sh), ctypes.byref(pa), rho.data_ptr(),
+                                pbar_c.data_ptr(), out.data_ptr() if keep > 0 else None,
+                                _ptr(fused), _ptr(prio), _stream(dev)), "e2s_fuse_select")
+    return out, fused, prio
 
 
 def workspace_size(shape: Shape, params: Params) -> int:

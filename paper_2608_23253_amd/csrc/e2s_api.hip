@@ -56,6 +56,33 @@ e2s_status run_score(const Dims& d, const e2s_params* params, const void* q, con
         e2s::launch_score_mean_prob(d, params->dtype, scale, q, k, support_c, r_opt, st));
 }
 
+// Eq. 1, 8-10: per-layer rho and pbar_c, on chip when a layer fits, else through
+// the supports in `workspace`.
+e2s_status run_layer_reliability(const Dims& d, const e2s_params* params, const void* q,
+                                 const void* k, void* workspace, float* rho, float* pbar_c,
+                                 hipStream_t st) {
+    if (params->mode == E2S_SCORE_MEAN_LOGIT && e2s::layer_evidence_fits(d))
+        return from_hip(e2s::launch_layer_evidence(d, params->dtype, effective_scale(params, d), q,
+                                                   k, rho, pbar_c, st));
+    float* support_c = static_cast<float*>(workspace);
+    E2S_TRY(run_score(d, params, q, k, support_c, nullptr, st));
+    return from_hip(e2s::launch_head_reliability(d, support_c, rho, pbar_c, st));
+}
+
+e2s_status check_score_inputs(const e2s_shape* shape, const e2s_params* params, const void* q,
+                              const void* k, void* workspace, size_t workspace_bytes, Dims* d) {
+    E2S_TRY(e2s::check_shape(shape, d));
+    E2S_TRY(e2s::check_score_params(params));
+    E2S_TRY(need(q));
+    E2S_TRY(need(k));
+    E2S_TRY(need(workspace));
+    E2S_TRY(e2s::check_aligned(q, 16));
+    E2S_TRY(e2s::check_aligned(k, 16));
+    E2S_TRY(e2s::check_aligned(workspace, 256));
+    if (workspace_bytes < e2s::prune_workspace_bytes(*d)) return E2S_ERR_WORKSPACE_TOO_SMALL;
+    return E2S_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -164,43 +191,58 @@ e2s_status e2s_prune_workspace_size(const e2s_shape* shape, const e2s_params* pa
     return E2S_OK;
 }
 
+e2s_status e2s_layer_reliability(const e2s_shape* shape, const e2s_params* params,
+                                 const void* q, const void* k, void* workspace,
+                                 size_t workspace_bytes, float* rho, float* pbar_c,
+                                 void* stream) {
+    Dims d;
+    E2S_TRY(check_score_inputs(shape, params, q, k, workspace, workspace_bytes, &d));
+    E2S_TRY(need(rho));
+    E2S_TRY(need(pbar_c));
+    E2S_TRY(e2s::check_aligned(rho, 4));
+    E2S_TRY(e2s::check_aligned(pbar_c, 4));
+    return run_layer_reliability(d, params, q, k, workspace, rho, pbar_c,
+                                 static_cast<hipStream_t>(stream));
+}
+
+e2s_status e2s_fuse_select(const e2s_shape* shape, const e2s_params* params, const float* rho,
+                           const float* pbar_c, int32_t* keep_idx, float* fused_opt,
+                           float* prio_c_opt, void* stream) {
+    Dims d;
+    E2S_TRY(e2s::check_shape(shape, &d));
+    E2S_TRY(e2s::check_select_params(params, d));
+    E2S_TRY(need(rho));
+    E2S_TRY(need(pbar_c));
+    if (params->keep > 0) E2S_TRY(need(keep_idx));
+    E2S_TRY(e2s::check_aligned(rho, 4));
+    E2S_TRY(e2s::check_aligned(pbar_c, 4));
+    E2S_TRY(aligned_opt(keep_idx, 4));
+    E2S_TRY(aligned_opt(fused_opt, 4));
+    E2S_TRY(aligned_opt(prio_c_opt, 4));
+    return from_hip(e2s::launch_ds_select(d, params->cells, params->lambda, params->keep, rho,
+                                          pbar_c, keep_idx, fused_opt, prio_c_opt,
+                                          static_cast<hipStream_t>(stream)));
+}
+
 e2s_status e2s_prune(const e2s_shape* shape, const e2s_params* params, const void* q,
                      const void* k, void* workspace, size_t workspace_bytes, int32_t* keep_idx,
                      float* fused_opt, float* prio_c_opt, void* stream) {
     Dims d;
-    E2S_TRY(e2s::check_shape(shape, &d));
-    E2S_TRY(e2s::check_score_params(params));
+    E2S_TRY(check_score_inputs(shape, params, q, k, workspace, workspace_bytes, &d));
     E2S_TRY(e2s::check_select_params(params, d));
-    E2S_TRY(need(q));
-    E2S_TRY(need(k));
-    E2S_TRY(need(workspace));
     if (params->keep > 0) E2S_TRY(need(keep_idx));
-    E2S_TRY(e2s::check_aligned(q, 16));
-    E2S_TRY(e2s::check_aligned(k, 16));
-    E2S_TRY(e2s::check_aligned(workspace, 256));
     E2S_TRY(aligned_opt(keep_idx, 4));
     E2S_TRY(aligned_opt(fused_opt, 4));
     E2S_TRY(aligned_opt(prio_c_opt, 4));
-    if (workspace_bytes < e2s::prune_workspace_bytes(d)) return E2S_ERR_WORKSPACE_TOO_SMALL;
 
     const hipStream_t st = static_cast<hipStream_t>(stream);
-    if (params->mode == E2S_SCORE_MEAN_LOGIT && e2s::layer_evidence_fits(d)) {
-        // one workgroup per layer keeps the supports in LDS: rho, pbar_c in the workspace
-        float* rho = static_cast<float*>(workspace);
-        float* pbar = rho + d.B * d.L * d.N;
-        E2S_TRY(from_hip(e2s::launch_layer_evidence(d, params->dtype, effective_scale(params, d),
-                                                    q, k, rho, pbar, st)));
-        return from_hip(e2s::launch_ds_select(d, params->cells, params->lambda, params->keep, rho,
-                                              pbar, keep_idx, fused_opt, prio_c_opt, st));
-    }
-    float* support_c = static_cast<float*>(workspace);
-    const size_t e_bytes = e2s::prune_region_bytes(d);
-    float* prio_c = prio_c_opt ? prio_c_opt
-                               : reinterpret_cast<float*>(static_cast<char*>(workspace) + e_bytes);
-    E2S_TRY(run_score(d, params, q, k, support_c, nullptr, st));
-    E2S_TRY(from_hip(e2s::launch_fuse_evidence(d, support_c, fused_opt, nullptr, prio_c, st)));
-    return from_hip(e2s::launch_spatial_select(d, params->cells, params->lambda, params->keep,
-                                               prio_c, keep_idx, nullptr, nullptr, st));
+    char* ws = static_cast<char*>(workspace);
+    float* rho = reinterpret_cast<float*>(ws + e2s::support_region_bytes(d));
+    float* pbar_c = reinterpret_cast<float*>(ws + e2s::support_region_bytes(d) +
+                                             e2s::layer_region_bytes(d));
+    E2S_TRY(run_layer_reliability(d, params, q, k, workspace, rho, pbar_c, st));
+    return from_hip(e2s::launch_ds_select(d, params->cells, params->lambda, params->keep, rho,
+                                          pbar_c, keep_idx, fused_opt, prio_c_opt, st));
 }
 
 }  // extern "C"

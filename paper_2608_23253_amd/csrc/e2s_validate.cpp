@@ -63,15 +63,16 @@ e2s_status check_select_params(const e2s_params* p, const Dims& d) {
     return E2S_OK;
 }
 
-size_t prune_region_bytes(const Dims& d) {
-    const size_t e = static_cast<size_t>(d.B * d.L * d.H * d.N) * sizeof(float);
-    const size_t rel = 2 * static_cast<size_t>(d.B * d.L * d.N) * sizeof(float);
-    return align_up(e > rel ? e : rel, 256);
+size_t support_region_bytes(const Dims& d) {
+    return align_up(static_cast<size_t>(d.B * d.L * d.H * d.N) * sizeof(float), 256);
+}
+
+size_t layer_region_bytes(const Dims& d) {
+    return align_up(static_cast<size_t>(d.B * d.L * d.N) * sizeof(float), 256);
 }
 
 size_t prune_workspace_bytes(const Dims& d) {
-    const size_t c = static_cast<size_t>(d.B * d.N) * sizeof(float);
-    return prune_region_bytes(d) + align_up(c, 256);
+    return support_region_bytes(d) + 2 * layer_region_bytes(d);
 }
 
 }  // namespace e2s

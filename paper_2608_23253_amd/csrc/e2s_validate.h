@@ -23,10 +23,11 @@ e2s_status check_score_params(const e2s_params* p);
 e2s_status check_select_params(const e2s_params* p, const Dims& d);
 e2s_status check_aligned(const void* ptr, size_t align);
 
-// Bytes of e2s_prune's workspace: a first region holding either the supports
-// e [B,L,H,N] f32 or rho and pbar_c [B,L,N] f32 (whichever is larger), then the
-// priorities c [B,N] f32, each rounded up to 256 bytes.
-size_t prune_region_bytes(const Dims& d);
+// Workspace of e2s_layer_reliability and e2s_prune: the supports e [B,L,H,N] f32
+// (used only when a layer's supports do not stay on chip), then rho and pbar_c
+// [B,L,N] f32 (e2s_prune), each region rounded up to 256 bytes.
+size_t support_region_bytes(const Dims& d);
+size_t layer_region_bytes(const Dims& d);
 size_t prune_workspace_bytes(const Dims& d);
 size_t align_up(size_t x, size_t a);
 

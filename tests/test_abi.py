@@ -45,12 +45,24 @@ def prune(shape, params, q=A, k=A, ws=A, ws_bytes=None, out=A):
                          None, None, None)
 
 
+def layer_rel(shape, params, q=A, k=A, ws=A, ws_bytes=None, rho=A, pbar=A):
+    if ws_bytes is None:
+        ws_bytes = L.workspace_size(shape, params)
+    return lib.e2s_layer_reliability(ctypes.byref(shape), ctypes.byref(params), q, k, ws,
+                                     ws_bytes, rho, pbar, None)
+
+
+def fuse_sel(shape, params, rho=A, pbar=A, out=A, fused=None, prio=None):
+    return lib.e2s_fuse_select(ctypes.byref(shape), ctypes.byref(params), rho, pbar, out, fused,
+                               prio, None)
+
+
 def test_exports_every_declared_entry_point():
     names = L.header_entry_points()
-    assert len(names) == 10
+    assert len(names) == 12
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.e2s_abi_version() == 1
+    assert lib.e2s_abi_version() == 2
 
 
 def test_status_strings():
@@ -81,6 +93,8 @@ def test_bad_shapes(field, value, expect):
 ])
 def test_bad_score_params(field, value):
     assert score(good_shape(), good_params(**{field: value})) == L.ERR_BAD_PARAM
+    assert layer_rel(good_shape(), good_params(**{field: value}), ws_bytes=1 << 30) == \
+        L.ERR_BAD_PARAM
 
 
 @pytest.mark.parametrize("field,value", [
@@ -91,6 +105,7 @@ def test_bad_select_params(field, value):
     # grid 6x7 = 42 tokens: cells <= 6, keep <= 42
     assert select(good_shape(), good_params(**{field: value})) == L.ERR_BAD_PARAM
     assert prune(good_shape(), good_params(**{field: value}), ws_bytes=1 << 30) == L.ERR_BAD_PARAM
+    assert fuse_sel(good_shape(), good_params(**{field: value})) == L.ERR_BAD_PARAM
 
 
 def test_null_pointers():
@@ -110,6 +125,10 @@ def test_null_pointers():
         L.ERR_NULL_POINTER
     assert lib.e2s_fuse_evidence(ctypes.byref(sh), None, None, None, A, None) == \
         L.ERR_NULL_POINTER
+    for kw in ({"q": None}, {"k": None}, {"ws": None}, {"rho": None}, {"pbar": None}):
+        assert layer_rel(good_shape(), good_params(), **kw) == L.ERR_NULL_POINTER, kw
+    for kw in ({"rho": None}, {"pbar": None}, {"out": None}):
+        assert fuse_sel(good_shape(), good_params(), **kw) == L.ERR_NULL_POINTER, kw
     n = ctypes.c_size_t()
     assert lib.e2s_prune_workspace_size(None, ctypes.byref(good_params()), ctypes.byref(n)) == \
         L.ERR_NULL_POINTER
@@ -121,15 +140,21 @@ def test_misaligned_pointers():
     assert score(good_shape(), good_params(), e=A + 2) == L.ERR_MISALIGNED
     assert select(good_shape(), good_params(), adj=A + 4) == L.ERR_MISALIGNED
     assert prune(good_shape(), good_params(), ws=A + 16) == L.ERR_MISALIGNED
+    assert layer_rel(good_shape(), good_params(), ws=A + 16) == L.ERR_MISALIGNED
+    assert layer_rel(good_shape(), good_params(), q=A + 4) == L.ERR_MISALIGNED
+    assert layer_rel(good_shape(), good_params(), rho=A + 2) == L.ERR_MISALIGNED
+    assert fuse_sel(good_shape(), good_params(), pbar=A + 1) == L.ERR_MISALIGNED
+    assert fuse_sel(good_shape(), good_params(), prio=A + 2) == L.ERR_MISALIGNED
 
 
 def test_workspace_size_and_too_small():
     sh, pa = good_shape(), good_params()
     need = L.workspace_size(sh, pa)
-    e = 2 * 3 * 4 * 42 * 4
-    c = 2 * 42 * 4
-    assert need == -(-e // 256) * 256 + -(-c // 256) * 256
+    e = 2 * 3 * 4 * 42 * 4          # supports [B, L, H, N]
+    rel = 2 * 3 * 42 * 4            # rho or pbar_c [B, L, N]
+    assert need == -(-e // 256) * 256 + 2 * (-(-rel // 256) * 256)
     assert prune(sh, pa, ws_bytes=need - 1) == L.ERR_WORKSPACE_TOO_SMALL
+    assert layer_rel(sh, pa, ws_bytes=need - 1) == L.ERR_WORKSPACE_TOO_SMALL
 
 
 def test_keep_zero_allows_null_output():
@@ -138,6 +163,7 @@ def test_keep_zero_allows_null_output():
     output pointer, stops it before any launch."""
     assert select(good_shape(), good_params(keep=0), c=A + 2, out=None) == L.ERR_MISALIGNED
     assert select(good_shape(), good_params(keep=1), c=A + 2, out=None) == L.ERR_NULL_POINTER
+    assert fuse_sel(good_shape(), good_params(keep=0), rho=A + 2, out=None) == L.ERR_MISALIGNED
 
 
 def test_binding_rejects_cpu_tensors():

@@ -87,10 +87,17 @@ def _run_case(cfg, mode):
     keep, adj, rep = E.spatial_select(prio, gh, gw, K, G, lam, want_adj=True, want_rep=True)
     keep_p, fused_p, prio_p = E.prune(qd, kd, gh, gw, K, G, lam, mode, want_fused=True,
                                       want_prio=True)
+    rho_l, pbar_l = E.layer_reliability(qd, kd, gh, gw, mode)
+    keep_f, fused_f, prio_f = E.fuse_select(rho, pbar, gh, gw, K, G, lam, want_fused=True,
+                                            want_prio=True)
     torch.cuda.synchronize()
 
-    # fused / end-to-end entry points return exactly the staged bits
+    # fused / end-to-end entry points return exactly the staged bits (the on-chip
+    # layer path for one query head per key head in the mean-of-logits reading, the
+    # staged kernels otherwise)
     assert torch.equal(fused, f2) and torch.equal(conflict, c2) and torch.equal(prio, p2)
+    assert torch.equal(rho, rho_l) and torch.equal(pbar, pbar_l)
+    assert torch.equal(keep, keep_f) and torch.equal(fused, fused_f) and torch.equal(prio, prio_f)
     assert torch.equal(fused, fused_p) and torch.equal(prio, prio_p)
     assert torch.equal(keep, keep_p)
 

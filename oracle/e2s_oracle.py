@@ -35,6 +35,11 @@ import numpy as np
 
 SCORE_MODES = ("mean_logit", "mean_prob")
 
+# The full method and the ablation variants of Sec. 5 (ablation study, Table 2);
+# each removes or replaces one component, as read in prune_stage.
+VARIANTS = ("full", "a1_attention_topk", "a2_no_head_reliability", "a3_no_layer_fusion",
+            "a4_no_conflict_protection", "a5_no_spatial_novelty")
+
 
 # ---------------------------------------------------------------------------
 # Stage 1 inputs: text-to-visual attention (Sec. 3.1 and 4.1)
@@ -150,16 +155,23 @@ def dempster_step(acc: np.ndarray, m: np.ndarray):
     return fused, np.where(ok, K, 1.0)
 
 
-def ds_combine_layers(masses: np.ndarray):
+def ds_combine_layers(masses: np.ndarray, init: np.ndarray | None = None):
     """Eq. (12)-(19) over the source layers in order (axis 0 of masses [L, N, 3]).
 
-    Returns (fused [N,3], conflict [L,N] with row 0 = 0, Pl [N], q [N], Bel [N]).
+    Without `init` the recursion starts from the first layer (Eq. 12) and
+    conflict row 0 is 0.  With `init` [N, 3], the cumulative mass carried from
+    earlier pruning operations, every layer is combined onto it and row l holds
+    the conflict of that layer's step.
+    Returns (fused [N,3], conflict [L,N], Pl [N], q [N], Bel [N]).
     """
     masses = np.asarray(masses, dtype=np.float64)
     L = masses.shape[0]
-    acc = masses[0].copy()                                    # Eq. (12)
     conflict = np.zeros(masses.shape[:2], dtype=np.float64)
-    for l in range(1, L):
+    if init is None:
+        acc, first = masses[0].copy(), 1                      # Eq. (12)
+    else:
+        acc, first = np.asarray(init, dtype=np.float64).copy(), 0
+    for l in range(first, L):
         acc, conflict[l] = dempster_step(acc, masses[l])
     bel = acc[..., 0]                                         # Eq. (17)
     pl = acc[..., 0] + acc[..., 2]                            # Eq. (18)
@@ -171,34 +183,39 @@ def ds_combine_layers(masses: np.ndarray):
 # Spatial novelty and top-K (Sec. 4.3)
 # ---------------------------------------------------------------------------
 
-def cell_of_token(grid_h: int, grid_w: int, cells: int) -> np.ndarray:
-    """Cell id of every token of a grid_h x grid_w raster under a G x G partition."""
-    n = np.arange(grid_h * grid_w)
+def cell_of_token(grid_h: int, grid_w: int, cells: int, pos: np.ndarray | None = None) -> np.ndarray:
+    """Cell id of every token of a grid_h x grid_w raster under a G x G partition
+    (of the tokens at raster positions `pos`, default all of them in order)."""
+    n = np.arange(grid_h * grid_w) if pos is None else np.asarray(pos, dtype=np.int64)
     row, col = n // grid_w, n % grid_w
     return (row * cells // grid_h) * cells + (col * cells // grid_w)
 
 
-def cell_representatives(q: np.ndarray, grid_h: int, grid_w: int, cells: int) -> np.ndarray:
+def cell_representatives(q: np.ndarray, grid_h: int, grid_w: int, cells: int,
+                         pos: np.ndarray | None = None) -> np.ndarray:
     """Eq. (20)-(21): b_n = 1 for the highest-q token of each occupied cell.
 
-    Ties go to the lowest token index (np.argmax returns the first maximum)."""
+    q[i] belongs to the token at raster position pos[i] (default i; positions
+    ascending).  A cell is occupied when it holds at least one of these tokens.
+    Ties go to the lowest index (np.argmax returns the first maximum)."""
     q = np.asarray(q, dtype=np.float64)
-    cell = cell_of_token(grid_h, grid_w, cells)
+    cell = cell_of_token(grid_h, grid_w, cells, pos)
     b = np.zeros(q.shape[0], dtype=np.int64)
     for g in range(cells * cells):
-        members = np.nonzero(cell == g)[0]          # ascending token indices
+        members = np.nonzero(cell == g)[0]          # ascending indices
         if members.size:
             b[members[int(np.argmax(q[members]))]] = 1
     return b
 
 
 def spatial_select(q: np.ndarray, grid_h: int, grid_w: int, cells: int, lam: float,
-                   keep: int):
+                   keep: int, pos: np.ndarray | None = None):
     """Eq. (20)-(23): representatives, q~ = (1-lam) q + lam b, keep the K largest q~.
 
-    Ties in q~ go to the lowest index.  Returns (kept ascending [K], q~ [N], b [N])."""
+    Ties in q~ go to the lowest index.  Returns (kept ascending [K], q~ [N], b [N]),
+    indices into q."""
     q = np.asarray(q, dtype=np.float64)
-    b = cell_representatives(q, grid_h, grid_w, cells)
+    b = cell_representatives(q, grid_h, grid_w, cells, pos)
     qt = (1.0 - lam) * q + lam * b                            # Eq. (22)
     idx = np.arange(q.shape[0])
     order = np.lexsort((idx, -qt))                            # by -q~, then index
@@ -218,33 +235,134 @@ class ImageResult:
     pbar: np.ndarray       # [L, N]     mean support
     masses: np.ndarray     # [L, N, 3]  layer masses (Eq. 11)
     fused: np.ndarray      # [N, 3]     cumulative fused mass after the last layer
-    conflict: np.ndarray   # [L, N]     K^(l), row 0 = 0 (Eq. 13)
+    conflict: np.ndarray   # [L, N]     K^(l) of each step (Eq. 13)
     pl: np.ndarray         # [N]        plausibility of I (Eq. 18)
     q: np.ndarray          # [N]        retention priority (Eq. 19)
     qt: np.ndarray         # [N]        spatially adjusted score (Eq. 22)
     is_rep: np.ndarray     # [N]        representative indicator b (Eq. 21)
-    keep: np.ndarray       # [K]        kept tokens, ascending (Eq. 23)
+    keep: np.ndarray       # [K]        kept entries, ascending (Eq. 23)
+    score: np.ndarray | None = None   # [N] ranking score of the A1 variant
+    keep_pos: np.ndarray | None = None   # [K] raster positions of the kept entries
+    m_out: np.ndarray | None = None      # [K, 3] fused mass of the kept entries
+
+
+def prune_stage(q: np.ndarray, k: np.ndarray, cand_pos: np.ndarray, grid_h: int, grid_w: int,
+                keep: int, cells: int = 4, lam: float = 0.1, mode: str = "mean_logit",
+                scale: float | None = None, m_prev: np.ndarray | None = None,
+                variant: str = "full") -> ImageResult:
+    """One pruning operation of Algorithm 1 for one image.
+
+    q: [L, H, N_T, d] text queries of the operation's L evidence layers;
+    k: [L, Hkv, N_l, d] keys of the N_l current candidates, in candidate order;
+    cand_pos: [N_l] the candidates' raster positions on the grid_h x grid_w grid,
+    ascending; m_prev: [N_l, 3] their cumulative fused mass from the earlier
+    operations (None for the first).  N_l is the N_l of Eq. (9) and the softmax of
+    Eq. (8) runs over the candidates.  Returns indices into the candidate list, the
+    kept positions and the kept tokens' fused masses (carried to the next
+    operation).
+
+    Ablation variants (Sec. 5, Table 2), each changing one component:
+      a1_attention_topk          top-K of the attention r averaged over the
+                                 operation's layers and heads; no evidence, no
+                                 carried mass, no spatial term
+      a2_no_head_reliability     rho = 1 in Eq. (11): Bayesian layer masses
+      a3_no_layer_fusion         only the operation's last layer's masses; no
+                                 Dempster combination with earlier layers or
+                                 operations, so K = 0 and q = Pl
+      a4_no_conflict_protection  q = Pl(I) instead of Eq. (19)
+      a5_no_spatial_novelty      lambda = 0 in Eq. (22)
+    """
+    if variant not in VARIANTS:
+        raise ValueError(f"unknown variant {variant!r}")
+    cand_pos = np.asarray(cand_pos, dtype=np.int64)
+    n_l = k.shape[2]
+    if cand_pos.shape != (n_l,):
+        raise ValueError("cand_pos must list the raster position of every candidate")
+    r, p = score_heads(q, k, mode, scale)
+    if variant == "a1_attention_topk":
+        score = r.mean(axis=(0, 1))                           # [N_l]
+        idx = np.arange(n_l)
+        kept = np.sort(np.lexsort((idx, -score))[:keep]).astype(np.int64)
+        nan = np.full(n_l, np.nan)
+        return ImageResult(r, p, nan, nan, np.full((1, n_l, 3), np.nan), np.full((n_l, 3), np.nan),
+                           np.zeros((1, n_l)), nan, nan, nan, np.zeros(n_l, np.int64), kept,
+                           score=score, keep_pos=cand_pos[kept], m_out=None)
+    rho, pbar = head_reliability(p)
+    if variant == "a2_no_head_reliability":
+        rho = np.ones_like(rho)
+    masses = head_masses(rho, pbar)
+    if variant == "a3_no_layer_fusion":
+        fused, conflict, pl, prio, _ = ds_combine_layers(masses[-1:])
+    else:
+        fused, conflict, pl, prio, _ = ds_combine_layers(masses, m_prev)
+    if variant == "a4_no_conflict_protection":
+        prio = pl
+    if variant == "a5_no_spatial_novelty":
+        lam = 0.0
+    kept, qt, b = spatial_select(prio, grid_h, grid_w, cells, lam, keep, cand_pos)
+    return ImageResult(r, p, rho, pbar, masses, fused, conflict, pl, prio, qt, b, kept,
+                       keep_pos=cand_pos[kept], m_out=fused[kept])
 
 
 def prune_image(q: np.ndarray, k: np.ndarray, grid_h: int, grid_w: int, keep: int,
                 cells: int = 4, lam: float = 0.1, mode: str = "mean_logit",
-                scale: float | None = None) -> ImageResult:
-    """Algorithm 1 for one image with all evidence layers fused before one top-K.
+                scale: float | None = None, variant: str = "full") -> ImageResult:
+    """Algorithm 1 for one image with all evidence layers fused before one top-K
+    (one pruning operation over every visual token).
 
     q: [L, H, N_T, d]; k: [L, Hkv, N_V, d] with N_V = grid_h * grid_w."""
     if k.shape[2] != grid_h * grid_w:
         raise ValueError("N_V must equal grid_h * grid_w")
-    r, p = score_heads(q, k, mode, scale)
-    rho, pbar = head_reliability(p)
-    masses = head_masses(rho, pbar)
-    fused, conflict, pl, prio, _ = ds_combine_layers(masses)
-    kept, qt, b = spatial_select(prio, grid_h, grid_w, cells, lam, keep)
-    return ImageResult(r, p, rho, pbar, masses, fused, conflict, pl, prio, qt, b, kept)
+    return prune_stage(q, k, np.arange(grid_h * grid_w), grid_h, grid_w, keep, cells, lam, mode,
+                       scale, None, variant)
 
 
 def prune(q: np.ndarray, k: np.ndarray, grid_h: int, grid_w: int, keep: int,
           cells: int = 4, lam: float = 0.1, mode: str = "mean_logit",
-          scale: float | None = None):
+          scale: float | None = None, variant: str = "full"):
     """prune_image over a batch: q [B, L, H, N_T, d], k [B, L, Hkv, N_V, d]."""
-    return [prune_image(q[b], k[b], grid_h, grid_w, keep, cells, lam, mode, scale)
+    return [prune_image(q[b], k[b], grid_h, grid_w, keep, cells, lam, mode, scale, variant)
             for b in range(q.shape[0])]
+
+
+# ---------------------------------------------------------------------------
+# Progressive schedule (Algorithm 1 with shrinking candidate sets; Sec. 5.1)
+# ---------------------------------------------------------------------------
+
+def prune_progressive(q_ops, k_ops, grid_h: int, grid_w: int, budgets, cells: int = 4,
+                      lam: float = 0.1, mode: str = "mean_logit", scale: float | None = None,
+                      variant: str = "full"):
+    """Algorithm 1 for one image over a sequence of pruning operations.
+
+    q_ops[s]: [L_s, H, N_T, d] text queries of operation s; k_ops[s]: [L_s, Hkv,
+    N_V, d] keys of every visual token at operation s's layers (the operation sees
+    only the rows of its current candidates); budgets[s]: K_s, non-increasing.
+    Operation s keeps budgets[s] of its candidates and hands them, with their
+    fused masses, to operation s + 1.  Returns the list of per-operation results;
+    result.keep_pos of the last is the retained set V."""
+    cand = np.arange(grid_h * grid_w)
+    m_prev = None
+    out = []
+    for s, keep in enumerate(budgets):
+        if keep > cand.size:
+            raise ValueError("a budget exceeds the candidates left")
+        res = prune_stage(q_ops[s], k_ops[s][:, :, cand, :], cand, grid_h, grid_w, keep, cells,
+                          lam, mode, scale, m_prev, variant)
+        out.append(res)
+        cand = res.keep_pos
+        m_prev = res.m_out
+    return out
+
+
+def avg_tokens(num_layers: int, n_visual: int, prune_after, kept) -> float:
+    """Eq. (24): mean over the num_layers LLM layers of the visual tokens each
+    layer processes, when pruning after layers prune_after[j] (1-based) leaves
+    kept[j] tokens for the layers that follow."""
+    counts = []
+    for i in range(1, num_layers + 1):
+        t = n_visual
+        for a, kj in zip(prune_after, kept):
+            if i > a:
+                t = kj
+        counts.append(t)
+    return sum(counts) / num_layers

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define E2S_ABI_VERSION 2
+#define E2S_ABI_VERSION 3
 
 #if defined(__GNUC__) || defined(__clang__)
 #define E2S_API __attribute__((visibility("default")))
@@ -84,6 +84,26 @@ typedef struct {
     int32_t grid_w;        /* visual grid cols >= 1; N = grid_h*grid_w <= 16384 */
 } e2s_shape;
 
+/* The full method and the ablation variants of the paper's ablation study (Sec. 5,
+ * Table 2), each removing or replacing one component.  Honoured by e2s_prune and
+ * e2s_prune_stage (all) and e2s_fuse_select (all but ATTENTION_TOPK, which needs
+ * the per-head supports); the staged entry points always compute the full method.
+ *  ATTENTION_TOPK      (A1) keep the K tokens of largest attention r averaged over
+ *                      the layers and heads; no evidence, no spatial term
+ *  NO_HEAD_RELIABILITY (A2) rho = 1 in Eq. 11 (Bayesian layer masses)
+ *  NO_LAYER_FUSION     (A3) the last layer's masses only: no Dempster combination
+ *                      with earlier layers or operations, so K = 0 and q = Pl
+ *  NO_CONFLICT         (A4) q = Pl(I) instead of Eq. 19
+ *  NO_SPATIAL_NOVELTY  (A5) lambda = 0 in Eq. 22                                  */
+typedef enum {
+    E2S_VARIANT_FULL = 0,
+    E2S_VARIANT_ATTENTION_TOPK = 1,
+    E2S_VARIANT_NO_HEAD_RELIABILITY = 2,
+    E2S_VARIANT_NO_LAYER_FUSION = 3,
+    E2S_VARIANT_NO_CONFLICT = 4,
+    E2S_VARIANT_NO_SPATIAL_NOVELTY = 5
+} e2s_variant;
+
 typedef struct {
     int32_t dtype;   /* e2s_dtype of q and k                                     */
     int32_t mode;    /* e2s_score_mode                                           */
@@ -91,6 +111,7 @@ typedef struct {
     int32_t cells;   /* G: cells per side, 1 <= G <= min(grid_h, grid_w) (paper: 4) */
     float lambda;    /* novelty weight of Eq. 22, finite, in [0, 1] (paper: 0.1) */
     int32_t keep;    /* K of Eq. 23, 0 <= K <= N                                 */
+    int32_t variant; /* an e2s_variant; 0 is the full method                       */
 } e2s_params;
 
 /* Score stage (Sec. 3.1 Eq. 1; Sec. 4.1 Eq. 8-9).
@@ -160,12 +181,12 @@ E2S_API e2s_status e2s_layer_reliability(const e2s_shape* shape, const e2s_param
                                  void* stream);
 
 /* Masses, fusion and selection in one call (Sec. 4.1 Eq. 11; Sec. 4.2 Eq. 12-19;
- * Sec. 4.3 Eq. 20-23) from rho, pbar_c [B, L, N]; one workgroup per image.  The
- * results are bit-identical to e2s_head_masses -> e2s_ds_combine_layers ->
- * e2s_spatial_select.
+ * Sec. 4.3 Eq. 20-23) from rho, pbar_c [B, L, N]; one workgroup per image.  With
+ * the full method the results are bit-identical to e2s_head_masses ->
+ * e2s_ds_combine_layers -> e2s_spatial_select.
  *   keep_idx [B, K] int32 out (NULL iff K == 0); fused_opt [B, N, 3] and
  *   prio_c_opt [B, N] f32 out or NULL.
- * Uses params->cells, lambda and keep. */
+ * Uses params->cells, lambda, keep and variant (ATTENTION_TOPK: E2S_ERR_UNSUPPORTED). */
 E2S_API e2s_status e2s_fuse_select(const e2s_shape* shape, const e2s_params* params,
                            const float* rho, const float* pbar_c, int32_t* keep_idx,
                            float* fused_opt, float* prio_c_opt, void* stream);
@@ -180,10 +201,37 @@ E2S_API e2s_status e2s_prune_workspace_size(const e2s_shape* shape, const e2s_pa
  * `workspace` (256-byte aligned, >= e2s_prune_workspace_size bytes, contents
  * undefined on return); the result equals the staged calls bit for bit.
  *   keep_idx [B, K] int32 out (NULL iff K == 0); fused_opt [B, N, 3] and
- *   prio_c_opt [B, N] f32 out or NULL. */
+ *   prio_c_opt [B, N] f32 out or NULL (not written by ATTENTION_TOPK).
+ * Honours params->variant. */
 E2S_API e2s_status e2s_prune(const e2s_shape* shape, const e2s_params* params, const void* q,
                      const void* k, void* workspace, size_t workspace_bytes,
                      int32_t* keep_idx, float* fused_opt, float* prio_c_opt, void* stream);
+
+/* One pruning operation of Algorithm 1 over the current candidate tokens: the
+ * progressive schedule (Sec. 4, Algorithm 1; Sec. 5.1) calls it once per pruning
+ * layer with the survivors of the previous call.  shape describes the ORIGINAL
+ * grid (cells of Eq. 20) and the operation's L evidence layers; num_cand = N_l
+ * candidates, 1 <= N_l <= grid_h * grid_w, 0 <= params->keep <= N_l.
+ *   q        [B, L, H, N_T, d]    text queries at the operation's layers
+ *   k        [B, L, Hkv, N_l, d]  keys of the candidates, in candidate order
+ *   cand_pos_opt [B, N_l] int32 or NULL: raster positions of the candidates,
+ *            ascending (then index ties are position ties); NULL means positions
+ *            0 .. N_l-1.  A cell is occupied when it holds a candidate; a position
+ *            outside the grid gives its token no cell.
+ *   m_prev_opt [B, N_l, 3] f32 or NULL: the candidates' fused masses after the
+ *            previous operation (its m_out); every layer is combined onto them
+ *   keep_idx [B, K] int32 out: kept candidate indices, ascending (NULL iff K == 0)
+ *   keep_pos_opt [B, K] int32 out or NULL: their raster positions
+ *   m_out_opt [B, K, 3] f32 out or NULL: their fused masses, the next call's m_prev
+ * N_l is the N_l of Eq. 9 and the softmax of Eq. 8 runs over the candidates.
+ * workspace: 256-byte aligned, >= e2s_prune_workspace_size(shape, params) bytes.
+ * With num_cand = grid_h * grid_w and NULL optional arguments the result equals
+ * e2s_prune's. */
+E2S_API e2s_status e2s_prune_stage(const e2s_shape* shape, const e2s_params* params,
+                           int32_t num_cand, const void* q, const void* k,
+                           const int32_t* cand_pos_opt, const float* m_prev_opt,
+                           void* workspace, size_t workspace_bytes, int32_t* keep_idx,
+                           int32_t* keep_pos_opt, float* m_out_opt, void* stream);
 
 /* Static description of a status code (never NULL). */
 E2S_API const char* e2s_status_string(e2s_status status);

@@ -7,7 +7,8 @@ HIP kernels.  Two layers are exposed:
     the C entry points can be called directly with raw pointers;
   * functions with the C names minus the ``e2s_`` prefix (``score_heads``,
     ``head_reliability``, ``head_masses``, ``ds_combine_layers``,
-    ``fuse_evidence``, ``spatial_select``, ``prune``) that take torch tensors on
+    ``fuse_evidence``, ``spatial_select``, ``layer_reliability``, ``fuse_select``,
+    ``prune``, ``prune_stage``) that take torch tensors on
     the GPU, allocate the outputs with torch, pass raw device pointers and the
     current torch stream, and raise ``E2SError`` on a non-zero status.
 
@@ -33,6 +34,9 @@ OK, ERR_NULL_POINTER, ERR_BAD_SHAPE, ERR_BAD_PARAM, ERR_UNSUPPORTED, ERR_MISALIG
 DTYPE_F32, DTYPE_BF16 = 0, 1
 MEAN_LOGIT, MEAN_PROB = 0, 1
 MODES = {"mean_logit": MEAN_LOGIT, "mean_prob": MEAN_PROB}
+# e2s_variant: the full method and the ablation variants A1-A5
+VARIANTS = {"full": 0, "a1_attention_topk": 1, "a2_no_head_reliability": 2,
+            "a3_no_layer_fusion": 3, "a4_no_conflict_protection": 4, "a5_no_spatial_novelty": 5}
 
 
 class Shape(ctypes.Structure):
@@ -44,7 +48,8 @@ class Shape(ctypes.Structure):
 
 class Params(ctypes.Structure):
     _fields_ = [("dtype", ctypes.c_int32), ("mode", ctypes.c_int32), ("scale", ctypes.c_float),
-                ("cells", ctypes.c_int32), ("lam", ctypes.c_float), ("keep", ctypes.c_int32)]
+                ("cells", ctypes.c_int32), ("lam", ctypes.c_float), ("keep", ctypes.c_int32),
+                ("variant", ctypes.c_int32)]
 
 
 class E2SError(RuntimeError):
@@ -68,6 +73,8 @@ _SIGNATURES = {
     "e2s_fuse_select": [_SH, _PA, _P, _P, _P, _P, _P, _P],
     "e2s_prune_workspace_size": [_SH, _PA, ctypes.POINTER(ctypes.c_size_t)],
     "e2s_prune": [_SH, _PA, _P, _P, _P, ctypes.c_size_t, _P, _P, _P, _P],
+    "e2s_prune_stage": [_SH, _PA, ctypes.c_int32, _P, _P, _P, _P, _P, ctypes.c_size_t, _P, _P,
+                        _P, _P],
     "e2s_status_string": [ctypes.c_int],
     "e2s_abi_version": [],
 }
@@ -77,6 +84,15 @@ def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with "
                           "`python -m paper_2608_23253_amd.build` (or __graft_entry__.build())")
+    # Device memory and streams come from torch, whose wheel ships its own HIP
+    # runtime (libamdhip64.so, libhsa-runtime64.so).  Load it before the library:
+    # the library's libamdhip64.so.7 dependency then binds to that runtime.  Loaded
+    # the other way round, the process would hold two HIP runtimes that do not
+    # share device state (kernel attributes set through one fail on the other).
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     so = ctypes.CDLL(LIB_PATH)
     for name, args in _SIGNATURES.items():
         fn = getattr(so, name)
@@ -149,9 +165,10 @@ def make_shape(batch, num_layers, num_heads, num_kv_heads, head_dim, num_text, g
 
 
 def make_params(dtype=DTYPE_BF16, mode="mean_logit", scale=0.0, cells=4, lam=0.1,
-                keep=0) -> Params:
+                keep=0, variant="full") -> Params:
     m = MODES[mode] if isinstance(mode, str) else int(mode)
-    return Params(int(dtype), m, float(scale), int(cells), float(lam), int(keep))
+    v = VARIANTS[variant] if isinstance(variant, str) else int(variant)
+    return Params(int(dtype), m, float(scale), int(cells), float(lam), int(keep), v)
 
 
 def shape_from(q, k, grid_h: int, grid_w: int) -> Shape:
@@ -299,14 +316,14 @@ def layer_reliability(q, k, grid_h: int, grid_w: int, mode="mean_logit", scale: 
 
 
 def fuse_select(rho, pbar_c, grid_h: int, grid_w: int, keep: int, cells: int = 4,
-                lam: float = 0.1, want_fused=False, want_prio=False):
+                lam: float = 0.1, want_fused=False, want_prio=False, variant="full"):
     """Eq. 11-23 in one call: (keep_idx [B,K], fused [B,N,3] or None, prio_c [B,N] or None)."""
     torch = _torch()
     _check(rho, "rho", dtype=torch.float32, ndim=3)
     _check(pbar_c, "pbar_c", dtype=torch.float32, ndim=3)
     B, L, N = rho.shape
     sh = make_shape(B, L, 1, 1, 128, 1, grid_h, grid_w)
-    pa = make_params(cells=cells, lam=lam, keep=keep)
+    pa = make_params(cells=cells, lam=lam, keep=keep, variant=variant)
     dev = rho.device
     out = torch.empty((B, keep), device=dev, dtype=torch.int32)
     fused = torch.empty((B, N, 3), device=dev, dtype=torch.float32) if want_fused else None
@@ -328,12 +345,12 @@ class Pruner:
     """Holds the shape, params and workspace of repeated e2s_prune calls."""
 
     def __init__(self, q, k, grid_h: int, grid_w: int, keep: int, cells: int = 4,
-                 lam: float = 0.1, mode="mean_logit", scale: float = 0.0):
+                 lam: float = 0.1, mode="mean_logit", scale: float = 0.0, variant="full"):
         torch = _torch()
         _check(q, "q", ndim=5)
         _check(k, "k", dtype=q.dtype, ndim=5)
         self.shape = shape_from(q, k, grid_h, grid_w)
-        self.params = make_params(_dtype_code(q), mode, scale, cells, lam, keep)
+        self.params = make_params(_dtype_code(q), mode, scale, cells, lam, keep, variant)
         self.device = q.device
         self.workspace = torch.empty(workspace_size(self.shape, self.params), device=q.device,
                                      dtype=torch.uint8)
@@ -357,15 +374,81 @@ class Pruner:
 
 
 def prune(q, k, grid_h: int, grid_w: int, keep: int, cells: int = 4, lam: float = 0.1,
-          mode="mean_logit", scale: float = 0.0, want_fused=False, want_prio=False):
+          mode="mean_logit", scale: float = 0.0, want_fused=False, want_prio=False,
+          variant="full"):
     """The whole path: (keep_idx [B,K], fused [B,N,3] or None, prio_c [B,N] or None)."""
     torch = _torch()
-    p = Pruner(q, k, grid_h, grid_w, keep, cells, lam, mode, scale)
+    p = Pruner(q, k, grid_h, grid_w, keep, cells, lam, mode, scale, variant)
     B, N = p.shape.batch, grid_h * grid_w
     fused = torch.empty((B, N, 3), device=q.device, dtype=torch.float32) if want_fused else None
     prio = torch.empty((B, N), device=q.device, dtype=torch.float32) if want_prio else None
     idx = p(q, k, fused, prio)
     return idx, fused, prio
+
+
+class StagePruner:
+    """Repeated calls of one pruning operation of a progressive schedule
+    (e2s_prune_stage): the original grid, the operation's layers and its budget."""
+
+    def __init__(self, q, k, grid_h: int, grid_w: int, keep: int, cells: int = 4,
+                 lam: float = 0.1, mode="mean_logit", scale: float = 0.0, variant="full"):
+        torch = _torch()
+        _check(q, "q", ndim=5)
+        _check(k, "k", dtype=q.dtype, ndim=5)
+        B, L, H, NT, D = q.shape
+        self.num_cand = int(k.shape[3])
+        if self.num_cand > grid_h * grid_w:
+            raise ValueError("more candidates than grid positions")
+        self.shape = make_shape(B, L, H, k.shape[2], D, NT, grid_h, grid_w)
+        self.params = make_params(_dtype_code(q), mode, scale, cells, lam, keep, variant)
+        self.device = q.device
+        self.workspace = torch.empty(workspace_size(self.shape, self.params), device=q.device,
+                                     dtype=torch.uint8)
+        self.keep_idx = torch.empty((B, keep), device=q.device, dtype=torch.int32)
+        self.keep_pos = torch.empty((B, keep), device=q.device, dtype=torch.int32)
+        self.m_out = torch.empty((B, keep, 3), device=q.device, dtype=torch.float32)
+
+    def __call__(self, q, k, cand_pos=None, m_prev=None, stream: Optional[int] = None):
+        torch = _torch()
+        _check(q, "q", ndim=5)
+        _check(k, "k", dtype=q.dtype, ndim=5)
+        B, N = self.shape.batch, self.num_cand
+        sh = self.shape
+        if tuple(q.shape) != (B, sh.num_layers, sh.num_heads, sh.num_text, sh.head_dim):
+            raise ValueError("q does not match the StagePruner's shape")
+        if tuple(k.shape) != (B, sh.num_layers, sh.num_kv_heads, N, sh.head_dim):
+            raise ValueError("k does not match the StagePruner's candidates")
+        if _dtype_code(q) != self.params.dtype:
+            raise TypeError("q/k dtype does not match the StagePruner's")
+        if cand_pos is not None:
+            _check(cand_pos, "cand_pos", dtype=torch.int32, ndim=2)
+            if tuple(cand_pos.shape) != (B, N):
+                raise ValueError("cand_pos must be [B, num_cand]")
+        if m_prev is not None:
+            _check(m_prev, "m_prev", dtype=torch.float32, ndim=3)
+            if tuple(m_prev.shape) != (B, N, 3):
+                raise ValueError("m_prev must be [B, num_cand, 3]")
+        st = _stream(self.device) if stream is None else stream
+        K = self.params.keep
+        _raise(_LIB.e2s_prune_stage(ctypes.byref(self.shape), ctypes.byref(self.params), N,
+                                    q.data_ptr(), k.data_ptr(), _ptr(cand_pos), _ptr(m_prev),
+                                    self.workspace.data_ptr(), self.workspace.numel(),
+                                    self.keep_idx.data_ptr() if K > 0 else None,
+                                    self.keep_pos.data_ptr() if K > 0 else None,
+                                    self.m_out.data_ptr() if K > 0 else None, st),
+               "e2s_prune_stage")
+        return self.keep_idx, self.keep_pos, self.m_out
+
+
+def prune_stage(q, k, grid_h: int, grid_w: int, keep: int, cand_pos=None, m_prev=None,
+                cells: int = 4, lam: float = 0.1, mode="mean_logit", scale: float = 0.0,
+                variant="full"):
+    """One pruning operation over the candidates whose keys k [B,L,Hkv,N_l,d] holds:
+    (keep_idx [B,K] candidate indices, keep_pos [B,K] raster positions,
+    m_out [B,K,3] fused masses for the next operation)."""
+    sp = StagePruner(q, k, grid_h, grid_w, keep, cells, lam, mode, scale, variant)
+    idx, pos, m = sp(q, k, cand_pos, m_prev)
+    return idx, pos, m
 
 
 def default_scale(head_dim: int) -> float:

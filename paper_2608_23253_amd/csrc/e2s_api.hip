@@ -56,17 +56,64 @@ e2s_status run_score(const Dims& d, const e2s_params* params, const void* q, con
         e2s::launch_score_mean_prob(d, params->dtype, scale, q, k, support_c, r_opt, st));
 }
 
-// Eq. 1, 8-10: per-layer rho and pbar_c, on chip when a layer fits, else through
-// the supports in `workspace`.
+// Compute units of the current device (cached per device).
+int device_cus() {
+    static int cached[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    if (cached[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
+            cached[dev] = n;
+    }
+    return cached[dev];
+}
+
+// Eq. 1, 8-10: per-layer rho and pbar_c, on chip when a layer fits and there are
+// enough layers to occupy the device with one workgroup each, else through the
+// supports in `workspace` (both give the same bits).
 e2s_status run_layer_reliability(const Dims& d, const e2s_params* params, const void* q,
                                  const void* k, void* workspace, float* rho, float* pbar_c,
                                  hipStream_t st) {
-    if (params->mode == E2S_SCORE_MEAN_LOGIT && e2s::layer_evidence_fits(d))
+    if (params->mode == E2S_SCORE_MEAN_LOGIT && e2s::layer_evidence_fits(d) &&
+        d.B * d.L >= device_cus())
         return from_hip(e2s::launch_layer_evidence(d, params->dtype, effective_scale(params, d), q,
                                                    k, rho, pbar_c, st));
     float* support_c = static_cast<float*>(workspace);
     E2S_TRY(run_score(d, params, q, k, support_c, nullptr, st));
     return from_hip(e2s::launch_head_reliability(d, support_c, rho, pbar_c, st));
+}
+
+e2s::SelectArgs select_args(const e2s_params* p, int32_t* keep_idx, float* fused,
+                            float* prio_c) {
+    e2s::SelectArgs a{};
+    a.cells = p->cells;
+    a.lambda = p->variant == E2S_VARIANT_NO_SPATIAL_NOVELTY ? 0.0f : p->lambda;
+    a.keep = p->keep;
+    a.variant = p->variant;
+    a.keep_idx = keep_idx;
+    a.fused = fused;
+    a.prio_c = prio_c;
+    return a;
+}
+
+// A pruning operation after validation: the evidence (or, for attention top-K, the
+// supports) of the operation's layers, then the selection tail.  d.N is the
+// candidate count.
+e2s_status run_operation(const Dims& d, const e2s_params* params, const void* q, const void* k,
+                         void* workspace, const e2s::SelectArgs& a, const float* m_prev,
+                         hipStream_t st) {
+    char* ws = static_cast<char*>(workspace);
+    if (params->variant == E2S_VARIANT_ATTENTION_TOPK) {
+        float* support_c = reinterpret_cast<float*>(ws);
+        E2S_TRY(run_score(d, params, q, k, support_c, nullptr, st));
+        return from_hip(e2s::launch_attention_select(d, a, support_c, st));
+    }
+    float* rho = reinterpret_cast<float*>(ws + e2s::support_region_bytes(d));
+    float* pbar_c =
+        reinterpret_cast<float*>(ws + e2s::support_region_bytes(d) + e2s::layer_region_bytes(d));
+    E2S_TRY(run_layer_reliability(d, params, q, k, workspace, rho, pbar_c, st));
+    return from_hip(e2s::launch_ds_select(d, a, rho, pbar_c, m_prev, st));
 }
 
 e2s_status check_score_inputs(const e2s_shape* shape, const e2s_params* params, const void* q,
@@ -219,9 +266,9 @@ e2s_status e2s_fuse_select(const e2s_shape* shape, const e2s_params* params, con
     E2S_TRY(aligned_opt(keep_idx, 4));
     E2S_TRY(aligned_opt(fused_opt, 4));
     E2S_TRY(aligned_opt(prio_c_opt, 4));
-    return from_hip(e2s::launch_ds_select(d, params->cells, params->lambda, params->keep, rho,
-                                          pbar_c, keep_idx, fused_opt, prio_c_opt,
-                                          static_cast<hipStream_t>(stream)));
+    if (params->variant == E2S_VARIANT_ATTENTION_TOPK) return E2S_ERR_UNSUPPORTED;
+    return from_hip(e2s::launch_ds_select(d, select_args(params, keep_idx, fused_opt, prio_c_opt),
+                                          rho, pbar_c, nullptr, static_cast<hipStream_t>(stream)));
 }
 
 e2s_status e2s_prune(const e2s_shape* shape, const e2s_params* params, const void* q,
@@ -235,14 +282,35 @@ e2s_status e2s_prune(const e2s_shape* shape, const e2s_params* params, const voi
     E2S_TRY(aligned_opt(fused_opt, 4));
     E2S_TRY(aligned_opt(prio_c_opt, 4));
 
-    const hipStream_t st = static_cast<hipStream_t>(stream);
-    char* ws = static_cast<char*>(workspace);
-    float* rho = reinterpret_cast<float*>(ws + e2s::support_region_bytes(d));
-    float* pbar_c = reinterpret_cast<float*>(ws + e2s::support_region_bytes(d) +
-                                             e2s::layer_region_bytes(d));
-    E2S_TRY(run_layer_reliability(d, params, q, k, workspace, rho, pbar_c, st));
-    return from_hip(e2s::launch_ds_select(d, params->cells, params->lambda, params->keep, rho,
-                                          pbar_c, keep_idx, fused_opt, prio_c_opt, st));
+    return run_operation(d, params, q, k, workspace,
+                         select_args(params, keep_idx, fused_opt, prio_c_opt), nullptr,
+                         static_cast<hipStream_t>(stream));
+}
+
+e2s_status e2s_prune_stage(const e2s_shape* shape, const e2s_params* params, int32_t num_cand,
+                           const void* q, const void* k, const int32_t* cand_pos_opt,
+                           const float* m_prev_opt, void* workspace, size_t workspace_bytes,
+                           int32_t* keep_idx, int32_t* keep_pos_opt, float* m_out_opt,
+                           void* stream) {
+    Dims d;
+    // the workspace of the full grid bounds that of any candidate subset
+    E2S_TRY(check_score_inputs(shape, params, q, k, workspace, workspace_bytes, &d));
+    if (num_cand < 1 || num_cand > d.N) return E2S_ERR_BAD_SHAPE;
+    if (cand_pos_opt == nullptr && num_cand != d.N) return E2S_ERR_BAD_SHAPE;
+    d.N = num_cand;
+    E2S_TRY(e2s::check_select_params(params, d));
+    if (params->keep > 0) E2S_TRY(need(keep_idx));
+    E2S_TRY(aligned_opt(cand_pos_opt, 4));
+    E2S_TRY(aligned_opt(m_prev_opt, 4));
+    E2S_TRY(aligned_opt(keep_idx, 4));
+    E2S_TRY(aligned_opt(keep_pos_opt, 4));
+    E2S_TRY(aligned_opt(m_out_opt, 4));
+    e2s::SelectArgs a = select_args(params, keep_idx, nullptr, nullptr);
+    a.cand_pos = cand_pos_opt;
+    a.keep_pos = keep_pos_opt;
+    a.m_out = m_out_opt;
+    return run_operation(d, params, q, k, workspace, a, m_prev_opt,
+                         static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

@@ -42,9 +42,24 @@ hipError_t launch_spatial_select(const Dims& d, int cells, float lambda, int kee
 bool layer_evidence_fits(const Dims& d);
 hipError_t launch_layer_evidence(const Dims& d, int dtype, float scale, const void* q,
                                  const void* k, float* rho, float* pbar_c, hipStream_t stream);
-// Eq. 11-19 from rho, pbar_c, then Eq. 20-23; fused and prio_c may be null.
-hipError_t launch_ds_select(const Dims& d, int cells, float lambda, int keep, const float* rho,
-                            const float* pbar_c, int32_t* keep_idx, float* fused, float* prio_c,
-                            hipStream_t stream);
+// Arguments of the selection tail of a pruning operation.
+struct SelectArgs {
+    int cells;                 // G
+    float lambda;              // Eq. 22 (0 for the no-spatial-novelty variant)
+    int keep;                  // K
+    int variant;               // e2s_variant
+    const int32_t* cand_pos;   // [B, N] raster positions of the candidates, or null (0..N-1)
+    int32_t* keep_idx;         // [B, K] kept candidate indices, ascending
+    int32_t* keep_pos;         // [B, K] their raster positions, or null
+    float* m_out;              // [B, K, 3] their fused masses, or null
+    float* fused;              // [B, N, 3] fused masses, or null
+    float* prio_c;             // [B, N] c = 1 - q, or null
+};
+// Eq. 11-19 from rho, pbar_c (onto m_prev [B, N, 3] when given), then Eq. 20-23.
+hipError_t launch_ds_select(const Dims& d, const SelectArgs& a, const float* rho,
+                            const float* pbar_c, const float* m_prev, hipStream_t stream);
+// Attention top-K (ablation A1) from the supports [B, L, H, N].
+hipError_t launch_attention_select(const Dims& d, const SelectArgs& a, const float* support_c,
+                                   hipStream_t stream);
 
 }  // namespace e2s

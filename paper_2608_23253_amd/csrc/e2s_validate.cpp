@@ -60,6 +60,8 @@ e2s_status check_select_params(const e2s_params* p, const Dims& d) {
     if (!std::isfinite(p->lambda) || p->lambda < 0.0f || p->lambda > 1.0f)
         return E2S_ERR_BAD_PARAM;
     if (p->keep < 0 || p->keep > d.N) return E2S_ERR_BAD_PARAM;
+    if (p->variant < E2S_VARIANT_FULL || p->variant > E2S_VARIANT_NO_SPATIAL_NOVELTY)
+        return E2S_ERR_BAD_PARAM;
     return E2S_OK;
 }
 

@@ -29,6 +29,11 @@
 //     (Eq. 23); one block-wide scan of the per-thread counts places them in
 //     ascending token order.
 //
+// A pruning operation over a candidate subset (the progressive schedule) passes
+// the candidates' raster positions: cells come from the positions, a cell is
+// occupied when it holds a candidate, and the token index of every tie rule is
+// the candidate index.  A position outside the grid gives its token no cell.
+//
 // Ranking by (c^, index) ascending is ranking by (q~ descending, index ascending).
 // The greedy formulation (take the best remaining token K times) returns the same
 // set; the radix select needs a handful of rounds instead of K argmax steps.
@@ -119,15 +124,16 @@ struct SelectShared {
     uint64_t found;
 };
 
-// Selection of one image (Eq. 20-23).  cv[j] = c of token n0 + j for j < cnt
-// (registers of the calling thread, tokens owned as described above); best: G*G
-// words of LDS.  All threads of the workgroup call it.
-template <int MAXC>
-__device__ void select_image(const float (&cv)[MAXC], int n0, int cnt, int chunk,
-                             uint64_t* best, SelectShared& sh, int64_t b,
-                             int32_t* __restrict__ keep_idx, double* __restrict__ adj_out,
-                             uint8_t* __restrict__ rep_out, int N, int gh, int gw, int G,
-                             float lambda, int K) {
+// Selection of one image (Eq. 20-23).  cv[j] = c and posv[j] = raster position
+// of token n0 + j for j < cnt (registers of the calling thread, tokens owned as
+// described above); best: G*G words of LDS.  Calls keep(slot, j) once for every
+// kept token (slot = its rank in ascending token order).  All threads of the
+// workgroup call it.
+template <int MAXC, typename Keep>
+__device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], int n0, int cnt,
+                             int chunk, uint64_t* best, SelectShared& sh, int64_t b,
+                             double* __restrict__ adj_out, uint8_t* __restrict__ rep_out, int N,
+                             int gh, int gw, int G, float lambda, int K, Keep&& keep) {
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
 
     for (int i = tid; i < G * G; i += kThreads) best[i] = ~0ull;
@@ -140,8 +146,10 @@ __device__ void select_image(const float (&cv)[MAXC], int n0, int cnt, int chunk
     for (int j = 0; j < MAXC; ++j) {
         if (j >= chunk) break;
         const int n = n0 + j;
-        const int row = n / gw, col = n - (n / gw) * gw;
-        cell[j] = j < cnt ? (row * G / gh) * G + col * G / gw : -1 - lane;
+        const int pos = posv[j];
+        const bool placed = j < cnt && pos >= 0 && pos < gh * gw;
+        const int row = pos / gw, col = pos - (pos / gw) * gw;
+        cell[j] = placed ? (row * G / gh) * G + col * G / gw : -1 - lane;
         uint64_t key = j < cnt ? (static_cast<uint64_t>(ordered_bits(cv[j])) << 32) |
                                      static_cast<uint32_t>(n)
                                : ~0ull;
@@ -153,7 +161,7 @@ __device__ void select_image(const float (&cv)[MAXC], int n0, int cnt, int chunk
         const int next = static_cast<int>(
             __builtin_amdgcn_update_dpp(-1, cell[j], kRowShl1, 0xF, 0xF, false));
         const bool last = next != cell[j];   // lane 15 of a row reads -1
-        if (j < cnt && last)
+        if (placed && last)
             atomicMin(reinterpret_cast<unsigned long long*>(best + cell[j]),
                       static_cast<unsigned long long>(key));
     }
@@ -170,7 +178,8 @@ __device__ void select_image(const float (&cv)[MAXC], int n0, int cnt, int chunk
         if (j >= chunk) break;
         if (j < cnt) {
             const int n = n0 + j;
-            const bool rep = static_cast<uint32_t>(best[cell[j]]) == static_cast<uint32_t>(n);
+            const bool rep = cell[j] >= 0 &&
+                             static_cast<uint32_t>(best[cell[j]]) == static_cast<uint32_t>(n);
             const double t = __dmul_rn(oml, static_cast<double>(cv[j]));
             const double adj = rep ? t : __dadd_rn(t, lam);
             kk[j] = ordered_bits(adj);
@@ -290,7 +299,6 @@ __device__ void select_image(const float (&cv)[MAXC], int n0, int cnt, int chunk
     uint32_t before = incl - packed;
     for (int w = 0; w < wave; ++w) before += sh.scan[w];
     uint32_t lt_run = before >> 16, eq_run = before & 0xFFFFu;
-    int32_t* out = keep_idx + b * K;
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
         if (j >= chunk) break;
@@ -303,7 +311,7 @@ __device__ void select_image(const float (&cv)[MAXC], int n0, int cnt, int chunk
                 if (eq_run < need_eq) pos = lt_run + eq_run;
                 ++eq_run;
             }
-            if (pos < static_cast<uint32_t>(K)) out[pos] = n0 + j;
+            if (pos < static_cast<uint32_t>(K)) keep(static_cast<int>(pos), j);
         }
     }
 }
@@ -320,31 +328,50 @@ __global__ __launch_bounds__(kThreads) void spatial_select_kernel(
     const int cnt = min(N - n0, chunk);
     const float* cb = prio_c + b * N;
     float cv[MAXC];
+    int posv[MAXC];
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
         if (j >= chunk) break;
         cv[j] = cb[min(n0 + j, N - 1)];     // in bounds; unused past cnt
+        posv[j] = n0 + j;
     }
-    select_image<MAXC>(cv, n0, cnt, chunk, best, sh, b, keep_idx, adj_out, rep_out, N, gh, gw, G,
-                       lambda, K);
+    select_image<MAXC>(cv, posv, n0, cnt, chunk, best, sh, b, adj_out, rep_out, N, gh, gw, G,
+                       lambda, K, [&](int slot, int j) { keep_idx[b * K + slot] = n0 + j; });
+}
+
+// Raster positions of the owned tokens (candidate positions when given).
+template <int MAXC>
+__device__ __forceinline__ void owned_positions(int (&posv)[MAXC], const int32_t* cand_pos,
+                                                int64_t b, int N, int n0, int cnt, int chunk) {
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        if (j >= chunk) break;
+        posv[j] = cand_pos ? (j < cnt ? cand_pos[b * N + n0 + j] : -1) : n0 + j;
+    }
 }
 
 // Dempster fusion across the layers (Eq. 11-19) from per-layer reliability and
-// mean support, then the selection: the tail of e2s_prune after the per-layer
-// evidence kernel.  The per-token arithmetic is that of the staged mass and
+// mean support, then the selection: the tail of a pruning operation after the
+// per-layer evidence.  The per-token arithmetic is that of the staged mass and
 // Dempster kernels.  Each layer's inputs are requested together (and, with up to
-// 4 tokens per thread, before the previous layer is combined).
+// 4 tokens per thread, before the previous layer is combined).  m_prev, when
+// given, is the candidates' fused mass from earlier operations: every layer is
+// combined onto it.  The ablation variants change one step each (e2s.h).
 template <int MAXC>
 __global__ __launch_bounds__(kThreads) void ds_select_kernel(
-    const float* __restrict__ rho, const float* __restrict__ pbar_c, float* __restrict__ fused,
-    float* __restrict__ prio_c, int32_t* __restrict__ keep_idx, int L, int N, int gh, int gw,
-    int G, float lambda, int K) {
+    const float* __restrict__ rho, const float* __restrict__ pbar_c,
+    const float* __restrict__ m_prev, SelectArgs a, int L, int N, int gh, int gw) {
     extern __shared__ uint64_t best[];
     __shared__ SelectShared sh;
     const int64_t b = blockIdx.x;
     const int chunk = (N + kThreads - 1) / kThreads;
     const int n0 = min(N, static_cast<int>(threadIdx.x) * chunk);
     const int cnt = min(N - n0, chunk);
+    const int K = a.keep;
+    const bool unit_rho = a.variant == E2S_VARIANT_NO_HEAD_RELIABILITY;
+    const bool last_only = a.variant == E2S_VARIANT_NO_LAYER_FUSION;
+    const bool carried = m_prev != nullptr && !last_only;
+    const int l_first = last_only ? L - 1 : 0;          // first layer read
 
     float r[MAXC], e[MAXC];      // current layer's inputs
     float aI[MAXC], aU[MAXC], aT[MAXC], kl[MAXC];
@@ -354,53 +381,122 @@ __global__ __launch_bounds__(kThreads) void ds_select_kernel(
         for (int j = 0; j < MAXC; ++j) {
             if (j >= chunk) break;
             const int64_t i = base + min(n0 + j, N - 1);   // in bounds; unused past cnt
-            rr[j] = rho[i];
+            rr[j] = unit_rho ? 1.0f : rho[i];
             ee[j] = pbar_c[i];
         }
     };
-    load_layer(0, r, e);
+    load_layer(l_first, r, e);
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
         if (j >= chunk) break;
-        masses_from_reliability(r[j], e[j], aI[j], aU[j], aT[j]);
         kl[j] = 0.f;
+        if (carried) {
+            const int64_t i = 3 * (b * N + min(n0 + j, N - 1));
+            aI[j] = m_prev[i];
+            aU[j] = m_prev[i + 1];
+            aT[j] = m_prev[i + 2];
+            float mI, mU, mT;
+            masses_from_reliability(r[j], e[j], mI, mU, mT);
+            kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
+        } else {
+            masses_from_reliability(r[j], e[j], aI[j], aU[j], aT[j]);
+        }
     }
     // with many tokens per thread the prefetch would not fit in registers
     constexpr bool kPrefetch = MAXC <= 4;
-    if (kPrefetch && L > 1) load_layer(1, r, e);
-    for (int l = 1; l < L; ++l) {
+    const int l_end = last_only ? l_first + 1 : L;
+    if (kPrefetch && l_first + 1 < l_end) load_layer(l_first + 1, r, e);
+    for (int l = l_first + 1; l < l_end; ++l) {
         float r2[MAXC], e2[MAXC];
         if (!kPrefetch) load_layer(l, r, e);
-        else if (l + 1 < L) load_layer(l + 1, r2, e2);
+        else if (l + 1 < l_end) load_layer(l + 1, r2, e2);
 #pragma unroll
         for (int j = 0; j < MAXC; ++j) {
             if (j >= chunk) break;
             float mI, mU, mT;
             masses_from_reliability(r[j], e[j], mI, mU, mT);
             kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
-            if (kPrefetch && l + 1 < L) {
+            if (kPrefetch && l + 1 < l_end) {
                 r[j] = r2[j];
                 e[j] = e2[j];
             }
         }
     }
+    const bool protect = a.variant != E2S_VARIANT_NO_CONFLICT;
+    float cv[MAXC];
+    int posv[MAXC];
+    owned_positions<MAXC>(posv, a.cand_pos, b, N, n0, cnt, chunk);
+#pragma unroll
+    for (int j = 0; j < MAXC; ++j) {
+        if (j >= chunk) break;
+        cv[j] = priority_complement(aU[j], protect ? kl[j] : 0.0f);
+        if (j < cnt) {
+            const int64_t i = b * N + n0 + j;
+            if (a.fused) {
+                a.fused[3 * i + 0] = aI[j];
+                a.fused[3 * i + 1] = aU[j];
+                a.fused[3 * i + 2] = aT[j];
+            }
+            if (a.prio_c) a.prio_c[i] = cv[j];
+        }
+    }
+    select_image<MAXC>(cv, posv, n0, cnt, chunk, best, sh, b, nullptr, nullptr, N, gh, gw, a.cells,
+                       a.lambda, K, [&](int slot, int j) {
+                           const int64_t o = b * K + slot;
+                           a.keep_idx[o] = n0 + j;
+                           if (a.keep_pos) a.keep_pos[o] = posv[j];
+                           if (a.m_out) {
+                               a.m_out[3 * o + 0] = aI[j];
+                               a.m_out[3 * o + 1] = aU[j];
+                               a.m_out[3 * o + 2] = aT[j];
+                           }
+                       });
+}
+
+// Ablation A1 (attention top-K): the K tokens of largest attention averaged over
+// the layers and heads, from the supports e = p - 1/2: with u = N r - 1,
+// e = u / (2 (2 + u)), so u = 4e / (1 - 2e) and the ranking by mean r is the
+// ranking by sum_{l,h} u.  Layers in order, heads in order within a layer.  No
+// spatial term; carried masses (m_out) are written vacuous.
+template <int MAXC>
+__global__ __launch_bounds__(kThreads) void attention_select_kernel(
+    const float* __restrict__ support_c, SelectArgs a, int L, int H, int N, int gh, int gw) {
+    extern __shared__ uint64_t best[];
+    __shared__ SelectShared sh;
+    const int64_t b = blockIdx.x;
+    const int chunk = (N + kThreads - 1) / kThreads;
+    const int n0 = min(N, static_cast<int>(threadIdx.x) * chunk);
+    const int cnt = min(N - n0, chunk);
+    const int K = a.keep;
     float cv[MAXC];
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
         if (j >= chunk) break;
-        cv[j] = priority_complement(aU[j], kl[j]);
-        if (j < cnt) {
-            const int64_t i = b * N + n0 + j;
-            if (fused) {
-                fused[3 * i + 0] = aI[j];
-                fused[3 * i + 1] = aU[j];
-                fused[3 * i + 2] = aT[j];
-            }
-            if (prio_c) prio_c[i] = cv[j];
+        const float* eb = support_c + (b * L * H) * static_cast<int64_t>(N) + min(n0 + j, N - 1);
+        float s = 0.f;
+        for (int lh = 0; lh < L * H; lh += 8) {
+            float ev[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) ev[u] = lh + u < L * H ? eb[(lh + u) * static_cast<int64_t>(N)] : 0.f;
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                if (lh + u < L * H) s += (4.0f * ev[u]) / (1.0f - 2.0f * ev[u]);
         }
+        cv[j] = -s;
     }
-    select_image<MAXC>(cv, n0, cnt, chunk, best, sh, b, keep_idx, nullptr, nullptr, N, gh, gw, G,
-                       lambda, K);
+    int posv[MAXC];
+    owned_positions<MAXC>(posv, a.cand_pos, b, N, n0, cnt, chunk);
+    select_image<MAXC>(cv, posv, n0, cnt, chunk, best, sh, b, nullptr, nullptr, N, gh, gw, a.cells,
+                       0.0f, K, [&](int slot, int j) {
+                           const int64_t o = b * K + slot;
+                           a.keep_idx[o] = n0 + j;
+                           if (a.keep_pos) a.keep_pos[o] = posv[j];
+                           if (a.m_out) {
+                               a.m_out[3 * o + 0] = 0.0f;
+                               a.m_out[3 * o + 1] = 0.0f;
+                               a.m_out[3 * o + 2] = 1.0f;
+                           }
+                       });
 }
 
 template <typename Kern>
@@ -411,16 +507,28 @@ hipError_t allow_lds(Kern kern, size_t lds) {
 }
 
 template <int MAXC>
-hipError_t launch_dssel(const Dims& d, int cells, float lambda, int keep, const float* rho,
-                        const float* pbar_c, int32_t* keep_idx, float* fused, float* prio_c,
-                        hipStream_t st) {
-    const size_t lds = static_cast<size_t>(cells) * cells * sizeof(uint64_t);
+hipError_t launch_dssel(const Dims& d, const SelectArgs& a, const float* rho, const float* pbar_c,
+                        const float* m_prev, hipStream_t st) {
+    const size_t lds = static_cast<size_t>(a.cells) * a.cells * sizeof(uint64_t);
     auto kern = ds_select_kernel<MAXC>;
     hipError_t err = allow_lds(kern, lds);
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(kThreads), lds, st, rho, pbar_c,
-                       fused, prio_c, keep_idx, static_cast<int>(d.L), static_cast<int>(d.N),
-                       static_cast<int>(d.gh), static_cast<int>(d.gw), cells, lambda, keep);
+                       m_prev, a, static_cast<int>(d.L), static_cast<int>(d.N),
+                       static_cast<int>(d.gh), static_cast<int>(d.gw));
+    return hipGetLastError();
+}
+
+template <int MAXC>
+hipError_t launch_attsel(const Dims& d, const SelectArgs& a, const float* support_c,
+                         hipStream_t st) {
+    const size_t lds = static_cast<size_t>(a.cells) * a.cells * sizeof(uint64_t);
+    auto kern = attention_select_kernel<MAXC>;
+    hipError_t err = allow_lds(kern, lds);
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(kThreads), lds, st, support_c,
+                       a, static_cast<int>(d.L), static_cast<int>(d.H), static_cast<int>(d.N),
+                       static_cast<int>(d.gh), static_cast<int>(d.gw));
     return hipGetLastError();
 }
 
@@ -445,17 +553,25 @@ int chunk_class(const Dims& d) {
 
 }  // namespace
 
-hipError_t launch_ds_select(const Dims& d, int cells, float lambda, int keep, const float* rho,
-                            const float* pbar_c, int32_t* keep_idx, float* fused, float* prio_c,
-                            hipStream_t st) {
+hipError_t launch_ds_select(const Dims& d, const SelectArgs& a, const float* rho,
+                            const float* pbar_c, const float* m_prev, hipStream_t st) {
     switch (chunk_class(d)) {
-        case 1: return launch_dssel<1>(d, cells, lambda, keep, rho, pbar_c, keep_idx, fused, prio_c, st);
-        case 2: return launch_dssel<2>(d, cells, lambda, keep, rho, pbar_c, keep_idx, fused, prio_c, st);
-        case 4: return launch_dssel<4>(d, cells, lambda, keep, rho, pbar_c, keep_idx, fused, prio_c, st);
-        case 8: return launch_dssel<8>(d, cells, lambda, keep, rho, pbar_c, keep_idx, fused, prio_c, st);
-        default:
-            return launch_dssel<kMaxChunk>(d, cells, lambda, keep, rho, pbar_c, keep_idx, fused,
-                                           prio_c, st);
+        case 1: return launch_dssel<1>(d, a, rho, pbar_c, m_prev, st);
+        case 2: return launch_dssel<2>(d, a, rho, pbar_c, m_prev, st);
+        case 4: return launch_dssel<4>(d, a, rho, pbar_c, m_prev, st);
+        case 8: return launch_dssel<8>(d, a, rho, pbar_c, m_prev, st);
+        default: return launch_dssel<kMaxChunk>(d, a, rho, pbar_c, m_prev, st);
+    }
+}
+
+hipError_t launch_attention_select(const Dims& d, const SelectArgs& a, const float* support_c,
+                                   hipStream_t st) {
+    switch (chunk_class(d)) {
+        case 1: return launch_attsel<1>(d, a, support_c, st);
+        case 2: return launch_attsel<2>(d, a, support_c, st);
+        case 4: return launch_attsel<4>(d, a, support_c, st);
+        case 8: return launch_attsel<8>(d, a, support_c, st);
+        default: return launch_attsel<kMaxChunk>(d, a, support_c, st);
     }
 }
 

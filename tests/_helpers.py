@@ -38,17 +38,24 @@ class SetCompare:
 
 
 def compare_sets(gpu_keep: np.ndarray, ref: O.ImageResult, gap: float = TIE_GAP) -> SetCompare:
+    """Tie rule on the oracle's ranking score: q~ with an absolute window, or, for
+    the attention top-K variant, the mean attention with a window relative to the
+    K-th kept value (attention averages 1/N, so an absolute window would not
+    scale)."""
     ok = list(ref.keep)
     K = len(ok)
     if K == 0:
         return SetCompare("exact" if len(gpu_keep) == 0 else "fail", 0, 0)
-    s_k = ref.qt[ok].min()
-    near = int((np.abs(ref.qt - s_k) < gap).sum())
+    score = ref.qt if ref.score is None else ref.score
+    s_k = score[ok].min()
+    if ref.score is not None:
+        gap = gap * abs(s_k)
+    near = int((np.abs(score - s_k) < gap).sum())
     g, o = set(int(x) for x in gpu_keep), set(int(x) for x in ok)
     if g == o:
         return SetCompare("exact", 0, near)
     sym = g ^ o
-    if len(g) == K and all(abs(ref.qt[n] - s_k) < gap for n in sym):
+    if len(g) == K and all(abs(score[n] - s_k) < gap for n in sym):
         return SetCompare("tie", len(sym) // 2, near)
     return SetCompare("fail", len(sym) // 2, near)
 

@@ -57,12 +57,20 @@ def fuse_sel(shape, params, rho=A, pbar=A, out=A, fused=None, prio=None):
                                prio, None)
 
 
+def stage(shape, params, ncand, q=A, k=A, pos=A, mprev=None, ws=A, ws_bytes=None, out=A,
+          kpos=None, mout=None):
+    if ws_bytes is None:
+        ws_bytes = L.workspace_size(shape, params)
+    return lib.e2s_prune_stage(ctypes.byref(shape), ctypes.byref(params), ncand, q, k, pos, mprev,
+                               ws, ws_bytes, out, kpos, mout, None)
+
+
 def test_exports_every_declared_entry_point():
     names = L.header_entry_points()
-    assert len(names) == 12
+    assert len(names) == 13
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.e2s_abi_version() == 2
+    assert lib.e2s_abi_version() == 3
 
 
 def test_status_strings():
@@ -171,3 +179,30 @@ def test_binding_rejects_cpu_tensors():
     q = torch.zeros((1, 1, 1, 1, 64), dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         L.score_heads(q, q, 1, 1)
+
+
+@pytest.mark.parametrize("variant", [-1, 6])
+def test_bad_variant(variant):
+    assert prune(good_shape(), good_params(variant=variant)) == L.ERR_BAD_PARAM
+    assert fuse_sel(good_shape(), good_params(variant=variant)) == L.ERR_BAD_PARAM
+    assert stage(good_shape(), good_params(variant=variant), 42) == L.ERR_BAD_PARAM
+
+
+def test_fuse_select_has_no_attention_topk():
+    """A1 needs the per-head supports, which e2s_fuse_select does not receive."""
+    assert fuse_sel(good_shape(), good_params(variant="a1_attention_topk")) == L.ERR_UNSUPPORTED
+
+
+def test_stage_validation():
+    sh = good_shape()                      # grid 6 x 7 = 42 positions
+    assert stage(sh, good_params(keep=5), 0) == L.ERR_BAD_SHAPE
+    assert stage(sh, good_params(keep=5), 43) == L.ERR_BAD_SHAPE
+    assert stage(sh, good_params(keep=5), 20, pos=None) == L.ERR_BAD_SHAPE   # positions needed
+    assert stage(sh, good_params(keep=21), 20) == L.ERR_BAD_PARAM            # K > N_l
+    assert stage(sh, good_params(keep=5), 20, out=None) == L.ERR_NULL_POINTER
+    assert stage(sh, good_params(keep=0), 20, out=None, pos=A + 2) == L.ERR_MISALIGNED
+    assert stage(sh, good_params(keep=5), 20, mprev=A + 2) == L.ERR_MISALIGNED
+    assert stage(sh, good_params(keep=5), 20, kpos=A + 1) == L.ERR_MISALIGNED
+    assert stage(sh, good_params(keep=5), 20, ws_bytes=16) == L.ERR_WORKSPACE_TOO_SMALL
+    assert stage(sh, good_params(keep=5), 20, q=None) == L.ERR_NULL_POINTER
+    assert stage(sh, good_params(keep=5, cells=7), 20) == L.ERR_BAD_PARAM

@@ -2,8 +2,9 @@
 
 Shapes span several tiles and ragged tails (token counts that are not multiples
 of 16 or 64, query-head groups of 1, 2, 7, 8 and 12, head_dim 64 and 128, fp32
-and bf16 storage, one to four source layers) and include the largest supported
-grid (128 x 128 = 16384 tokens).  Each stage is checked twice: fed the GPU's own
+and bf16 storage, one to eight source layers) and include the largest supported
+grid (128 x 128 = 16384 tokens) and batches with at least one (image, layer) per
+compute unit, where the whole path keeps each layer's supports on chip.  Each stage is checked twice: fed the GPU's own
 upstream output (isolates that stage's arithmetic) and end to end from Q and K.
 
 Tolerances (absolute + relative to the oracle value), all float32 arithmetic on
@@ -60,6 +61,13 @@ CASES = [
     synth.heavy_tailed(synth.config_by_name("llava").replace(batch=1), name="heavy_llava"),
     _small("max_grid_16384", config_id=56, batch=1, num_layers=1, num_heads=2, num_kv_heads=1,
            num_text=2, grid_h=128, grid_w=128, keep=1000, salient_count=40, clusters=4),
+    # batch x layers >= the CU count: e2s_prune / e2s_layer_reliability take the
+    # on-chip layer path (one workgroup per image and layer)
+    _small("layer_path_ragged", config_id=57, batch=64, num_layers=4, num_heads=6,
+           num_kv_heads=6, num_text=5, grid_h=7, grid_w=9, keep=13, cells=3),
+    _small("layer_path_f32_d128", config_id=58, batch=32, num_layers=8, num_heads=20,
+           num_kv_heads=20, head_dim=128, num_text=3, grid_h=9, grid_w=10, keep=25,
+           dtype="f32", lambdas=(0.2,)),
 ]
 
 

@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum CPU time spent timing the oracle")
     ap.add_argument("--kernel-only", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the ablation-variant and progressive-schedule timings")
     ap.add_argument("--copy-calibrate", type=int, default=0, metavar="N_MIB")
     ap.add_argument("--hbm-probe", type=int, default=0, metavar="N_MIB",
                     help="time a streaming read (torch sum) of N MiB: a practical read ceiling")
@@ -120,6 +122,85 @@ def hbm_probe(mib: int):
     torch.cuda.synchronize()
     ms = s.elapsed_time(e) / 10
     print(json.dumps({"read_mib": mib, "ms": ms, "GBps": n * 4 / ms / 1e6}))
+
+
+def avg_tokens(num_layers, n_visual, prune_after, kept):
+    """Eq. 24: mean over the LLM layers of the visual tokens each layer processes."""
+    total = 0
+    for i in range(1, num_layers + 1):
+        t = n_visual
+        for a, k in zip(prune_after, kept):
+            if i > a:
+                t = k
+        total += t
+    return total / num_layers
+
+
+# The paper's default LLaVA-1.5-7B schedule (Sec. 5.1): pruning after LLM layers 3,
+# 17 and 22 of 32 keeps 122, 48 and 42 of the 576 visual tokens (AvgTokens 128).
+SCHEDULE = (122, 48, 42)
+PRUNE_AFTER = (3, 17, 22)
+
+
+def bench_variants_and_schedule(args, cfg, qd, kd, stream, timed):
+    """Per-step time of every ablation variant through e2s_prune, and the
+    progressive schedule as three e2s_prune_stage calls (operation s on source
+    layer s of the batch; its candidates' keys gathered beforehand from that
+    layer's keys, as the model would compute them for the pruned sequence)."""
+    import numpy as np
+    import torch
+    import paper_2608_23253_amd as E
+
+    B, gh, gw, N = cfg.batch, cfg.grid_h, cfg.grid_w, cfg.num_visual
+    n_rep = max(20, args.steps // 4)
+    variants = {}
+    for v in E.VARIANTS:
+        pr = E.Pruner(qd, kd, gh, gw, cfg.keep, cfg.cells, cfg.lam, args.mode, variant=v)
+        for _ in range(args.warmup):
+            pr(qd, kd)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(n_rep):
+            pr(qd, kd)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / n_rep
+        variants[v] = {"ms_per_step": round(ms, 4), "images_per_s": round(B / ms * 1e3, 1)}
+    log("[bench] variants: " + ", ".join(f"{k} {v['ms_per_step']:.3f} ms"
+                                         for k, v in variants.items()))
+
+    # progressive schedule: prepare each operation's inputs with one untimed pass
+    ops = []
+    pos, m_prev = None, None
+    for s, budget in enumerate(SCHEDULE):
+        q_s = qd[:, s:s + 1].contiguous()
+        if pos is None:
+            k_s = kd[:, s:s + 1].contiguous()
+        else:
+            idx = pos.long()[:, None, :, None].expand(B, kd.shape[2], pos.shape[1], kd.shape[4])
+            k_s = torch.gather(kd[:, s], 2, idx).unsqueeze(1).contiguous()
+        sp = E.StagePruner(q_s, k_s, gh, gw, budget, cfg.cells, cfg.lam, args.mode)
+        _, kpos, m_out = sp(q_s, k_s, pos, m_prev)
+        torch.cuda.synchronize()
+        ops.append((sp, q_s, k_s, None if pos is None else pos.clone(),
+                    None if m_prev is None else m_prev.clone()))
+        pos, m_prev = kpos.clone(), m_out.clone()
+    calls = [(lambda o=o: (o[0](o[1], o[2], o[3], o[4]), 0)[1]) for o in ops]
+    times = timed(calls, n_rep)
+    op_us = [float(t.mean()) * 1e3 for t in times]
+    total_us = sum(op_us)
+    qk_bytes = sum(o[1].numel() * o[1].element_size() + o[2].numel() * o[2].element_size()
+                   for o in ops)
+    prog = {
+        "schedule": "->".join(str(x) for x in (N,) + SCHEDULE),
+        "avg_tokens_eq24": avg_tokens(32, N, PRUNE_AFTER, SCHEDULE),
+        "operation_us": [round(x, 2) for x in op_us],
+        "images_per_s": round(B / (total_us * 1e-6), 1),
+        "qk_bytes_per_batch": int(qk_bytes),
+        "hbm_frac": round(qk_bytes / (total_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+    }
+    log(f"[bench] progressive {prog['schedule']}: {', '.join(f'{x:.1f}' for x in op_us)} us "
+        f"-> {prog['images_per_s']:.0f} images/s")
+    return {"variants": variants, "progressive": prog}
 
 
 def main():
@@ -256,6 +337,10 @@ def main():
         f"{t_fs.mean() * 1e3:.1f} us | staged: score {t_score.mean() * 1e3:.1f} us, fuse "
         f"{t_fuse.mean() * 1e3:.1f} us, select {t_sel.mean() * 1e3:.1f} us")
 
+    extras = {}
+    if not args.no_extras:
+        extras = bench_variants_and_schedule(args, cfg, qd, kd, stream, timed)
+
     # ---- CPU oracle baseline ----------------------------------------------------
     import oracle as O
     from threadpoolctl import threadpool_info
@@ -327,6 +412,7 @@ def main():
                        f"images 0..{B - 1}), NumPy float64 oracle, mode {args.mode}"),
         },
     }
+    out.update(extras)
     print(json.dumps(out))
 
 

@@ -8,45 +8,6 @@
 
 namespace e2s {
 
-constexpr int kGroupWaves = 4;                       // waves of one reduction group
-constexpr int kGroupThreads = kGroupWaves * kWave;   // 256
-
-// Phase A for one query head: wave lw of a 4-wave group sums rows
-// lw*RPW + wrow + i*STEP (RPW = 64/(D/8) rows per wave load, STEP = 4*RPW) of the
-// head's [N_T, d] queries, lane wl holding dims 8*wl .. 8*wl+7; the RPW row groups
-// of the wave are then combined by shuffles, so lanes with wrow == 0 hold the
-// wave's partial sums.  qh points at the head's row 0, offset by 8*wl elements.
-template <typename T, int D>
-__device__ __forceinline__ void query_partial(const T* __restrict__ qh, int NT, int lw, int wrow,
-                                              float (&acc)[8]) {
-    constexpr int LPR = D / 8, RPW = kWave / LPR, STEP = kGroupWaves * RPW, QU = 4;
-#pragma unroll
-    for (int m = 0; m < 8; ++m) acc[m] = 0.f;
-    for (int t = lw * RPW + wrow; t - wrow < NT; t += QU * STEP) {
-        Packet<T> p[QU];
-#pragma unroll
-        for (int u = 0; u < QU; ++u)
-            load_packet(p[u], qh + static_cast<int64_t>(min(t + u * STEP, NT - 1)) * D);
-#pragma unroll
-        for (int u = 0; u < QU; ++u) {
-            float x[8];
-            unpack(p[u], x);
-            const bool ok = t + u * STEP < NT;
-#pragma unroll
-            for (int m = 0; m < 8; ++m) acc[m] += ok ? x[m] : 0.f;
-        }
-    }
-#pragma unroll
-    for (int m = 0; m < 8; ++m)
-        for (int o = LPR; o < kWave; o <<= 1) acc[m] += __shfl_xor(acc[m], o);
-}
-
-// The four wave partials p[0], p[D], p[2D], p[3D] of one query-mean element,
-// combined left to right and scaled by scale / N_T.
-__device__ __forceinline__ float query_mean(const float* p, int D, float qscale) {
-    return (((p[0] + p[D]) + p[2 * D]) + p[3 * D]) * qscale;
-}
-
 // Logit of one key row: lane wl's 8-element dot product, summed over the LPR lanes
 // that share the row.
 template <int LPR>
@@ -67,66 +28,6 @@ __device__ __forceinline__ float expm1_series(float x) {
     p = fmaf(p, x, 0.5f);
     p = fmaf(p, x, 1.0f);
     return p * x;
-}
-
-// Softmax statistics of one head's N logits a[] (LDS) over a group of 256 threads
-// (lt = index within the group): a[n] is replaced by a[n] - max and the return
-// value is L = log(S / N) (see log_mean_exp).  near reports whether the head's
-// logits span at most kSeriesRange, in which case every a - max and every
-// a - max - L lies in [-kSeriesRange, kSeriesRange] (L lies between the smallest
-// a - max and 0) and expm1 is evaluated by the short series; otherwise by the
-// library.  red: 16 floats of LDS owned by the group.  Contains two block-wide
-// barriers, so every thread of the workgroup calls it the same number of times;
-// threads of an inactive group pass active = false.
-__device__ __forceinline__ float softmax_centre(float* a, int N, int lt, float* red, bool active,
-                                                bool& near) {
-    const int lw = lt / kWave, lane = lt % kWave;
-    float m = -INFINITY, lo = INFINITY;
-    if (active) {
-        for (int n = lt; n < N; n += kGroupThreads) {
-            m = fmaxf(m, a[n]);
-            lo = fminf(lo, a[n]);
-        }
-    }
-    m = wave_max(m);
-    lo = -wave_max(-lo);
-    if (lane == 0) {
-        red[lw] = m;
-        red[12 + lw] = lo;
-    }
-    __syncthreads();
-    m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-    lo = fminf(fminf(red[12], red[13]), fminf(red[14], red[15]));
-    near = m - lo <= kSeriesRange;
-    float E = 0.f, S = 0.f;
-    if (active) {
-        if (near) {
-            for (int n = lt; n < N; n += kGroupThreads) {
-                const float d = a[n] - m;
-                a[n] = d;
-                const float t = expm1_series(d);
-                E += t;
-                S += 1.0f + t;
-            }
-        } else {
-            for (int n = lt; n < N; n += kGroupThreads) {
-                const float d = a[n] - m;
-                a[n] = d;
-                E += expm1f(d);
-                S += expf(d);
-            }
-        }
-    }
-    E = wave_sum(E);
-    S = wave_sum(S);
-    if (lane == 0) {
-        red[4 + lw] = E;
-        red[8 + lw] = S;
-    }
-    __syncthreads();
-    E = ((red[4] + red[5]) + red[6]) + red[7];
-    S = ((red[8] + red[9]) + red[10]) + red[11];
-    return log_mean_exp(E, S, static_cast<float>(N));
 }
 
 // Support e = p - 1/2 of a centred logit dc = a - max - L (Eq. 8-9).
@@ -214,8 +115,11 @@ __device__ __forceinline__ void wave_query_mean(const T* __restrict__ qh, int NT
 // Eq. 8-9 for one head's N logits a[] (LDS, complete and visible to the wave): per
 // lane max / min / sums over n = lane, lane + 64, ... in increasing order, then
 // butterflies across the wave.  Calls emit(n, dc, near) once per token, from lane
-// n % 64, with the centred logit dc = a_n - max - L (u = N r - 1 = expm1(dc));
-// near as in softmax_centre.
+// n % 64, with the centred logit dc = a_n - max - L (u = N r - 1 = expm1(dc)).
+// near: the head's logits span at most kSeriesRange, so every a - max and every
+// a - max - L lies in [-kSeriesRange, kSeriesRange] (L lies between the smallest
+// a - max and 0) and expm1 is evaluated by the short series; otherwise by the
+// library.  L = log(S / N) is taken by log_mean_exp.
 template <typename Emit>
 __device__ __forceinline__ void wave_softmax(float* a, int N, int lane, Emit&& emit) {
     float mx = -INFINITY, lo = INFINITY;
@@ -274,23 +178,6 @@ __device__ __forceinline__ void wave_head(const T* __restrict__ qh, const T* __r
     }
     wave_lds_sync();
     wave_softmax(a, N, lane, emit);
-}
-
-// Eq. 10 for one token from its H supports e[h * stride], in the order of the
-// evidence kernels: head group g = 0..3 sums heads g, g+4, ... in increasing order
-// and the four partial sums are combined left to right.
-__device__ __forceinline__ void reliability_token(const float* e, int stride, int H, float& rho,
-                                                  float& ebar) {
-    float p[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int g = 0; g < 4; ++g)
-        for (int h = g; h < H; h += 4) p[g] += e[h * stride];
-    const float s1 = ((p[0] + p[1]) + p[2]) + p[3];
-    ebar = s1 / static_cast<float>(H);
-    float a[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int g = 0; g < 4; ++g)
-        for (int h = g; h < H; h += 4) a[g] += fabsf(e[h * stride] - ebar);
-    const float s2 = ((a[0] + a[1]) + a[2]) + a[3];
-    rho = reliability_from_sums(s1, s2, 2.0f / static_cast<float>(H));
 }
 
 }  // namespace e2s

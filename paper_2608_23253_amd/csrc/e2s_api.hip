@@ -142,7 +142,7 @@ const char* e2s_status_string(e2s_status status) {
         case E2S_ERR_NULL_POINTER: return "E2S_ERR_NULL_POINTER: a required pointer is NULL";
         case E2S_ERR_BAD_SHAPE: return "E2S_ERR_BAD_SHAPE: a count is out of range or inconsistent";
         case E2S_ERR_BAD_PARAM: return "E2S_ERR_BAD_PARAM: dtype, mode, scale, cells, lambda or keep";
-        case E2S_ERR_UNSUPPORTED: return "E2S_ERR_UNSUPPORTED: valid but not implemented by this build";
+        case E2S_ERR_UNSUPPORTED: return "E2S_ERR_UNSUPPORTED: valid but not implemented by this library";
         case E2S_ERR_MISALIGNED: return "E2S_ERR_MISALIGNED: a pointer violates the alignment rule";
         case E2S_ERR_WORKSPACE_TOO_SMALL: return "E2S_ERR_WORKSPACE_TOO_SMALL: workspace below e2s_prune_workspace_size";
         case E2S_ERR_LAUNCH: return "E2S_ERR_LAUNCH: the HIP runtime refused a kernel launch";

@@ -168,8 +168,9 @@ E2S_API e2s_status e2s_spatial_select(const e2s_shape* shape, const e2s_params* 
 /* Score and head reliability in one call (Sec. 3.1 Eq. 1; Sec. 4.1 Eq. 8-10):
  *   rho, pbar_c [B, L, N] f32 out, bit-identical to e2s_score_heads followed by
  *   e2s_head_reliability.
- * With the MEAN_LOGIT reading, H == Hkv and one layer's supports on chip
- * (H * (N + d) * 4 <= 153600 bytes), one workgroup per (image, layer) keeps the
+ * With the MEAN_LOGIT reading, H == Hkv, one layer's supports on chip
+ * (H * (N + d) * 4 <= 153600 bytes) and at least as many (image, layer) pairs as
+ * the device has compute units, one workgroup per (image, layer) keeps the
  * supports in local memory and only rho and pbar_c reach device memory; otherwise
  * the two staged kernels run with the supports in `workspace`.
  *   workspace: 256-byte aligned, >= e2s_prune_workspace_size bytes, contents

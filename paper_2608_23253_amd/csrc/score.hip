@@ -20,7 +20,9 @@
 // layer, head) unit and runs all steps on its own, without workgroup barriers
 // (wave_head).  Grouped-query attention: one workgroup owns one (image, layer,
 // key head) unit and a chunk of the query heads sharing it, so every key row is
-// read from HBM once per chunk (score_group_kernel).
+// read from HBM once per chunk; with bf16 keys the logits of the chunk's heads are
+// one matrix-core product per 16 keys (score_group_mfma_kernel), with fp32 keys a
+// dot product per head (score_group_kernel).
 //
 // The supports are written with non-temporal stores: the key stream reads at
 // ~7 TB/s on its own, and cached write-backs interleaved with it cost more
@@ -39,6 +41,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 namespace e2s {
 namespace {
@@ -123,17 +126,186 @@ __global__ __launch_bounds__(kGroupKernelThreads) void score_group_kernel(
     }
     __syncthreads();
 
-    const float fN = static_cast<float>(N);
     for (int j = wave; j < nh; j += NW) {
-        float* aj = a + j * N;
         const int64_t row = (bl * H + h0 + j) * static_cast<int64_t>(N);
-        float* eo = e_out + row;
-        float* ro = r_out ? r_out + row : nullptr;
-        wave_softmax(aj, N, lane, [&](int n, float dc, bool near) {
-            __builtin_nontemporal_store(support_from_centred(dc, near), eo + n);
-            if (ro) ro[n] = expf(dc) / fN;
-        });
+        wave_softmax_store(a + j * N, N, lane, e_out + row, r_out ? r_out + row : nullptr);
     }
+}
+
+// Grouped-query attention with bf16 keys: the logits of every head of a chunk
+// against a 16-row key tile form a (16 x d) . (d x heads) product, which runs on
+// the matrix cores (v_mfma_f32_16x16x32_bf16: 16 keys x 16 query heads per tile).
+// The fp32 query means are split exactly into three bf16 terms
+// (hi + mid + lo = qbar: each term takes the next 8 significant bits, 24 in all),
+// kept in LDS, and the three products are accumulated in fp32, so a logit carries
+// the same information as the fp32 dot product of the vector kernels; only the
+// rounding of the sums differs.  Steps 1 and 3 are those of score_group_kernel.
+//
+// The stage streams Q and K with no reuse, and a launch has few workgroups (one
+// per (image, layer, key head)), so what bounds it is the bytes each wave keeps
+// in flight: up to kQueryRows query rows per lane in step 1 (with the first
+// kTilesEarly key tiles already requested), then kTilesInFlight key tiles, a
+// tile's registers being refilled with the tile kTilesInFlight positions ahead as
+// soon as its products are issued.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+constexpr int kMfmaMaxChunk = 16;             // query heads per MFMA tile (B columns)
+constexpr int kTilesInFlight = 4;
+constexpr int kTilesEarly = 2;
+constexpr int kQueryRows = 8;
+
+__device__ __forceinline__ uint32_t bf16_bits_rne(float x) {
+    const uint32_t u = __float_as_uint(x);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// x = hi + mid + lo exactly for finite x of normal range: each residual is exact in
+// fp32 and carries at most 16, then 8, significant bits.
+__device__ __forceinline__ void split_bf16x3(float x, uint16_t& hi, uint16_t& mid, uint16_t& lo) {
+    const uint32_t h = bf16_bits_rne(x);
+    const float r1 = x - __uint_as_float(h << 16);
+    const uint32_t m = bf16_bits_rne(r1);
+    const float r2 = r1 - __uint_as_float(m << 16);
+    hi = static_cast<uint16_t>(h);
+    mid = static_cast<uint16_t>(m);
+    lo = static_cast<uint16_t>(bf16_bits_rne(r2));
+}
+
+// MFMA operand layout (k = 32 per step): lane (lr, lg) = (lane % 16, lane / 16)
+// supplies row lr and elements 8 lg .. 8 lg + 7 of the step, i.e. head dims
+// 32 s + 8 lg .. + 7 of step s in both operands, so one wave-wide key load reads 64
+// contiguous bytes of each of 16 rows.
+// Two workgroups per CU (at most 128 VGPRs): a launch has about two per CU.
+template <int D>
+__global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, float* __restrict__ e_out,
+    float* __restrict__ r_out, int H, int Hkv, int NT, int N, int group, int hchunk,
+    int nchunks, float qscale) {
+    constexpr int NS = D / 32;            // MFMA steps per tile
+    constexpr int P = kTilesInFlight;
+    constexpr int NW = kGroupKernelThreads / kWave;
+    constexpr int BS = D + 8;             // padded row of the split query means
+    extern __shared__ __align__(16) float smem_mfma[];
+    uint16_t* bsplit = reinterpret_cast<uint16_t*>(smem_mfma);   // [3][16][BS] bf16 bits
+    float* qbar = smem_mfma + 3 * 16 * BS / 2;                    // [hchunk][D]
+    float* a = qbar + hchunk * D;         // [hchunk][N], rows 16-byte aligned if 4 | N
+
+    const int unit = blockIdx.x / nchunks;        // (b*L + l)*Hkv + g
+    const int ci = blockIdx.x - unit * nchunks;
+    const int g = unit % Hkv;
+    const int64_t bl = unit / Hkv;
+    const int h0 = g * group + ci * hchunk;
+    const int nh = min(hchunk, group - ci * hchunk);
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int lr = lane % 16, lg = lane / 16;
+    const uint16_t* kg = k + static_cast<int64_t>(unit) * N * D + 8 * lg;
+    const int tiles = (N + 15) / 16;
+    const int cnt = wave < tiles ? (tiles - wave + NW - 1) / NW : 0;   // this wave's tiles
+
+    bf16x8 kt[P][NS];
+    auto load_tile = [&](bf16x8 (&f)[NS], int i) {
+        const int row = min((wave + i * NW) * 16 + lr, N - 1);
+        const uint16_t* src = kg + static_cast<int64_t>(row) * D;
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+            f[s] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(src + 32 * s));
+    };
+#pragma unroll
+    for (int p = 0; p < kTilesEarly; ++p)
+        if (p < cnt) load_tile(kt[p], p);
+
+    // ---- 1. query means, split into bf16 terms ------------------------------------
+    {
+        using G = WaveRows<uint16_t, D>;
+        const int wrow = lane / G::LPR, wl = lane % G::LPR;
+        for (int j = wave; j < nh; j += NW) {
+            float qb[8];
+            wave_query_mean<uint16_t, D, kQueryRows>(q + ((bl * H + h0 + j) * NT) * D + wl * 8,
+                                                     NT, wrow, qscale, qb);
+            if (wrow == 0) {
+#pragma unroll
+                for (int m = 0; m < 8; ++m) qbar[j * D + wl * 8 + m] = qb[m];
+            }
+        }
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < 16 * D; idx += kGroupKernelThreads) {
+        const int hh = idx / D, dd = idx - hh * D;
+        uint16_t hi, mid, lo;
+        split_bf16x3(hh < nh ? qbar[hh * D + dd] : 0.f, hi, mid, lo);
+        bsplit[hh * BS + dd] = hi;
+        bsplit[(16 + hh) * BS + dd] = mid;
+        bsplit[(32 + hh) * BS + dd] = lo;
+    }
+#pragma unroll
+    for (int p = kTilesEarly; p < P; ++p)
+        if (p < cnt) load_tile(kt[p], p);
+    __syncthreads();
+
+    // ---- 2. logits of every head of the chunk, 16 keys per tile ----------------
+    const uint16_t* bq = bsplit + lr * BS + 8 * lg;
+    const bool vec_store = (N & 3) == 0;
+    for (int i0 = 0; i0 < cnt; i0 += P) {
+#pragma unroll
+        for (int p = 0; p < P; ++p) {
+            const int i = i0 + p;
+            if (i < cnt) {
+                f32x4 ch = {0.f, 0.f, 0.f, 0.f}, cm = ch, co = ch;
+#pragma unroll
+                for (int s = 0; s < NS; ++s) {
+                    const bf16x8 bh = *reinterpret_cast<const bf16x8*>(bq + 32 * s);
+                    const bf16x8 bm = *reinterpret_cast<const bf16x8*>(bq + 16 * BS + 32 * s);
+                    const bf16x8 bo = *reinterpret_cast<const bf16x8*>(bq + 32 * BS + 32 * s);
+                    ch = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[p][s], bh, ch, 0, 0, 0);
+                    cm = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[p][s], bm, cm, 0, 0, 0);
+                    co = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[p][s], bo, co, 0, 0, 0);
+                }
+                if (i + P < cnt) load_tile(kt[p], i + P);
+                // lane (lr, lg): keys 4 lg + r of the tile against head lr
+                const int key0 = (wave + i * NW) * 16 + 4 * lg;
+                f32x4 z;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) z[r] = (co[r] + cm[r]) + ch[r];
+                if (lr < nh) {
+                    float* dst = a + lr * N + key0;
+                    if (vec_store && key0 + 3 < N) {
+                        *reinterpret_cast<f32x4*>(dst) = z;
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            if (key0 + r < N) dst[r] = z[r];
+                    }
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- 3. softmax and supports per head ----------------------------------------
+    for (int j = wave; j < nh; j += NW) {
+        const int64_t row = (bl * H + h0 + j) * static_cast<int64_t>(N);
+        wave_softmax_store(a + j * N, N, lane, e_out + row, r_out ? r_out + row : nullptr);
+    }
+}
+
+template <int D>
+hipError_t launch_group_mfma(const Dims& d, float qscale, const void* q, const void* k, float* e,
+                             float* r, int hchunk, hipStream_t st) {
+    const int nchunks = static_cast<int>((d.group + hchunk - 1) / hchunk);
+    const size_t lds = 3 * 16 * (D + 8) * sizeof(uint16_t) +
+                       static_cast<size_t>(hchunk) * (D + d.N) * sizeof(float);
+    auto kern = score_group_mfma_kernel<D>;
+    if (lds > 64 * 1024) {
+        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             static_cast<int>(lds));
+        if (err != hipSuccess) return err;
+    }
+    const int64_t blocks = d.B * d.L * d.Hkv * nchunks;
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(blocks)), dim3(kGroupKernelThreads), lds,
+                       st, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), e, r,
+                       static_cast<int>(d.H), static_cast<int>(d.Hkv), static_cast<int>(d.NT),
+                       static_cast<int>(d.N), static_cast<int>(d.group), hchunk, nchunks, qscale);
+    return hipGetLastError();
 }
 
 template <typename T, int D, int HC>
@@ -168,14 +340,8 @@ __global__ __launch_bounds__(kThreads) void score_wave_kernel(
     const int64_t unit = static_cast<int64_t>(blockIdx.x) * (blockDim.x / kWave) + wave;
     if (unit >= units) return;
     float* a = smem + wave * N;
-    float* eo = e_out + unit * N;
-    float* ro = r_out ? r_out + unit * N : nullptr;
-    const float fN = static_cast<float>(N);
-    wave_head<T, D>(q + unit * NT * D, k + unit * N * D, NT, N, qscale, a, lane,
-                    [&](int n, float dc, bool near) {
-                        __builtin_nontemporal_store(support_from_centred(dc, near), eo + n);
-                        if (ro) ro[n] = expf(dc) / fN;
-                    });
+    wave_head<T, D>(q + unit * NT * D, k + unit * N * D, NT, N, qscale, a, lane, e_out + unit * N,
+                    r_out ? r_out + unit * N : nullptr);
 }
 
 template <typename T, int D>
@@ -203,12 +369,16 @@ template <typename T, int D>
 hipError_t dispatch(const Dims& d, float qscale, const void* q, const void* k, float* e, float* r,
                     hipStream_t st) {
     if (d.group == 1) return launch_wave<T, D>(d, qscale, q, k, e, r, st);
-    // query heads per workgroup: all of the group, at most kMaxChunk, and as many
-    // as fit the LDS budget with their logits; chunks balanced
+    // query heads per workgroup: all of the group, at most one MFMA tile's columns
+    // (bf16) or kMaxChunk (fp32), and as many as fit the LDS budget with their
+    // logits; chunks balanced
+    constexpr bool mfma = std::is_same<T, uint16_t>::value;
     const int64_t fit = std::max<int64_t>(1, kLdsBudget / ((D + d.N) * 4));
-    int hchunk = static_cast<int>(std::min<int64_t>({d.group, kMaxChunk, fit}));
+    int hchunk = static_cast<int>(
+        std::min<int64_t>({d.group, mfma ? kMfmaMaxChunk : kMaxChunk, fit}));
     const int nchunks = static_cast<int>((d.group + hchunk - 1) / hchunk);
     hchunk = static_cast<int>((d.group + nchunks - 1) / nchunks);
+    if constexpr (mfma) return launch_group_mfma<D>(d, qscale, q, k, e, r, hchunk, st);
     if (hchunk <= 2) return launch_group<T, D, 2>(d, qscale, q, k, e, r, hchunk, st);
     if (hchunk <= 4) return launch_group<T, D, 4>(d, qscale, q, k, e, r, hchunk, st);
     return launch_group<T, D, 8>(d, qscale, q, k, e, r, hchunk, st);

@@ -30,10 +30,16 @@ __device__ __forceinline__ float expm1_series(float x) {
     return p * x;
 }
 
-// Support e = p - 1/2 of a centred logit dc = a - max - L (Eq. 8-9).
+// Support e = p - 1/2 of a centred logit dc = a - max - L (Eq. 8-9):
+// e = u / (2 (2 + u)) with u = expm1(dc) > -1, so the divisor exceeds 2; it is
+// inverted by the hardware reciprocal estimate and one Newton step (within about an
+// ulp, at a third of the cost of an IEEE division).
 __device__ __forceinline__ float support_from_centred(float dc, bool near) {
     const float u = near ? expm1_series(dc) : expm1f(dc);
-    return u / (2.0f * (2.0f + u));
+    const float d = 2.0f * (2.0f + u);
+    float r = __builtin_amdgcn_rcpf(d);
+    r = fmaf(r, fmaf(-d, r, 1.0f), r);
+    return u * r;
 }
 
 // Orders one wave's LDS stores before its later LDS loads of other lanes' data
@@ -84,12 +90,12 @@ __device__ __forceinline__ void key_batch_logits(const Packet<T> (&p)[KU], const
 // Query mean of one head by one wave: lane (wrow, wl) sums rows wrow, wrow + RPW,
 // ... of dims 8*wl .. 8*wl+7 in increasing row order; the RPW row sums are then
 // combined by a butterfly, so every lane holds the same qbar (times qscale).  qh is
-// offset by 8*wl elements.
-template <typename T, int D>
+// offset by 8*wl elements.  QU rows per lane are requested at once; the order of the
+// sums, hence the result, does not depend on QU.
+template <typename T, int D, int QU = WaveRows<T, D>::KU>
 __device__ __forceinline__ void wave_query_mean(const T* __restrict__ qh, int NT, int wrow,
                                                 float qscale, float (&qb)[8]) {
     constexpr int LPR = WaveRows<T, D>::LPR, RPW = WaveRows<T, D>::RPW;
-    constexpr int QU = WaveRows<T, D>::KU;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     for (int t0 = 0; t0 < NT; t0 += QU * RPW) {
         Packet<T> p[QU];
@@ -114,14 +120,15 @@ __device__ __forceinline__ void wave_query_mean(const T* __restrict__ qh, int NT
 
 // Eq. 8-9 for one head's N logits a[] (LDS, complete and visible to the wave): per
 // lane max / min / sums over n = lane, lane + 64, ... in increasing order, then
-// butterflies across the wave.  Calls emit(n, dc, near) once per token, from lane
-// n % 64, with the centred logit dc = a_n - max - L (u = N r - 1 = expm1(dc)).
-// near: the head's logits span at most kSeriesRange, so every a - max and every
-// a - max - L lies in [-kSeriesRange, kSeriesRange] (L lies between the smallest
-// a - max and 0) and expm1 is evaluated by the short series; otherwise by the
-// library.  L = log(S / N) is taken by log_mean_exp.
-template <typename Emit>
-__device__ __forceinline__ void wave_softmax(float* a, int N, int lane, Emit&& emit) {
+// butterflies across the wave.  wave_softmax_stats leaves a_n - max in a[] and
+// returns L and near; the centred logit of token n is then dc = a[n] - L
+// (u = N r - 1 = expm1(dc)).  near: the head's logits span at most kSeriesRange,
+// so every a - max and every a - max - L lies in [-kSeriesRange, kSeriesRange]
+// (L lies between the smallest a - max and 0) and expm1 is evaluated by the short
+// series; otherwise by the library.  L = log(S / N) is taken by log_mean_exp.
+// wave_softmax calls emit(n, dc, near) once per token, from lane n % 64.
+__device__ __forceinline__ void wave_softmax_stats(float* a, int N, int lane, float& L,
+                                                   bool& near) {
     float mx = -INFINITY, lo = INFINITY;
     for (int n = lane; n < N; n += kWave) {
         mx = fmaxf(mx, a[n]);
@@ -129,7 +136,7 @@ __device__ __forceinline__ void wave_softmax(float* a, int N, int lane, Emit&& e
     }
     mx = wave_max(mx);
     lo = -wave_max(-lo);
-    const bool near = mx - lo <= kSeriesRange;
+    near = mx - lo <= kSeriesRange;
     float E = 0.f, S = 0.f;
     if (near) {
         for (int n = lane; n < N; n += kWave) {
@@ -149,18 +156,63 @@ __device__ __forceinline__ void wave_softmax(float* a, int N, int lane, Emit&& e
     }
     E = wave_sum(E);
     S = wave_sum(S);
-    const float L = log_mean_exp(E, S, static_cast<float>(N));
-    for (int n = lane; n < N; n += kWave) emit(n, a[n] - L, near);
+    L = log_mean_exp(E, S, static_cast<float>(N));
+}
+
+template <typename Emit>
+__device__ __forceinline__ void wave_softmax(float* a, int N, int lane, Emit&& emit) {
+    float L;
+    bool near;
+    wave_softmax_stats(a, N, lane, L, near);
+    // near is uniform over the wave: one loop per case, unrolled so that the LDS
+    // reads of several tokens are in flight together
+    if (near) {
+#pragma unroll 4
+        for (int n = lane; n < N; n += kWave) emit(n, a[n] - L, true);
+    } else {
+#pragma unroll 4
+        for (int n = lane; n < N; n += kWave) emit(n, a[n] - L, false);
+    }
+}
+
+// Eq. 8-9 for one head's logits a[] (as for wave_softmax), written to HBM: the
+// supports to eo (non-temporal: nothing reads them back soon) and, when ro is
+// given, r_n = exp(dc) / N.  Each case is a loop of its own without branches.
+template <bool NEAR, bool WITH_R>
+__device__ __forceinline__ void store_head_rows(const float* a, int N, int lane, float L,
+                                                float* __restrict__ eo, float* __restrict__ ro) {
+    const float fN = static_cast<float>(N);
+#pragma unroll 4
+    for (int n = lane; n < N; n += kWave) {
+        const float dc = a[n] - L;
+        __builtin_nontemporal_store(support_from_centred(dc, NEAR), eo + n);
+        if constexpr (WITH_R) ro[n] = expf(dc) / fN;
+    }
+}
+
+__device__ __forceinline__ void wave_softmax_store(float* a, int N, int lane,
+                                                   float* __restrict__ eo,
+                                                   float* __restrict__ ro) {
+    float L;
+    bool near;
+    wave_softmax_stats(a, N, lane, L, near);
+    if (near) {
+        if (ro) store_head_rows<true, true>(a, N, lane, L, eo, ro);
+        else store_head_rows<true, false>(a, N, lane, L, eo, ro);
+    } else {
+        if (ro) store_head_rows<false, true>(a, N, lane, L, eo, ro);
+        else store_head_rows<false, false>(a, N, lane, L, eo, ro);
+    }
 }
 
 // Eq. 1, 8 and 9 for one query head, computed by one wave with no workgroup
 // barrier.  qh: the head's [N_T, d] queries; kh: its key head's [N, d] keys; a: N
 // floats of LDS owned by the wave.  The first key batch is requested before the
 // query mean, and each later batch before the previous one is used.
-template <typename T, int D, typename Emit>
+template <typename T, int D>
 __device__ __forceinline__ void wave_head(const T* __restrict__ qh, const T* __restrict__ kh,
                                           int NT, int N, float qscale, float* a, int lane,
-                                          Emit&& emit) {
+                                          float* __restrict__ eo, float* __restrict__ ro) {
     using G = WaveRows<T, D>;
     const int wrow = lane / G::LPR, wl = lane % G::LPR;
     qh += wl * 8;
@@ -177,7 +229,7 @@ __device__ __forceinline__ void wave_head(const T* __restrict__ qh, const T* __r
         key_batch_logits<T, D>(kb, qb, a, base + G::BATCH, wrow, wl, N);
     }
     wave_lds_sync();
-    wave_softmax(a, N, lane, emit);
+    wave_softmax_store(a, N, lane, eo, ro);
 }
 
 }  // namespace e2s

@@ -1,7 +1,7 @@
 """GPU parity of every stage against the CPU oracle on small seeded cases.
 
 Shapes span several tiles and ragged tails (token counts that are not multiples
-of 16 or 64, query-head groups of 1, 2, 7, 8 and 12, head_dim 64 and 128, fp32
+of 16 or 64, query-head groups of 1, 2, 7, 8, 12 and 16, head_dim 64 and 128, fp32
 and bf16 storage, one to eight source layers) and include the largest supported
 grid (128 x 128 = 16384 tokens) and batches with at least one (image, layer) per
 compute unit, where the whole path keeps each layer's supports on chip.  Each stage is checked twice: fed the GPU's own
@@ -54,6 +54,9 @@ CASES = [
            grid_h=11, grid_w=11, keep=30, salient_count=6, clusters=2),
     _small("group12_chunks", config_id=54, num_heads=12, num_kv_heads=1, num_text=4,
            grid_h=6, grid_w=6, keep=9, cells=2, lambdas=(0.5,)),
+    # a full 16-head matrix-core tile, 4 | N (vector stores), several tiles per wave
+    _small("group16_d128", config_id=59, num_heads=32, num_kv_heads=2, head_dim=128,
+           num_text=7, grid_h=16, grid_w=20, keep=40, salient_count=12, clusters=3),
     synth.config_by_name("llava").replace(batch=2),
     synth.heavy_tailed(_small("heavy_d128", config_id=55, num_layers=4, num_heads=8,
                               num_kv_heads=8, head_dim=128, num_text=16, grid_h=12, grid_w=12,

@@ -58,6 +58,10 @@ CASES = [
     _small("group16_d128", config_id=59, num_heads=32, num_kv_heads=2, head_dim=128,
            num_text=7, grid_h=16, grid_w=20, keep=40, salient_count=12, clusters=3),
     synth.config_by_name("llava").replace(batch=2),
+    # more text queries than one LDS chunk of the mean-of-probabilities kernel (128),
+    # ragged in both queries and tokens
+    _small("query_chunks_150", config_id=60, num_heads=4, num_kv_heads=2, head_dim=128,
+           num_text=150, grid_h=9, grid_w=11, keep=20),
     synth.heavy_tailed(_small("heavy_d128", config_id=55, num_layers=4, num_heads=8,
                               num_kv_heads=8, head_dim=128, num_text=16, grid_h=12, grid_w=12,
                               keep=24, salient_count=8, clusters=2)),

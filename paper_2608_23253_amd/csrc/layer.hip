@@ -70,11 +70,16 @@ __global__ __launch_bounds__(kMaxWaves * kWave) void layer_evidence_kernel(
     if (tid == 0) s_next = nwaves;
     for (int h = tid; h < H; h += nthreads) s_done[h] = 0;
 
+    // Key requests are unconditional (unit ids clamped, rows clamped to N - 1 by
+    // load_key_batch; surplus rows are never used), so every path through the loop
+    // has the same loads in flight and the compiler's wait before a batch's first
+    // use leaves the later batch's loads pending.
     int u = wave;                         // first unit; its rows load during step 1
     Packet<T> ka[G::KU], kb[G::KU];
-    if (u < units) {
-        const int h = u / nch;
-        load_key_batch<T, D>(ka, kl + static_cast<int64_t>(h) * N * D, (u - h * nch) * CR, wrow, N);
+    {
+        const int uc = min(u, units - 1), h = uc / nch;
+        load_key_batch<T, D>(ka, kl + static_cast<int64_t>(h) * N * D, (uc - h * nch) * CR, wrow,
+                             N);
     }
 
     // ---- 1. query means ---------------------------------------------------------
@@ -100,11 +105,11 @@ __global__ __launch_bounds__(kMaxWaves * kWave) void layer_evidence_kernel(
 #pragma unroll
         for (int m = 0; m < 8; ++m) qb[m] = qbar[h * D + wl * 8 + m];
         const bool second = base + G::BATCH < N;
-        if (second) load_key_batch<T, D>(kb, kh, base + G::BATCH, wrow, N);
+        load_key_batch<T, D>(kb, kh, base + G::BATCH, wrow, N);
         key_batch_logits<T, D>(ka, qb, a, base, wrow, wl, N);
-        if (un < units) {
-            const int hn = un / nch;
-            load_key_batch<T, D>(ka, kl + static_cast<int64_t>(hn) * N * D, (un - hn * nch) * CR,
+        {
+            const int uc = min(un, units - 1), hn = uc / nch;
+            load_key_batch<T, D>(ka, kl + static_cast<int64_t>(hn) * N * D, (uc - hn * nch) * CR,
                                  wrow, N);
         }
         if (second) key_batch_logits<T, D>(kb, qb, a, base + G::BATCH, wrow, wl, N);

@@ -221,11 +221,13 @@ __device__ __forceinline__ void wave_head(const T* __restrict__ qh, const T* __r
     load_key_batch<T, D>(ka, kh, 0, wrow, N);
     float qb[8];
     wave_query_mean<T, D>(qh, NT, wrow, qscale, qb);
+    // the requests are unconditional (rows past N are clamped and never used), so
+    // the wait before a batch's first use leaves the next batch's loads pending
     for (int base = 0; base < N; base += 2 * G::BATCH) {
-        if (base + G::BATCH < N) load_key_batch<T, D>(kb, kh, base + G::BATCH, wrow, N);
+        load_key_batch<T, D>(kb, kh, base + G::BATCH, wrow, N);
         key_batch_logits<T, D>(ka, qb, a, base, wrow, wl, N);
         if (base + G::BATCH >= N) break;
-        if (base + 2 * G::BATCH < N) load_key_batch<T, D>(ka, kh, base + 2 * G::BATCH, wrow, N);
+        load_key_batch<T, D>(ka, kh, base + 2 * G::BATCH, wrow, N);
         key_batch_logits<T, D>(kb, qb, a, base + G::BATCH, wrow, wl, N);
     }
     wave_lds_sync();

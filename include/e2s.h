@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define E2S_ABI_VERSION 3
+#define E2S_ABI_VERSION 4
 
 #if defined(__GNUC__) || defined(__clang__)
 #define E2S_API __attribute__((visibility("default")))
@@ -233,6 +233,65 @@ E2S_API e2s_status e2s_prune_stage(const e2s_shape* shape, const e2s_params* par
                            const int32_t* cand_pos_opt, const float* m_prev_opt,
                            void* workspace, size_t workspace_bytes, int32_t* keep_idx,
                            int32_t* keep_pos_opt, float* m_out_opt, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Ragged batches: every image with its own grid, text length and budget.
+ * Vision-language models with dynamic resolution give each image its own patch
+ * grid (Qwen2-VL, Sec. 5 of the paper), and prompts differ in length.  The path
+ * is defined per image (Algorithm 1; Eq. 1-23 never mix images), so a ragged
+ * batch computes, for every image b, exactly what e2s_prune computes for that
+ * image alone.
+ * ------------------------------------------------------------------------- */
+
+/* One image of a ragged batch.  Offsets count elements of the array they index,
+ * so the images may sit anywhere in the caller's buffers (packed, or with gaps).
+ * q_offset and k_offset must keep the image's blocks 16-byte aligned (multiples
+ * of 8 elements for bf16, 4 for f32). */
+typedef struct {
+    int32_t grid_h;        /* image b's grid rows >= 1                             */
+    int32_t grid_w;        /* grid cols >= 1; N_b = grid_h * grid_w <= 16384       */
+    int32_t num_text;      /* N_T,b >= 1 text queries                              */
+    int32_t keep;          /* K_b, 0 <= K_b <= N_b                                 */
+    int64_t q_offset;      /* q + q_offset: the image's Q block [L, H, N_T,b, d]   */
+    int64_t k_offset;      /* k + k_offset: its K block [L, Hkv, N_b, d]           */
+    int64_t token_offset;  /* its N_b tokens in fused_opt / prio_c_opt start here;
+                              the images' ranges [token_offset, token_offset + N_b)
+                              must not overlap                                     */
+    int64_t keep_offset;   /* its K_b kept indices in keep_idx start here; ranges
+                              [keep_offset, keep_offset + K_b) must not overlap    */
+} e2s_image;               /* 48 bytes */
+
+typedef struct {
+    int32_t batch;         /* B >= 1 images                                        */
+    int32_t num_layers;    /* L >= 1                                               */
+    int32_t num_heads;     /* H >= 1, at most 128                                  */
+    int32_t num_kv_heads;  /* Hkv >= 1, H % Hkv == 0                               */
+    int32_t head_dim;      /* d: 64 or 128                                         */
+} e2s_ragged_shape;
+
+/* Bytes of device workspace e2s_prune_ragged needs: the supports [L, H, .] and
+ * rho, pbar_c [L, .] of every image, each image's block at L*H*token_offset
+ * (resp. L*token_offset), i.e. (L*H + 2L) * T floats in three 256-byte aligned
+ * regions, T = max over b of token_offset + N_b (host-only query). */
+E2S_API e2s_status e2s_prune_ragged_workspace_size(const e2s_ragged_shape* shape,
+                                                   const e2s_image* images_host,
+                                                   size_t* bytes);
+
+/* e2s_prune over a ragged batch.  images_host [B] (host memory) is validated and
+ * sizes the launches; images_dev [B] (device memory, 8-byte aligned) must hold
+ * the same records: the kernels read it.  Per image b, with its own N_b, N_T,b
+ * and K_b, the results are those of e2s_prune on that image alone, bit for bit:
+ *   keep_idx + keep_offset   [K_b] int32 out, ascending token indices of image b
+ *   fused_opt + 3*token_offset [N_b, 3], prio_c_opt + token_offset [N_b] f32 out
+ *   (both may be NULL; not written by ATTENTION_TOPK)
+ * params->keep is ignored (each image has its own); params->cells must not
+ * exceed any image's grid_h or grid_w.  keep_idx may be NULL iff every K_b is 0.
+ * workspace: 256-byte aligned, >= e2s_prune_ragged_workspace_size bytes. */
+E2S_API e2s_status e2s_prune_ragged(const e2s_ragged_shape* shape, const e2s_params* params,
+                                    const e2s_image* images_host, const e2s_image* images_dev,
+                                    const void* q, const void* k, void* workspace,
+                                    size_t workspace_bytes, int32_t* keep_idx,
+                                    float* fused_opt, float* prio_c_opt, void* stream);
 
 /* Static description of a status code (never NULL). */
 E2S_API const char* e2s_status_string(e2s_status status);

@@ -8,7 +8,7 @@ HIP kernels.  Two layers are exposed:
   * functions with the C names minus the ``e2s_`` prefix (``score_heads``,
     ``head_reliability``, ``head_masses``, ``ds_combine_layers``,
     ``fuse_evidence``, ``spatial_select``, ``layer_reliability``, ``fuse_select``,
-    ``prune``, ``prune_stage``) that take torch tensors on
+    ``prune``, ``prune_stage``, ``prune_ragged``) that take torch tensors on
     the GPU, allocate the outputs with torch, pass raw device pointers and the
     current torch stream, and raise ``E2SError`` on a non-zero status.
 
@@ -52,6 +52,20 @@ class Params(ctypes.Structure):
                 ("variant", ctypes.c_int32)]
 
 
+class Image(ctypes.Structure):
+    """e2s_image: one image of a ragged batch (sizes and element offsets)."""
+    _fields_ = [("grid_h", ctypes.c_int32), ("grid_w", ctypes.c_int32),
+                ("num_text", ctypes.c_int32), ("keep", ctypes.c_int32),
+                ("q_offset", ctypes.c_int64), ("k_offset", ctypes.c_int64),
+                ("token_offset", ctypes.c_int64), ("keep_offset", ctypes.c_int64)]
+
+
+class RaggedShape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("num_layers", ctypes.c_int32),
+                ("num_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32)]
+
+
 class E2SError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
@@ -75,6 +89,10 @@ _SIGNATURES = {
     "e2s_prune": [_SH, _PA, _P, _P, _P, ctypes.c_size_t, _P, _P, _P, _P],
     "e2s_prune_stage": [_SH, _PA, ctypes.c_int32, _P, _P, _P, _P, _P, ctypes.c_size_t, _P, _P,
                         _P, _P],
+    "e2s_prune_ragged_workspace_size": [ctypes.POINTER(RaggedShape), _P,
+                                        ctypes.POINTER(ctypes.c_size_t)],
+    "e2s_prune_ragged": [ctypes.POINTER(RaggedShape), _PA, _P, _P, _P, _P, _P, ctypes.c_size_t,
+                         _P, _P, _P, _P],
     "e2s_status_string": [ctypes.c_int],
     "e2s_abi_version": [],
 }
@@ -453,3 +471,88 @@ def prune_stage(q, k, grid_h: int, grid_w: int, keep: int, cand_pos=None, m_prev
 
 def default_scale(head_dim: int) -> float:
     return 1.0 / math.sqrt(head_dim)
+
+
+# ---------------------------------------------------------------------------
+# ragged batches (e2s_prune_ragged)
+# ---------------------------------------------------------------------------
+
+def packed_images(dims, num_layers: int, num_heads: int, num_kv_heads: int, head_dim: int):
+    """e2s_image records of images packed one after the other: dims is a list of
+    (grid_h, grid_w, num_text, keep).  Returns (ctypes array, total Q elements,
+    total K elements, total tokens, total kept)."""
+    arr = (Image * len(dims))()
+    qo = ko = to = kk = 0
+    for i, (gh, gw, nt, keep) in enumerate(dims):
+        n = gh * gw
+        arr[i] = Image(gh, gw, nt, keep, qo, ko, to, kk)
+        qo += num_layers * num_heads * nt * head_dim
+        ko += num_layers * num_kv_heads * n * head_dim
+        to += n
+        kk += keep
+    return arr, qo, ko, to, kk
+
+
+class RaggedPruner:
+    """Repeated e2s_prune_ragged calls over one ragged batch layout.
+
+    images: a ctypes array of Image records (see packed_images); the records are
+    copied once to a device table.  q and k are flat device tensors holding every
+    image's blocks at the records' offsets."""
+
+    def __init__(self, images, num_layers: int, num_heads: int, num_kv_heads: int,
+                 head_dim: int, device, dtype=DTYPE_BF16, mode="mean_logit", scale: float = 0.0,
+                 cells: int = 4, lam: float = 0.1, variant="full"):
+        torch = _torch()
+        self.images = images
+        self.shape = RaggedShape(len(images), num_layers, num_heads, num_kv_heads, head_dim)
+        self.params = make_params(dtype, mode, scale, cells, lam, 0, variant)
+        self.device = torch.device(device)
+        raw = bytes(images)
+        host = torch.frombuffer(bytearray(raw), dtype=torch.uint8)
+        self.images_dev = host.to(self.device)
+        n = ctypes.c_size_t(0)
+        _raise(_LIB.e2s_prune_ragged_workspace_size(ctypes.byref(self.shape),
+                                                    ctypes.addressof(images), ctypes.byref(n)),
+               "e2s_prune_ragged_workspace_size")
+        self.workspace = torch.empty(int(n.value), device=self.device, dtype=torch.uint8)
+        self.tokens = max(im.token_offset + im.grid_h * im.grid_w for im in images)
+        self.kept = max([im.keep_offset + im.keep for im in images if im.keep > 0] or [0])
+        self.keep_idx = torch.empty(max(self.kept, 1), device=self.device, dtype=torch.int32)
+
+    def __call__(self, q, k, fused=None, prio_c=None, stream: Optional[int] = None):
+        torch = _torch()
+        _check(q, "q")
+        _check(k, "k", dtype=q.dtype)
+        if _dtype_code(q) != self.params.dtype:
+            raise TypeError("q/k dtype does not match the RaggedPruner's")
+        for t, name, n in ((fused, "fused", 3 * self.tokens), (prio_c, "prio_c", self.tokens)):
+            if t is not None:
+                _check(t, name, dtype=torch.float32)
+                if t.numel() < n:
+                    raise ValueError(f"{name} holds fewer than {n} values")
+        st = _stream(self.device) if stream is None else stream
+        _raise(_LIB.e2s_prune_ragged(ctypes.byref(self.shape), ctypes.byref(self.params),
+                                     ctypes.addressof(self.images), self.images_dev.data_ptr(),
+                                     q.data_ptr(), k.data_ptr(), self.workspace.data_ptr(),
+                                     self.workspace.numel(),
+                                     self.keep_idx.data_ptr() if self.kept > 0 else None,
+                                     _ptr(fused), _ptr(prio_c), st), "e2s_prune_ragged")
+        return self.keep_idx
+
+
+def prune_ragged(q, k, images, num_layers: int, num_heads: int, num_kv_heads: int,
+                 head_dim: int, cells: int = 4, lam: float = 0.1, mode="mean_logit",
+                 scale: float = 0.0, want_fused=False, want_prio=False, variant="full"):
+    """The whole path over a ragged batch: (keep_idx [sum K_b] int32, fused
+    [tokens, 3] or None, prio_c [tokens] or None), image b's entries at its
+    record's keep_offset / token_offset."""
+    torch = _torch()
+    p = RaggedPruner(images, num_layers, num_heads, num_kv_heads, head_dim, q.device,
+                     _dtype_code(q), mode, scale, cells, lam, variant)
+    fused = (torch.empty((p.tokens, 3), device=q.device, dtype=torch.float32)
+             if want_fused else None)
+    prio = torch.empty(p.tokens, device=q.device, dtype=torch.float32) if want_prio else None
+    idx = p(q, k, fused, prio)
+    return idx[:p.kept], fused, prio
+

@@ -298,6 +298,7 @@ e2s_status e2s_prune_stage(const e2s_shape* shape, const e2s_params* params, int
     if (num_cand < 1 || num_cand > d.N) return E2S_ERR_BAD_SHAPE;
     if (cand_pos_opt == nullptr && num_cand != d.N) return E2S_ERR_BAD_SHAPE;
     d.N = num_cand;
+    d.tokens = d.B * d.N;
     E2S_TRY(e2s::check_select_params(params, d));
     if (params->keep > 0) E2S_TRY(need(keep_idx));
     E2S_TRY(aligned_opt(cand_pos_opt, 4));
@@ -310,6 +311,52 @@ e2s_status e2s_prune_stage(const e2s_shape* shape, const e2s_params* params, int
     a.keep_pos = keep_pos_opt;
     a.m_out = m_out_opt;
     return run_operation(d, params, q, k, workspace, a, m_prev_opt,
+                         static_cast<hipStream_t>(stream));
+}
+
+e2s_status e2s_prune_ragged_workspace_size(const e2s_ragged_shape* shape,
+                                           const e2s_image* images_host, size_t* bytes) {
+    Dims d;
+    E2S_TRY(e2s::check_ragged(shape, images_host, 0, &d, nullptr));
+    E2S_TRY(need(bytes));
+    *bytes = e2s::prune_workspace_bytes(d);
+    return E2S_OK;
+}
+
+e2s_status e2s_prune_ragged(const e2s_ragged_shape* shape, const e2s_params* params,
+                            const e2s_image* images_host, const e2s_image* images_dev,
+                            const void* q, const void* k, void* workspace,
+                            size_t workspace_bytes, int32_t* keep_idx, float* fused_opt,
+                            float* prio_c_opt, void* stream) {
+    E2S_TRY(e2s::check_score_params(params));
+    Dims d;
+    int64_t min_side = 0;
+    const int elem = params->dtype == E2S_DTYPE_BF16 ? 2 : 4;
+    E2S_TRY(e2s::check_ragged(shape, images_host, elem, &d, &min_side));
+    E2S_TRY(need(images_dev));
+    E2S_TRY(need(q));
+    E2S_TRY(need(k));
+    E2S_TRY(need(workspace));
+    E2S_TRY(e2s::check_aligned(images_dev, 8));
+    E2S_TRY(e2s::check_aligned(q, 16));
+    E2S_TRY(e2s::check_aligned(k, 16));
+    E2S_TRY(e2s::check_aligned(workspace, 256));
+    if (workspace_bytes < e2s::prune_workspace_bytes(d)) return E2S_ERR_WORKSPACE_TOO_SMALL;
+    // selection parameters: cells within every image's grid; keep is per image
+    if (params->cells < 1 || params->cells > min_side) return E2S_ERR_BAD_PARAM;
+    if (!std::isfinite(params->lambda) || params->lambda < 0.0f || params->lambda > 1.0f)
+        return E2S_ERR_BAD_PARAM;
+    if (params->variant < E2S_VARIANT_FULL || params->variant > E2S_VARIANT_NO_SPATIAL_NOVELTY)
+        return E2S_ERR_BAD_PARAM;
+    bool any_keep = false;
+    for (int64_t b = 0; b < d.B; ++b) any_keep = any_keep || images_host[b].keep > 0;
+    if (any_keep) E2S_TRY(need(keep_idx));
+    E2S_TRY(aligned_opt(keep_idx, 4));
+    E2S_TRY(aligned_opt(fused_opt, 4));
+    E2S_TRY(aligned_opt(prio_c_opt, 4));
+    d.images = images_dev;
+    return run_operation(d, params, q, k, workspace,
+                         select_args(params, keep_idx, fused_opt, prio_c_opt), nullptr,
                          static_cast<hipStream_t>(stream));
 }
 

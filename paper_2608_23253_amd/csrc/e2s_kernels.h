@@ -5,9 +5,24 @@
 
 #include <hip/hip_runtime.h>
 
+#include "batch_geom.h"
 #include "e2s_validate.h"
 
 namespace e2s {
+
+// The kernels' view of a validated call's batch (keep: K of a uniform selection).
+inline BatchGeom batch_geom(const Dims& d, int keep = 0) {
+    return BatchGeom{d.images,
+                     static_cast<int>(d.L),
+                     static_cast<int>(d.H),
+                     static_cast<int>(d.Hkv),
+                     static_cast<int>(d.D),
+                     static_cast<int>(d.NT),
+                     static_cast<int>(d.N),
+                     static_cast<int>(d.gh),
+                     static_cast<int>(d.gw),
+                     keep};
+}
 
 // Score stage, mean-of-logits reading (Eq. 1 then Eq. 8, 9).
 hipError_t launch_score_mean_logit(const Dims& d, int dtype, float scale, const void* q,

@@ -1,8 +1,10 @@
 // Host-side argument checks of the C ABI (see e2s_validate.h).
 #include "e2s_validate.h"
 
+#include <algorithm>
 #include <cmath>
 #include <limits>
+#include <vector>
 
 namespace e2s {
 
@@ -41,7 +43,75 @@ e2s_status check_shape(const e2s_shape* s, Dims* out) {
     if (qel > big || kel > big || eel > big) return E2S_ERR_BAD_SHAPE;
     if (static_cast<double>(d.B) * d.L * d.H > 2147483647.0) return E2S_ERR_BAD_SHAPE;
     if (static_cast<double>(d.B) * d.N > 2147483647.0) return E2S_ERR_BAD_SHAPE;
+    d.tokens = d.B * d.N;
     if (out) *out = d;
+    return E2S_OK;
+}
+
+namespace {
+// Ranges [start, start + len) of the records with len > 0 must not overlap.
+bool disjoint(std::vector<std::pair<int64_t, int64_t>> r) {
+    std::sort(r.begin(), r.end());
+    for (size_t i = 1; i < r.size(); ++i)
+        if (r[i].first < r[i - 1].first + r[i - 1].second) return false;
+    return true;
+}
+}  // namespace
+
+e2s_status check_ragged(const e2s_ragged_shape* s, const e2s_image* images, int elem_bytes,
+                        Dims* out, int64_t* min_side) {
+    if (s == nullptr || images == nullptr) return E2S_ERR_NULL_POINTER;
+    if (s->batch < 1 || s->num_layers < 1 || s->num_heads < 1 || s->num_kv_heads < 1 ||
+        s->head_dim < 1)
+        return E2S_ERR_BAD_SHAPE;
+    if (s->num_heads % s->num_kv_heads != 0) return E2S_ERR_BAD_SHAPE;
+    Dims d;
+    d.B = s->batch;
+    d.L = s->num_layers;
+    d.H = s->num_heads;
+    d.Hkv = s->num_kv_heads;
+    d.D = s->head_dim;
+    d.group = d.H / d.Hkv;
+    d.gh = 0;
+    d.gw = 0;
+    if (d.H > kMaxHeads) return E2S_ERR_UNSUPPORTED;
+    if (d.D != 64 && d.D != 128) return E2S_ERR_UNSUPPORTED;
+    const double big = static_cast<double>(std::numeric_limits<int64_t>::max() / 16);
+    const int64_t align_el = elem_bytes > 0 ? 16 / elem_bytes : 1;
+    int64_t nt_max = 0, n_max = 0, span = 0, side = std::numeric_limits<int64_t>::max();
+    std::vector<std::pair<int64_t, int64_t>> toks, keeps;
+    toks.reserve(static_cast<size_t>(d.B));
+    for (int64_t b = 0; b < d.B; ++b) {
+        const e2s_image& im = images[b];
+        if (im.grid_h < 1 || im.grid_w < 1 || im.num_text < 1) return E2S_ERR_BAD_SHAPE;
+        const int64_t n = static_cast<int64_t>(im.grid_h) * im.grid_w;
+        if (n > kMaxVisual) return E2S_ERR_UNSUPPORTED;
+        if (im.keep < 0 || im.keep > n) return E2S_ERR_BAD_PARAM;
+        if (im.q_offset < 0 || im.k_offset < 0 || im.token_offset < 0 || im.keep_offset < 0)
+            return E2S_ERR_BAD_SHAPE;
+        if (im.q_offset % align_el != 0 || im.k_offset % align_el != 0) return E2S_ERR_MISALIGNED;
+        const double qel = static_cast<double>(im.q_offset) +
+                           static_cast<double>(d.L) * d.H * im.num_text * d.D;
+        const double kel = static_cast<double>(im.k_offset) + static_cast<double>(d.L) * d.Hkv * n * d.D;
+        const double tel = (static_cast<double>(im.token_offset) + n) * d.L * d.H;
+        const double kp = static_cast<double>(im.keep_offset) + im.keep;
+        if (qel > big || kel > big || tel > big || kp > 2147483647.0) return E2S_ERR_BAD_SHAPE;
+        nt_max = std::max<int64_t>(nt_max, im.num_text);
+        n_max = std::max(n_max, n);
+        span = std::max(span, im.token_offset + n);
+        side = std::min<int64_t>(side, std::min(im.grid_h, im.grid_w));
+        toks.emplace_back(im.token_offset, n);
+        if (im.keep > 0) keeps.emplace_back(im.keep_offset, im.keep);
+    }
+    if (!disjoint(toks) || !disjoint(keeps)) return E2S_ERR_BAD_SHAPE;
+    if (static_cast<double>(d.B) * d.L * d.H > 2147483647.0) return E2S_ERR_BAD_SHAPE;
+    if (static_cast<double>(d.B) * d.L * ((n_max + 63) / 64) > 2147483647.0)
+        return E2S_ERR_BAD_SHAPE;
+    d.NT = nt_max;
+    d.N = n_max;
+    d.tokens = span;
+    if (out) *out = d;
+    if (min_side) *min_side = side;
     return E2S_OK;
 }
 
@@ -66,11 +136,11 @@ e2s_status check_select_params(const e2s_params* p, const Dims& d) {
 }
 
 size_t support_region_bytes(const Dims& d) {
-    return align_up(static_cast<size_t>(d.B * d.L * d.H * d.N) * sizeof(float), 256);
+    return align_up(static_cast<size_t>(d.L * d.H * d.tokens) * sizeof(float), 256);
 }
 
 size_t layer_region_bytes(const Dims& d) {
-    return align_up(static_cast<size_t>(d.B * d.L * d.N) * sizeof(float), 256);
+    return align_up(static_cast<size_t>(d.L * d.tokens) * sizeof(float), 256);
 }
 
 size_t prune_workspace_bytes(const Dims& d) {

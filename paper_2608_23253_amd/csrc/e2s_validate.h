@@ -13,6 +13,12 @@ namespace e2s {
 struct Dims {
     int64_t B, L, H, Hkv, D, NT, gh, gw, N;
     int64_t group;  // H / Hkv query heads per key head
+    // Ragged batch: the device table of per-image records; NT and N are then the
+    // largest N_T,b and N_b (launch sizes), gh and gw unused.  Null: uniform.
+    const e2s_image* images = nullptr;
+    // Token span of the per-token arrays: B * N (uniform), or the largest
+    // token_offset + N_b (ragged); sizes the workspace.
+    int64_t tokens = 0;
 };
 
 constexpr int64_t kMaxVisual = 16384;  // one image's scores fit in a workgroup's LDS
@@ -22,6 +28,13 @@ e2s_status check_shape(const e2s_shape* s, Dims* out);
 e2s_status check_score_params(const e2s_params* p);
 e2s_status check_select_params(const e2s_params* p, const Dims& d);
 e2s_status check_aligned(const void* ptr, size_t align);
+
+// A ragged batch: the shape, every image record (sizes, offsets, alignment of the
+// Q and K blocks for elements of elem_bytes bytes; 0 skips that check, disjoint
+// token and keep ranges), giving Dims with the largest N_T,b and N_b and the
+// token span.  min_side: the smallest grid side over the images.
+e2s_status check_ragged(const e2s_ragged_shape* s, const e2s_image* images, int elem_bytes,
+                        Dims* out, int64_t* min_side);
 
 // Workspace of e2s_layer_reliability and e2s_prune: the supports e [B,L,H,N] f32
 // (used only when a layer's supports do not stay on chip), then rho and pbar_c

@@ -61,21 +61,27 @@ __device__ __forceinline__ void reliability_group(const float (&v)[HPT], int H, 
 
 template <int HPT>
 __global__ __launch_bounds__(kThreads) void head_reliability_kernel(
-    const float* __restrict__ e, float* __restrict__ rho, float* __restrict__ pbar_c, int H,
-    int N, int tiles) {
+    const float* __restrict__ e, float* __restrict__ rho, float* __restrict__ pbar_c,
+    BatchGeom bg, int tiles) {
     __shared__ float red[2 * kHG * kTok];
-    const int64_t bl = blockIdx.x / tiles;
+    const int64_t bl = blockIdx.x / tiles;        // b*L + l
     const int tile = blockIdx.x - static_cast<int>(bl) * tiles;
+    const int64_t b = bl / bg.L;
+    const int l = static_cast<int>(bl - b * bg.L);
+    const ImageGeom ig = image_geom(bg, b);
+    const int H = bg.H, N = ig.N;
+    if (tile * kTok >= N) return;                 // past a smaller image's tokens (whole block)
     const int t = threadIdx.x % kTok, hg = threadIdx.x / kTok;
     const int n = tile * kTok + t;
     const bool ok = n < N;
     float v[HPT];
-    load_heads(v, e + bl * H * static_cast<int64_t>(N), N, n, ok, hg, H);
+    load_heads(v, e + bg.L * H * ig.tok + static_cast<int64_t>(l) * H * N, N, n, ok, hg, H);
     float r, eb;
     reliability_group(v, H, hg, t, red, r, eb);
     if (hg == 0 && ok) {
-        rho[bl * N + n] = r;
-        pbar_c[bl * N + n] = eb;
+        const int64_t o = bg.L * ig.tok + static_cast<int64_t>(l) * N + n;
+        rho[o] = r;
+        pbar_c[o] = eb;
     }
 }
 
@@ -177,8 +183,7 @@ template <int HPT> struct RelLaunch {
     static hipError_t run(const Dims& d, const float* e, float* rho, float* pbar, hipStream_t st) {
         const int tiles = static_cast<int>((d.N + kTok - 1) / kTok);
         hipLaunchKernelGGL(head_reliability_kernel<HPT>, dim3(static_cast<unsigned>(d.B * d.L * tiles)),
-                           dim3(kThreads), 0, st, e, rho, pbar, static_cast<int>(d.H),
-                           static_cast<int>(d.N), tiles);
+                           dim3(kThreads), 0, st, e, rho, pbar, batch_geom(d), tiles);
         return hipGetLastError();
     }
 };

@@ -51,21 +51,28 @@ __device__ __forceinline__ int wave_uniform(int v) { return __builtin_amdgcn_rea
 template <typename T, int D>
 __global__ __launch_bounds__(kMaxWaves * kWave) void layer_evidence_kernel(
     const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ rho_out,
-    float* __restrict__ pbar_out, int H, int NT, int N, float qscale) {
+    float* __restrict__ pbar_out, BatchGeom bg, float scale) {
     using G = WaveRows<T, D>;
     constexpr int CR = 2 * G::BATCH;      // key rows per unit
+    const int64_t b = blockIdx.x / bg.L;  // workgroup (b, l)
+    const int l = static_cast<int>(blockIdx.x - b * bg.L);
+    const ImageGeom ig = image_geom(bg, b);
+    const int H = bg.H, NT = ig.NT, N = ig.N;
+    const float qscale = mean_query_scale(scale, NT);
     extern __shared__ float smem[];
     float* buf = smem;                    // [H][N] logits, then supports
     float* qbar = smem + H * N;           // [H][D]
     __shared__ int s_next;                // next unit to hand out
     __shared__ int s_done[kMaxLayerHeads];   // finished units per head
 
-    const int64_t bl = blockIdx.x;        // b*L + l
     const int tid = threadIdx.x, nthreads = blockDim.x;
     const int wave = tid / kWave, lane = tid % kWave, nwaves = nthreads / kWave;
     const int wrow = lane / G::LPR, wl = lane % G::LPR;
     const int nch = (N + CR - 1) / CR, units = H * nch;
-    const T* kl = k + bl * H * static_cast<int64_t>(N) * D + wl * 8;
+    const T* ql = q + ig.q_off + static_cast<int64_t>(l) * H * NT * D;
+    const T* kl = k + ig.k_off + static_cast<int64_t>(l) * H * N * D + wl * 8;
+    float* rho_l = rho_out + bg.L * ig.tok + static_cast<int64_t>(l) * N;
+    float* pbar_l = pbar_out + bg.L * ig.tok + static_cast<int64_t>(l) * N;
 
     if (tid == 0) s_next = nwaves;
     for (int h = tid; h < H; h += nthreads) s_done[h] = 0;
@@ -85,7 +92,7 @@ __global__ __launch_bounds__(kMaxWaves * kWave) void layer_evidence_kernel(
     // ---- 1. query means ---------------------------------------------------------
     for (int h = wave; h < H; h += nwaves) {
         float qb[8];
-        wave_query_mean<T, D>(q + ((bl * H + h) * NT) * D + wl * 8, NT, wrow, qscale, qb);
+        wave_query_mean<T, D>(ql + static_cast<int64_t>(h) * NT * D + wl * 8, NT, wrow, qscale, qb);
         if (wrow == 0) {
 #pragma unroll
             for (int m = 0; m < 8; ++m) qbar[h * D + wl * 8 + m] = qb[m];
@@ -140,8 +147,8 @@ __global__ __launch_bounds__(kMaxWaves * kWave) void layer_evidence_kernel(
         for (int hh = g; hh < H; hh += 4) d += fabsf(buf[hh * N + n] - ebar);
         const float s2 = quad_sum_in_order(d);
         if (g == 0) {
-            rho_out[bl * N + n] = reliability_from_sums(s1, s2, two_over_h);
-            pbar_out[bl * N + n] = ebar;
+            rho_l[n] = reliability_from_sums(s1, s2, two_over_h);
+            pbar_l[n] = ebar;
         }
     }
 }
@@ -151,7 +158,7 @@ size_t layer_lds(const Dims& d) {
 }
 
 template <typename T, int D>
-hipError_t launch_layer(const Dims& d, float qscale, const void* q, const void* k, float* rho,
+hipError_t launch_layer(const Dims& d, float scale, const void* q, const void* k, float* rho,
                         float* pbar, hipStream_t st) {
     const size_t lds = layer_lds(d);
     auto kern = layer_evidence_kernel<T, D>;
@@ -164,8 +171,7 @@ hipError_t launch_layer(const Dims& d, float qscale, const void* q, const void* 
     const int waves = static_cast<int>(std::min<int64_t>(d.H, kMaxWaves));
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B * d.L)), dim3(waves * kWave), lds, st,
                        static_cast<const T*>(q), static_cast<const T*>(k), rho, pbar,
-                       static_cast<int>(d.H), static_cast<int>(d.NT), static_cast<int>(d.N),
-                       qscale);
+                       batch_geom(d), scale);
     return hipGetLastError();
 }
 
@@ -177,13 +183,12 @@ bool layer_evidence_fits(const Dims& d) {
 
 hipError_t launch_layer_evidence(const Dims& d, int dtype, float scale, const void* q,
                                  const void* k, float* rho, float* pbar_c, hipStream_t stream) {
-    const float qscale = static_cast<float>(static_cast<double>(scale) / static_cast<double>(d.NT));
     if (dtype == E2S_DTYPE_BF16) {
-        if (d.D == 128) return launch_layer<uint16_t, 128>(d, qscale, q, k, rho, pbar_c, stream);
-        return launch_layer<uint16_t, 64>(d, qscale, q, k, rho, pbar_c, stream);
+        if (d.D == 128) return launch_layer<uint16_t, 128>(d, scale, q, k, rho, pbar_c, stream);
+        return launch_layer<uint16_t, 64>(d, scale, q, k, rho, pbar_c, stream);
     }
-    if (d.D == 128) return launch_layer<float, 128>(d, qscale, q, k, rho, pbar_c, stream);
-    return launch_layer<float, 64>(d, qscale, q, k, rho, pbar_c, stream);
+    if (d.D == 128) return launch_layer<float, 128>(d, scale, q, k, rho, pbar_c, stream);
+    return launch_layer<float, 64>(d, scale, q, k, rho, pbar_c, stream);
 }
 
 }  // namespace e2s

@@ -64,31 +64,37 @@ constexpr int kLdsBudget = 96 * 1024;         // bytes of dynamic LDS per workgr
 template <typename T, int D, int HC>
 __global__ __launch_bounds__(kGroupKernelThreads) void score_group_kernel(
     const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
-    float* __restrict__ r_out, int H, int Hkv, int NT, int N, int group, int hchunk,
-    int nchunks, float qscale) {
+    float* __restrict__ r_out, BatchGeom bg, int group, int hchunk, int nchunks, float scale) {
     using G = WaveRows<T, D>;
     constexpr int KU = G::KU / 2;         // rows per lane per batch (registers: HC q-means)
     constexpr int BATCH = KU * G::RPW;
     constexpr int NW = kGroupKernelThreads / kWave;
+    const int64_t unit = blockIdx.x / nchunks;    // (b*L + l)*Hkv + g
+    const int ci = static_cast<int>(blockIdx.x - unit * nchunks);
+    const int64_t b = unit / (bg.L * bg.Hkv);
+    const int lkv = static_cast<int>(unit - b * bg.L * bg.Hkv);   // l*Hkv + g
+    const int l = lkv / bg.Hkv, g = lkv - l * bg.Hkv;
+    const ImageGeom ig = image_geom(bg, b);
+    const int H = bg.H, NT = ig.NT, N = ig.N;
+    const float qscale = mean_query_scale(scale, NT);
     extern __shared__ float smem[];
     float* qbar = smem;                   // [hchunk][D]
     float* a = smem + hchunk * D;         // [hchunk][N]
 
-    const int unit = blockIdx.x / nchunks;        // (b*L + l)*Hkv + g
-    const int ci = blockIdx.x - unit * nchunks;
-    const int g = unit % Hkv;
-    const int64_t bl = unit / Hkv;
     const int h0 = g * group + ci * hchunk;
     const int nh = min(hchunk, group - ci * hchunk);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int wrow = lane / G::LPR, wl = lane % G::LPR;
-    const T* kg = k + static_cast<int64_t>(unit) * N * D + wl * 8;
+    const T* kg = k + ig.k_off + static_cast<int64_t>(lkv) * N * D + wl * 8;
+    const T* ql = q + ig.q_off + static_cast<int64_t>(l) * H * NT * D;
+    const int64_t erow = bg.L * bg.H * ig.tok + static_cast<int64_t>(l) * H * N;
 
     Packet<T> ka[KU], kb[KU];
     load_key_batch<T, D>(ka, kg, wave * BATCH, wrow, N);
     for (int j = wave; j < nh; j += NW) {
         float qb[8];
-        wave_query_mean<T, D>(q + ((bl * H + h0 + j) * NT) * D + wl * 8, NT, wrow, qscale, qb);
+        wave_query_mean<T, D>(ql + static_cast<int64_t>(h0 + j) * NT * D + wl * 8, NT, wrow, qscale,
+                              qb);
         if (wrow == 0) {
 #pragma unroll
             for (int m = 0; m < 8; ++m) qbar[j * D + wl * 8 + m] = qb[m];
@@ -127,7 +133,7 @@ __global__ __launch_bounds__(kGroupKernelThreads) void score_group_kernel(
     __syncthreads();
 
     for (int j = wave; j < nh; j += NW) {
-        const int64_t row = (bl * H + h0 + j) * static_cast<int64_t>(N);
+        const int64_t row = erow + static_cast<int64_t>(h0 + j) * N;
         wave_softmax_store(a + j * N, N, lane, e_out + row, r_out ? r_out + row : nullptr);
     }
 }
@@ -178,8 +184,15 @@ __device__ __forceinline__ void split_bf16x3(float x, uint16_t& hi, uint16_t& mi
 template <int D>
 __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, float* __restrict__ e_out,
-    float* __restrict__ r_out, int H, int Hkv, int NT, int N, int group, int hchunk,
-    int nchunks, float qscale) {
+    float* __restrict__ r_out, BatchGeom bg, int group, int hchunk, int nchunks, float scale) {
+    const int64_t unit = blockIdx.x / nchunks;    // (b*L + l)*Hkv + g
+    const int ci = static_cast<int>(blockIdx.x - unit * nchunks);
+    const int64_t b = unit / (bg.L * bg.Hkv);
+    const int lkv = static_cast<int>(unit - b * bg.L * bg.Hkv);   // l*Hkv + g
+    const int l = lkv / bg.Hkv, g = lkv - l * bg.Hkv;
+    const ImageGeom ig = image_geom(bg, b);
+    const int H = bg.H, NT = ig.NT, N = ig.N;
+    const float qscale = mean_query_scale(scale, NT);
     constexpr int NS = D / 32;            // MFMA steps per tile
     constexpr int P = kTilesInFlight;
     constexpr int NW = kGroupKernelThreads / kWave;
@@ -189,15 +202,13 @@ __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kerne
     float* qbar = smem_mfma + 3 * 16 * BS / 2;                    // [hchunk][D]
     float* a = qbar + hchunk * D;         // [hchunk][N], rows 16-byte aligned if 4 | N
 
-    const int unit = blockIdx.x / nchunks;        // (b*L + l)*Hkv + g
-    const int ci = blockIdx.x - unit * nchunks;
-    const int g = unit % Hkv;
-    const int64_t bl = unit / Hkv;
     const int h0 = g * group + ci * hchunk;
     const int nh = min(hchunk, group - ci * hchunk);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int lr = lane % 16, lg = lane / 16;
-    const uint16_t* kg = k + static_cast<int64_t>(unit) * N * D + 8 * lg;
+    const uint16_t* kg = k + ig.k_off + static_cast<int64_t>(lkv) * N * D + 8 * lg;
+    const uint16_t* ql = q + ig.q_off + static_cast<int64_t>(l) * H * NT * D;
+    const int64_t erow = bg.L * bg.H * ig.tok + static_cast<int64_t>(l) * H * N;
     const int tiles = (N + 15) / 16;
     const int cnt = wave < tiles ? (tiles - wave + NW - 1) / NW : 0;   // this wave's tiles
 
@@ -219,8 +230,8 @@ __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kerne
         const int wrow = lane / G::LPR, wl = lane % G::LPR;
         for (int j = wave; j < nh; j += NW) {
             float qb[8];
-            wave_query_mean<uint16_t, D, kQueryRows>(q + ((bl * H + h0 + j) * NT) * D + wl * 8,
-                                                     NT, wrow, qscale, qb);
+            wave_query_mean<uint16_t, D, kQueryRows>(
+                ql + static_cast<int64_t>(h0 + j) * NT * D + wl * 8, NT, wrow, qscale, qb);
             if (wrow == 0) {
 #pragma unroll
                 for (int m = 0; m < 8; ++m) qbar[j * D + wl * 8 + m] = qb[m];
@@ -282,13 +293,13 @@ __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kerne
 
     // ---- 3. softmax and supports per head ----------------------------------------
     for (int j = wave; j < nh; j += NW) {
-        const int64_t row = (bl * H + h0 + j) * static_cast<int64_t>(N);
+        const int64_t row = erow + static_cast<int64_t>(h0 + j) * N;
         wave_softmax_store(a + j * N, N, lane, e_out + row, r_out ? r_out + row : nullptr);
     }
 }
 
 template <int D>
-hipError_t launch_group_mfma(const Dims& d, float qscale, const void* q, const void* k, float* e,
+hipError_t launch_group_mfma(const Dims& d, float scale, const void* q, const void* k, float* e,
                              float* r, int hchunk, hipStream_t st) {
     const int nchunks = static_cast<int>((d.group + hchunk - 1) / hchunk);
     const size_t lds = 3 * 16 * (D + 8) * sizeof(uint16_t) +
@@ -303,13 +314,12 @@ hipError_t launch_group_mfma(const Dims& d, float qscale, const void* q, const v
     const int64_t blocks = d.B * d.L * d.Hkv * nchunks;
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(blocks)), dim3(kGroupKernelThreads), lds,
                        st, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), e, r,
-                       static_cast<int>(d.H), static_cast<int>(d.Hkv), static_cast<int>(d.NT),
-                       static_cast<int>(d.N), static_cast<int>(d.group), hchunk, nchunks, qscale);
+                       batch_geom(d), static_cast<int>(d.group), hchunk, nchunks, scale);
     return hipGetLastError();
 }
 
 template <typename T, int D, int HC>
-hipError_t launch_group(const Dims& d, float qscale, const void* q, const void* k, float* e,
+hipError_t launch_group(const Dims& d, float scale, const void* q, const void* k, float* e,
                         float* r, int hchunk, hipStream_t st) {
     const int nchunks = static_cast<int>((d.group + hchunk - 1) / hchunk);
     const size_t lds = static_cast<size_t>(hchunk) * (D + d.N) * sizeof(float);
@@ -323,8 +333,7 @@ hipError_t launch_group(const Dims& d, float qscale, const void* q, const void* 
     const int64_t blocks = d.B * d.L * d.Hkv * nchunks;
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(blocks)), dim3(kGroupKernelThreads), lds,
                        st, static_cast<const T*>(q), static_cast<const T*>(k), e, r,
-                       static_cast<int>(d.H), static_cast<int>(d.Hkv), static_cast<int>(d.NT),
-                       static_cast<int>(d.N), static_cast<int>(d.group), hchunk, nchunks, qscale);
+                       batch_geom(d), static_cast<int>(d.group), hchunk, nchunks, scale);
     return hipGetLastError();
 }
 
@@ -334,18 +343,25 @@ hipError_t launch_group(const Dims& d, float qscale, const void* q, const void* 
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void score_wave_kernel(
     const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
-    float* __restrict__ r_out, int64_t units, int NT, int N, float qscale) {
+    float* __restrict__ r_out, BatchGeom bg, int64_t units, int nmax, float scale) {
     extern __shared__ float smem[];
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int64_t unit = static_cast<int64_t>(blockIdx.x) * (blockDim.x / kWave) + wave;
     if (unit >= units) return;
-    float* a = smem + wave * N;
-    wave_head<T, D>(q + unit * NT * D, k + unit * N * D, NT, N, qscale, a, lane, e_out + unit * N,
-                    r_out ? r_out + unit * N : nullptr);
+    const int64_t b = unit / (bg.L * bg.H);               // unit = (b*L + l)*H + h
+    const int lh = static_cast<int>(unit - b * bg.L * bg.H);
+    const ImageGeom ig = image_geom(bg, b);
+    const int NT = ig.NT, N = ig.N;
+    float* a = smem + wave * nmax;
+    const int64_t row = bg.L * bg.H * ig.tok + static_cast<int64_t>(lh) * N;
+    wave_head<T, D>(q + ig.q_off + static_cast<int64_t>(lh) * NT * D,
+                    k + ig.k_off + static_cast<int64_t>(lh) * N * D, NT, N,
+                    mean_query_scale(scale, NT), a, lane, e_out + row,
+                    r_out ? r_out + row : nullptr);
 }
 
 template <typename T, int D>
-hipError_t launch_wave(const Dims& d, float qscale, const void* q, const void* k, float* e,
+hipError_t launch_wave(const Dims& d, float scale, const void* q, const void* k, float* e,
                        float* r, hipStream_t st) {
     const int64_t per_wave = d.N * static_cast<int64_t>(sizeof(float));
     const int wpg = static_cast<int>(std::clamp<int64_t>(kLdsBudget / per_wave, 1, kWaves));
@@ -360,15 +376,15 @@ hipError_t launch_wave(const Dims& d, float qscale, const void* q, const void* k
         if (err != hipSuccess) return err;
     }
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(blocks)), dim3(wpg * kWave), lds, st,
-                       static_cast<const T*>(q), static_cast<const T*>(k), e, r, units,
-                       static_cast<int>(d.NT), static_cast<int>(d.N), qscale);
+                       static_cast<const T*>(q), static_cast<const T*>(k), e, r, batch_geom(d),
+                       units, static_cast<int>(d.N), scale);
     return hipGetLastError();
 }
 
 template <typename T, int D>
-hipError_t dispatch(const Dims& d, float qscale, const void* q, const void* k, float* e, float* r,
+hipError_t dispatch(const Dims& d, float scale, const void* q, const void* k, float* e, float* r,
                     hipStream_t st) {
-    if (d.group == 1) return launch_wave<T, D>(d, qscale, q, k, e, r, st);
+    if (d.group == 1) return launch_wave<T, D>(d, scale, q, k, e, r, st);
     // query heads per workgroup: all of the group, at most one MFMA tile's columns
     // (bf16) or kMaxChunk (fp32), and as many as fit the LDS budget with their
     // logits; chunks balanced
@@ -378,10 +394,10 @@ hipError_t dispatch(const Dims& d, float qscale, const void* q, const void* k, f
         std::min<int64_t>({d.group, mfma ? kMfmaMaxChunk : kMaxChunk, fit}));
     const int nchunks = static_cast<int>((d.group + hchunk - 1) / hchunk);
     hchunk = static_cast<int>((d.group + nchunks - 1) / nchunks);
-    if constexpr (mfma) return launch_group_mfma<D>(d, qscale, q, k, e, r, hchunk, st);
-    if (hchunk <= 2) return launch_group<T, D, 2>(d, qscale, q, k, e, r, hchunk, st);
-    if (hchunk <= 4) return launch_group<T, D, 4>(d, qscale, q, k, e, r, hchunk, st);
-    return launch_group<T, D, 8>(d, qscale, q, k, e, r, hchunk, st);
+    if constexpr (mfma) return launch_group_mfma<D>(d, scale, q, k, e, r, hchunk, st);
+    if (hchunk <= 2) return launch_group<T, D, 2>(d, scale, q, k, e, r, hchunk, st);
+    if (hchunk <= 4) return launch_group<T, D, 4>(d, scale, q, k, e, r, hchunk, st);
+    return launch_group<T, D, 8>(d, scale, q, k, e, r, hchunk, st);
 }
 
 }  // namespace
@@ -389,14 +405,13 @@ hipError_t dispatch(const Dims& d, float qscale, const void* q, const void* k, f
 hipError_t launch_score_mean_logit(const Dims& d, int dtype, float scale, const void* q,
                                    const void* k, float* support_c, float* r_opt,
                                    hipStream_t stream) {
-    const float qscale = static_cast<float>(static_cast<double>(scale) / static_cast<double>(d.NT));
     if (dtype == E2S_DTYPE_BF16) {
         if (d.D == 128)
-            return dispatch<uint16_t, 128>(d, qscale, q, k, support_c, r_opt, stream);
-        return dispatch<uint16_t, 64>(d, qscale, q, k, support_c, r_opt, stream);
+            return dispatch<uint16_t, 128>(d, scale, q, k, support_c, r_opt, stream);
+        return dispatch<uint16_t, 64>(d, scale, q, k, support_c, r_opt, stream);
     }
-    if (d.D == 128) return dispatch<float, 128>(d, qscale, q, k, support_c, r_opt, stream);
-    return dispatch<float, 64>(d, qscale, q, k, support_c, r_opt, stream);
+    if (d.D == 128) return dispatch<float, 128>(d, scale, q, k, support_c, r_opt, stream);
+    return dispatch<float, 64>(d, scale, q, k, support_c, r_opt, stream);
 }
 
 }  // namespace e2s

@@ -87,6 +87,12 @@ __device__ __forceinline__ void key_batch_logits(const Packet<T> (&p)[KU], const
     }
 }
 
+// Scale of the summed queries: Eq. 1's logit scale over N_T, rounded once from
+// the double quotient (per image, since a ragged batch has one N_T per image).
+__device__ __forceinline__ float mean_query_scale(float scale, int NT) {
+    return static_cast<float>(static_cast<double>(scale) / static_cast<double>(NT));
+}
+
 // Query mean of one head by one wave: lane (wrow, wl) sums rows wrow, wrow + RPW,
 // ... of dims 8*wl .. 8*wl+7 in increasing row order; the RPW row sums are then
 // combined by a butterfly, so every lane holds the same qbar (times qscale).  qh is

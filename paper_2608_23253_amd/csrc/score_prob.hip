@@ -196,8 +196,7 @@ struct ScaledSeries {
 template <typename T, int D, int TG>
 __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_kernel(
     const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
-    float* __restrict__ r_out, int H, int NT, int N, int group, int Hkv, float scale,
-    int nblocks, int qcap) {
+    float* __restrict__ r_out, BatchGeom bg, int group, float scale, int nblocks, int qcap) {
     using C = ProbCfg<T, D>;
     constexpr int QS = C::QS, NA = C::NA;
     using AFrag = typename C::AFrag;
@@ -213,16 +212,25 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
     float* colsum = lstat + 3 * qbcap * kThreads;                // [N]
     __shared__ int s_far;                                        // some |z s - c_t| > 1/8
 
-    const int bid = xcd_remap(blockIdx.x, nblocks);              // (b*L + l)*H + h
-    const int h = bid % H;
-    const int64_t bl = bid / H;
+    const int64_t bid = xcd_remap(blockIdx.x, nblocks);          // (b*L + l)*H + h
+    const int64_t b = bid / (bg.L * bg.H);
+    const int lh = static_cast<int>(bid - b * bg.L * bg.H);
+    const int l = lh / bg.H, h = lh - l * bg.H;
     const int g = h / group;
-    const T* qh = q + (bl * H + h) * static_cast<int64_t>(NT) * D;
-    const T* kg = k + (bl * Hkv + g) * static_cast<int64_t>(N) * D;
+    const ImageGeom ig = image_geom(bg, b);
+    const int NT = ig.NT, N = ig.N;
+    const T* qh = q + ig.q_off + static_cast<int64_t>(lh) * NT * D;
+    const T* kg = k + ig.k_off + static_cast<int64_t>(l * bg.Hkv + g) * N * D;
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const int lr = lane % 16, lg = lane / 16;
+    // Key tiles of 16 rows go to the waves round-robin (wave w: tiles w, w + 4,
+    // w + 8, ...), and a wave takes its own tiles TG at a time, in ascending order.
+    // The tile a lane sees, and the order in which its sums run, do not depend on
+    // TG, so the results do not either.
     const int ntiles = (N + 15) / 16;
-    const int ngroups = (ntiles + TG - 1) / TG;
+    const int ntw = wave < ntiles ? (ntiles - wave + kWaves - 1) / kWaves : 0;  // this wave's
+    const int ngw = (ntw + TG - 1) / TG;                                       // groups
+    auto tile_of = [&](int j, int tt) { return wave + kWaves * (j * TG + tt); };
     const float fN = static_cast<float>(N);
     const int koff = std::is_same<T, float>::value ? 4 * lg : 8 * lg;
     // this lane's statistics of query block qb: series sum E, or online (max,
@@ -231,31 +239,32 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
     float* lE = lstat + qbcap * kThreads + tid;
     float* lS = lstat + 2 * qbcap * kThreads + tid;
 
-    // keys of group gi (TG tiles of 16 rows) into A-operand registers; rows past N
-    // repeat row N - 1
-    auto load_group = [&](AFrag (&a)[TG][NA], int gi) {
+    // keys of this wave's group j (TG tiles of 16 rows) into A-operand registers;
+    // rows past N repeat row N - 1
+    auto load_group = [&](AFrag (&a)[TG][NA], int j) {
 #pragma unroll
         for (int tt = 0; tt < TG; ++tt) {
-            const int key = (gi * TG + tt) * 16 + lr;
+            const int key = tile_of(j, tt) * 16 + lr;
             load_keys<NA>(a[tt], kg + static_cast<int64_t>(min(key, N - 1)) * D + koff);
         }
     };
+    // no key of group j lies past N
+    auto group_full = [&](int j) { return (tile_of(j, TG - 1) + 1) * 16 <= N; };
 
-    // body(a, gi) for every group gi of this wave, the next group's keys requested
+    // body(a, j) for every group j of this wave, the next group's keys requested
     // before the current one is used.  The requests are unconditional (past the
     // last group they repeat it), so every path has the same loads in flight and
     // the wait before a group's first use leaves the next group's loads pending.
     auto stream_groups = [&](auto&& body) {
         AFrag a0[TG][NA], a1[TG][NA];
-        const int last = ngroups - 1;
-        load_group(a0, min(wave, last));
-        for (int gi = wave; gi < ngroups; gi += 2 * kWaves) {
-            const int g1 = gi + kWaves;
-            load_group(a1, min(g1, last));
-            body(a0, gi);
-            if (g1 >= ngroups) break;
-            load_group(a0, min(g1 + kWaves, last));
-            body(a1, g1);
+        const int last = max(ngw - 1, 0);
+        load_group(a0, 0);
+        for (int j = 0; j < ngw; j += 2) {
+            load_group(a1, min(j + 1, last));
+            body(a0, j);
+            if (j + 1 >= ngw) break;
+            load_group(a0, min(j + 2, last));
+            body(a1, j + 1);
         }
     };
 
@@ -303,8 +312,8 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
         const ScaledSeries<5> p5(scale);
         const ScaledSeries<6> p6(scale);
         float amax = 0.f;                                         // largest |y| seen
-        stream_groups([&](const AFrag (&a)[TG][NA], int gi) {
-            const bool full = (gi + 1) * TG * 16 <= N;            // no key past N
+        stream_groups([&](const AFrag (&a)[TG][NA], int j) {
+            const bool full = group_full(j);
             for (int qb = 0; qb < QB; ++qb) {
                 AFrag bq[NA];
                 load_queries<D>(bq, qs, qb * 16, lr, lg);
@@ -319,7 +328,7 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
                 if (!full) {
 #pragma unroll
                     for (int i = 0; i < TG * 4; ++i)
-                        y[i] = ((gi * TG + i / 4) * 16 + 4 * lg + i % 4 < N) ? y[i] : 0.f;
+                        y[i] = (tile_of(j, i / 4) * 16 + 4 * lg + i % 4 < N) ? y[i] : 0.f;
                 }
                 float E = lE[qb * kThreads];
 #pragma unroll
@@ -359,15 +368,15 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
                 lS[qb * kThreads] = 0.f;
             }
             float cnt = 0.f;                                      // valid keys seen by this lane
-            for (int gi = wave; gi < ngroups; gi += kWaves) {
+            for (int j = 0; j < ngw; ++j) {
                 AFrag a[TG][NA];
-                load_group(a, gi);
+                load_group(a, j);
                 bool kval[TG][4];
 #pragma unroll
                 for (int tt = 0; tt < TG; ++tt)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) kval[tt][r] = (gi * TG + tt) * 16 + 4 * lg + r < N;
-                const bool full = (gi + 1) * TG * 16 <= N;
+                    for (int r = 0; r < 4; ++r) kval[tt][r] = tile_of(j, tt) * 16 + 4 * lg + r < N;
+                const bool full = group_full(j);
                 float cntg = 0.f;                                 // valid keys of this lane here
 #pragma unroll
                 for (int tt = 0; tt < TG; ++tt)
@@ -476,18 +485,18 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
 
         // ---- pass 2: per key, sum over queries of expm1(z s - c_t - L_t) ---------
         // (zero query rows past N_T have z = 0 and shift 0: they add expm1(0) = 0)
-        auto add_columns = [&](const float (&col)[TG * 4], int gi, float unit) {
+        auto add_columns = [&](const float (&col)[TG * 4], int j, float unit) {
 #pragma unroll
             for (int i = 0; i < TG * 4; ++i) {
                 const float sum = group_sum<16>(col[i]);
-                const int key = (gi * TG + i / 4) * 16 + 4 * lg + i % 4;
+                const int key = tile_of(j, i / 4) * 16 + 4 * lg + i % 4;
                 if (lr == 0 && key < N) colsum[key] += unit * sum;
             }
         };
         if (!far) {
             // y = z - shift; |s y| <= 1/4: the degree-6 series; the column sums are
             // in units of s
-            stream_groups([&](const AFrag (&a)[TG][NA], int gi) {
+            stream_groups([&](const AFrag (&a)[TG][NA], int j) {
                 float col[TG * 4];
 #pragma unroll
                 for (int i = 0; i < TG * 4; ++i) col[i] = 0.f;
@@ -505,12 +514,12 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
                         }
                     }
                 }
-                add_columns(col, gi, scale);
+                add_columns(col, j, scale);
             });
         } else {
-            for (int gi = wave; gi < ngroups; gi += kWaves) {
+            for (int j = 0; j < ngw; ++j) {
                 AFrag a[TG][NA];
-                load_group(a, gi);
+                load_group(a, j);
                 float col[TG * 4];
 #pragma unroll
                 for (int i = 0; i < TG * 4; ++i) col[i] = 0.f;
@@ -538,13 +547,13 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
                         for (int i = 0; i < TG * 4; ++i) col[i] += expm1f(x[i]);
                     }
                 }
-                add_columns(col, gi, 1.0f);
+                add_columns(col, j, 1.0f);
             }
         }
     }
     __syncthreads();
 
-    const int64_t row = (bl * H + h) * static_cast<int64_t>(N);
+    const int64_t row = bg.L * bg.H * ig.tok + static_cast<int64_t>(lh) * N;
     const float inv_nt = 1.0f / static_cast<float>(NT);
     for (int n = tid; n < N; n += kThreads) {
         const float u = colsum[n] * inv_nt;
@@ -570,8 +579,7 @@ hipError_t launch_mp(const Dims& d, float scale, const void* q, const void* k, f
     const int64_t blocks = d.B * d.L * d.H;
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), lds, st,
                        static_cast<const T*>(q), static_cast<const T*>(k), e, r,
-                       static_cast<int>(d.H), static_cast<int>(d.NT), static_cast<int>(d.N),
-                       static_cast<int>(d.group), static_cast<int>(d.Hkv), scale,
+                       batch_geom(d), static_cast<int>(d.group), scale,
                        static_cast<int>(blocks), qcap);
     return hipGetLastError();
 }

@@ -126,12 +126,13 @@ struct SelectShared {
 
 // Selection of one image (Eq. 20-23).  cv[j] = c and posv[j] = raster position
 // of token n0 + j for j < cnt (registers of the calling thread, tokens owned as
-// described above); best: G*G words of LDS.  Calls keep(slot, j) once for every
+// described above); best: G*G words of LDS; tok: the image's first token in the
+// optional per-token outputs.  Calls keep(slot, j) once for every
 // kept token (slot = its rank in ascending token order).  All threads of the
 // workgroup call it.
 template <int MAXC, typename Keep>
 __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], int n0, int cnt,
-                             int chunk, uint64_t* best, SelectShared& sh, int64_t b,
+                             int chunk, uint64_t* best, SelectShared& sh, int64_t tok,
                              double* __restrict__ adj_out, uint8_t* __restrict__ rep_out, int N,
                              int gh, int gw, int G, float lambda, int K, Keep&& keep) {
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
@@ -185,8 +186,8 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], i
             kk[j] = ordered_bits(adj);
             kmin = kk[j] < kmin ? kk[j] : kmin;
             kmax = kk[j] > kmax ? kk[j] : kmax;
-            if (adj_out) adj_out[b * N + n] = adj;
-            if (rep_out) rep_out[b * N + n] = rep ? 1 : 0;
+            if (adj_out) adj_out[tok + n] = adj;
+            if (rep_out) rep_out[tok + n] = rep ? 1 : 0;
         }
     }
     if (K <= 0) return;
@@ -335,18 +336,18 @@ __global__ __launch_bounds__(kThreads) void spatial_select_kernel(
         cv[j] = cb[min(n0 + j, N - 1)];     // in bounds; unused past cnt
         posv[j] = n0 + j;
     }
-    select_image<MAXC>(cv, posv, n0, cnt, chunk, best, sh, b, adj_out, rep_out, N, gh, gw, G,
+    select_image<MAXC>(cv, posv, n0, cnt, chunk, best, sh, b * N, adj_out, rep_out, N, gh, gw, G,
                        lambda, K, [&](int slot, int j) { keep_idx[b * K + slot] = n0 + j; });
 }
 
 // Raster positions of the owned tokens (candidate positions when given).
 template <int MAXC>
 __device__ __forceinline__ void owned_positions(int (&posv)[MAXC], const int32_t* cand_pos,
-                                                int64_t b, int N, int n0, int cnt, int chunk) {
+                                                int64_t tok, int n0, int cnt, int chunk) {
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
         if (j >= chunk) break;
-        posv[j] = cand_pos ? (j < cnt ? cand_pos[b * N + n0 + j] : -1) : n0 + j;
+        posv[j] = cand_pos ? (j < cnt ? cand_pos[tok + n0 + j] : -1) : n0 + j;
     }
 }
 
@@ -360,14 +361,16 @@ __device__ __forceinline__ void owned_positions(int (&posv)[MAXC], const int32_t
 template <int MAXC>
 __global__ __launch_bounds__(kThreads) void ds_select_kernel(
     const float* __restrict__ rho, const float* __restrict__ pbar_c,
-    const float* __restrict__ m_prev, SelectArgs a, int L, int N, int gh, int gw) {
+    const float* __restrict__ m_prev, SelectArgs a, BatchGeom bg) {
     extern __shared__ uint64_t best[];
     __shared__ SelectShared sh;
     const int64_t b = blockIdx.x;
+    const ImageGeom ig = image_geom(bg, b);
+    const int L = bg.L, N = ig.N, gh = ig.gh, gw = ig.gw, K = ig.K;
+    const int64_t tok = ig.tok;
     const int chunk = (N + kThreads - 1) / kThreads;
     const int n0 = min(N, static_cast<int>(threadIdx.x) * chunk);
     const int cnt = min(N - n0, chunk);
-    const int K = a.keep;
     const bool unit_rho = a.variant == E2S_VARIANT_NO_HEAD_RELIABILITY;
     const bool last_only = a.variant == E2S_VARIANT_NO_LAYER_FUSION;
     const bool carried = m_prev != nullptr && !last_only;
@@ -376,7 +379,7 @@ __global__ __launch_bounds__(kThreads) void ds_select_kernel(
     float r[MAXC], e[MAXC];      // current layer's inputs
     float aI[MAXC], aU[MAXC], aT[MAXC], kl[MAXC];
     auto load_layer = [&](int l, float (&rr)[MAXC], float (&ee)[MAXC]) {
-        const int64_t base = (b * L + l) * N;
+        const int64_t base = L * tok + static_cast<int64_t>(l) * N;
 #pragma unroll
         for (int j = 0; j < MAXC; ++j) {
             if (j >= chunk) break;
@@ -391,7 +394,7 @@ __global__ __launch_bounds__(kThreads) void ds_select_kernel(
         if (j >= chunk) break;
         kl[j] = 0.f;
         if (carried) {
-            const int64_t i = 3 * (b * N + min(n0 + j, N - 1));
+            const int64_t i = 3 * (tok + min(n0 + j, N - 1));
             aI[j] = m_prev[i];
             aU[j] = m_prev[i + 1];
             aT[j] = m_prev[i + 2];
@@ -425,13 +428,13 @@ __global__ __launch_bounds__(kThreads) void ds_select_kernel(
     const bool protect = a.variant != E2S_VARIANT_NO_CONFLICT;
     float cv[MAXC];
     int posv[MAXC];
-    owned_positions<MAXC>(posv, a.cand_pos, b, N, n0, cnt, chunk);
+    owned_positions<MAXC>(posv, a.cand_pos, tok, n0, cnt, chunk);
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
         if (j >= chunk) break;
         cv[j] = priority_complement(aU[j], protect ? kl[j] : 0.0f);
         if (j < cnt) {
-            const int64_t i = b * N + n0 + j;
+            const int64_t i = tok + n0 + j;
             if (a.fused) {
                 a.fused[3 * i + 0] = aI[j];
                 a.fused[3 * i + 1] = aU[j];
@@ -440,9 +443,9 @@ __global__ __launch_bounds__(kThreads) void ds_select_kernel(
             if (a.prio_c) a.prio_c[i] = cv[j];
         }
     }
-    select_image<MAXC>(cv, posv, n0, cnt, chunk, best, sh, b, nullptr, nullptr, N, gh, gw, a.cells,
-                       a.lambda, K, [&](int slot, int j) {
-                           const int64_t o = b * K + slot;
+    select_image<MAXC>(cv, posv, n0, cnt, chunk, best, sh, tok, nullptr, nullptr, N, gh, gw,
+                       a.cells, a.lambda, K, [&](int slot, int j) {
+                           const int64_t o = ig.keep_off + slot;
                            a.keep_idx[o] = n0 + j;
                            if (a.keep_pos) a.keep_pos[o] = posv[j];
                            if (a.m_out) {
@@ -460,19 +463,21 @@ __global__ __launch_bounds__(kThreads) void ds_select_kernel(
 // spatial term; carried masses (m_out) are written vacuous.
 template <int MAXC>
 __global__ __launch_bounds__(kThreads) void attention_select_kernel(
-    const float* __restrict__ support_c, SelectArgs a, int L, int H, int N, int gh, int gw) {
+    const float* __restrict__ support_c, SelectArgs a, BatchGeom bg) {
     extern __shared__ uint64_t best[];
     __shared__ SelectShared sh;
     const int64_t b = blockIdx.x;
+    const ImageGeom ig = image_geom(bg, b);
+    const int L = bg.L, H = bg.H, N = ig.N, gh = ig.gh, gw = ig.gw, K = ig.K;
+    const int64_t tok = ig.tok;
     const int chunk = (N + kThreads - 1) / kThreads;
     const int n0 = min(N, static_cast<int>(threadIdx.x) * chunk);
     const int cnt = min(N - n0, chunk);
-    const int K = a.keep;
     float cv[MAXC];
 #pragma unroll
     for (int j = 0; j < MAXC; ++j) {
         if (j >= chunk) break;
-        const float* eb = support_c + (b * L * H) * static_cast<int64_t>(N) + min(n0 + j, N - 1);
+        const float* eb = support_c + L * H * tok + min(n0 + j, N - 1);
         float s = 0.f;
         for (int lh = 0; lh < L * H; lh += 8) {
             float ev[8];
@@ -485,10 +490,10 @@ __global__ __launch_bounds__(kThreads) void attention_select_kernel(
         cv[j] = -s;
     }
     int posv[MAXC];
-    owned_positions<MAXC>(posv, a.cand_pos, b, N, n0, cnt, chunk);
-    select_image<MAXC>(cv, posv, n0, cnt, chunk, best, sh, b, nullptr, nullptr, N, gh, gw, a.cells,
-                       0.0f, K, [&](int slot, int j) {
-                           const int64_t o = b * K + slot;
+    owned_positions<MAXC>(posv, a.cand_pos, tok, n0, cnt, chunk);
+    select_image<MAXC>(cv, posv, n0, cnt, chunk, best, sh, tok, nullptr, nullptr, N, gh, gw,
+                       a.cells, 0.0f, K, [&](int slot, int j) {
+                           const int64_t o = ig.keep_off + slot;
                            a.keep_idx[o] = n0 + j;
                            if (a.keep_pos) a.keep_pos[o] = posv[j];
                            if (a.m_out) {
@@ -514,8 +519,7 @@ hipError_t launch_dssel(const Dims& d, const SelectArgs& a, const float* rho, co
     hipError_t err = allow_lds(kern, lds);
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(kThreads), lds, st, rho, pbar_c,
-                       m_prev, a, static_cast<int>(d.L), static_cast<int>(d.N),
-                       static_cast<int>(d.gh), static_cast<int>(d.gw));
+                       m_prev, a, batch_geom(d, a.keep));
     return hipGetLastError();
 }
 
@@ -527,8 +531,7 @@ hipError_t launch_attsel(const Dims& d, const SelectArgs& a, const float* suppor
     hipError_t err = allow_lds(kern, lds);
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(kThreads), lds, st, support_c,
-                       a, static_cast<int>(d.L), static_cast<int>(d.H), static_cast<int>(d.N),
-                       static_cast<int>(d.gh), static_cast<int>(d.gw));
+                       a, batch_geom(d, a.keep));
     return hipGetLastError();
 }
 

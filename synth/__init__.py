@@ -31,6 +31,7 @@ import numpy as np
 __all__ = [
     "Config", "CONFIGS", "config_by_name", "gen_image", "gen_batch",
     "to_bf16_bits", "bf16_bits_to_f32", "salient_set", "heavy_tailed",
+    "RaggedConfig", "RAGGED", "ragged_by_name", "ragged_dims", "gen_ragged",
 ]
 
 SEED_ROOT = 2608
@@ -293,3 +294,84 @@ def storage_view(x: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "bf16":
         return to_bf16_bits(x)
     return np.ascontiguousarray(x, dtype=np.float32)
+
+
+# ---------------------------------------------------------------------------
+# ragged batches: every image its own grid, text length and budget
+# ---------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class RaggedConfig:
+    """A ragged workload.  Image b's grid sides are drawn uniformly from
+    grid_sides (rows and columns independently), its text-query count from
+    num_text, and it keeps round(keep_frac * N_b) tokens (at least 1).  The head
+    geometry, storage type and value recipe (salient clusters, shift) come from
+    `base`; image b's tensors are gen_image of base with image b's sizes and this
+    workload's config_id, so every image is reproducible on its own."""
+    name: str
+    config_id: int
+    batch: int
+    base: Config
+    grid_sides: tuple        # (smallest, largest) side
+    num_text: tuple          # (smallest, largest) N_T
+    keep_frac: float
+
+
+# Qwen2-VL-7B with dynamic resolution (Sec. 5: Qwen2-VL-7B's visual tokens come from
+# native-resolution images): 28 query heads over 4 KV heads, grids from 16x16 to
+# 40x40 patches (256-1600 tokens), prompts of 32-160 text tokens, 22.2 % of the
+# tokens kept (the paper's -77.8 % setting for Qwen2-VL, Table 5).
+RAGGED: tuple = (
+    RaggedConfig("qwen2vl_dynamic", 5, batch=32,
+                 base=CONFIGS[3].replace(name="qwen2vl_dynamic", config_id=5),
+                 grid_sides=(16, 40), num_text=(32, 160), keep_frac=0.222),
+)
+
+
+def ragged_by_name(name: str) -> RaggedConfig:
+    for c in RAGGED:
+        if c.name == name:
+            return c
+    raise KeyError(f"unknown ragged workload {name!r}; known: {[c.name for c in RAGGED]}")
+
+
+def ragged_dims(rc: RaggedConfig) -> list:
+    """[(grid_h, grid_w, num_text, keep)] of every image, from the workload's own
+    seeded stream."""
+    rng = np.random.Generator(np.random.Philox(
+        np.random.SeedSequence([SEED_ROOT, rc.config_id, 1 << 30])))
+    lo, hi = rc.grid_sides
+    out = []
+    for _ in range(rc.batch):
+        gh = int(rng.integers(lo, hi + 1))
+        gw = int(rng.integers(lo, hi + 1))
+        nt = int(rng.integers(rc.num_text[0], rc.num_text[1] + 1))
+        keep = max(1, int(round(rc.keep_frac * gh * gw)))
+        out.append((gh, gw, nt, keep))
+    return out
+
+
+def image_config(rc: RaggedConfig, dims: tuple) -> Config:
+    gh, gw, nt, keep = dims
+    return rc.base.replace(config_id=rc.config_id, grid_h=gh, grid_w=gw, num_text=nt, keep=keep)
+
+
+def gen_ragged(rc: RaggedConfig, dims: list | None = None, threads: int | None = None):
+    """Every image of a ragged workload: (list of Q_b [L,H,N_T,b,d] f32, list of
+    K_b [L,Hkv,N_b,d] f32, list of salient sets, dims)."""
+    dims = ragged_dims(rc) if dims is None else list(dims)
+    out = [None] * len(dims)
+    if threads is None:
+        threads = min(16, len(os.sched_getaffinity(0)))
+
+    def one(b):
+        out[b] = gen_image(image_config(rc, dims[b]), b)
+
+    if threads <= 1 or len(dims) == 1:
+        for b in range(len(dims)):
+            one(b)
+    else:
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            list(ex.map(one, range(len(dims))))
+    return [o[0] for o in out], [o[1] for o in out], [o[2] for o in out], dims
+

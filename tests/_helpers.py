@@ -62,6 +62,8 @@ def compare_sets(gpu_keep: np.ndarray, ref: O.ImageResult, gap: float = TIE_GAP)
 
 def check_keep_wellformed(keep: np.ndarray, N: int, K: int):
     assert keep.shape[-1] == K
+    if K == 0:
+        return
     for row in keep.reshape(-1, K):
         assert (np.diff(row) > 0).all(), "keep_idx must be strictly ascending"
         if K:

@@ -67,10 +67,10 @@ def stage(shape, params, ncand, q=A, k=A, pos=A, mprev=None, ws=A, ws_bytes=None
 
 def test_exports_every_declared_entry_point():
     names = L.header_entry_points()
-    assert len(names) == 13
+    assert len(names) == 15
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.e2s_abi_version() == 3
+    assert lib.e2s_abi_version() == 4
 
 
 def test_status_strings():
@@ -206,3 +206,89 @@ def test_stage_validation():
     assert stage(sh, good_params(keep=5), 20, ws_bytes=16) == L.ERR_WORKSPACE_TOO_SMALL
     assert stage(sh, good_params(keep=5), 20, q=None) == L.ERR_NULL_POINTER
     assert stage(sh, good_params(keep=5, cells=7), 20) == L.ERR_BAD_PARAM
+
+
+# ---------------------------------------------------------------------------
+# ragged batches
+# ---------------------------------------------------------------------------
+
+RAGGED_DIMS = [(6, 7, 5, 10), (4, 9, 1, 0), (8, 8, 12, 64)]
+
+
+def ragged_images(dims=RAGGED_DIMS, L_=3, H=4, Hkv=2, D=64):
+    arr, _, _, _, _ = L.packed_images(dims, L_, H, Hkv, D)
+    return arr
+
+
+def ragged(images, params=None, shape=None, dev=A, q=A, k=A, ws=A, ws_bytes=None, out=A):
+    shape = L.RaggedShape(len(images), 3, 4, 2, 64) if shape is None else shape
+    params = good_params() if params is None else params
+    if ws_bytes is None:
+        n = ctypes.c_size_t(0)
+        st = lib.e2s_prune_ragged_workspace_size(ctypes.byref(shape), ctypes.addressof(images),
+                                                 ctypes.byref(n))
+        ws_bytes = n.value if st == L.OK else 1 << 30
+    return lib.e2s_prune_ragged(ctypes.byref(shape), ctypes.byref(params),
+                                ctypes.addressof(images), dev, q, k, ws, ws_bytes, out, None,
+                                None, None)
+
+
+def test_ragged_workspace_size_is_the_token_span():
+    imgs = ragged_images()
+    n = ctypes.c_size_t(0)
+    sh = L.RaggedShape(3, 3, 4, 2, 64)
+    assert lib.e2s_prune_ragged_workspace_size(ctypes.byref(sh), ctypes.addressof(imgs),
+                                               ctypes.byref(n)) == L.OK
+    T = 42 + 36 + 64
+
+    def up(x):
+        return (x + 255) // 256 * 256
+    assert n.value == up(3 * 4 * T * 4) + 2 * up(3 * T * 4)
+    # a uniform batch packed as ragged records needs what e2s_prune needs
+    imgs = ragged_images([(6, 7, 5, 10)] * 2)
+    sh = L.RaggedShape(2, 3, 4, 2, 64)
+    assert lib.e2s_prune_ragged_workspace_size(ctypes.byref(sh), ctypes.addressof(imgs),
+                                               ctypes.byref(n)) == L.OK
+    assert n.value == L.workspace_size(good_shape(), good_params())
+
+
+def test_ragged_rejects_invalid_records():
+    imgs = ragged_images()
+    assert ragged(imgs, ws_bytes=1) == L.ERR_WORKSPACE_TOO_SMALL   # otherwise valid
+    bad = ragged_images()
+    bad[1].token_offset = 10                                        # overlaps image 0
+    assert ragged(bad) == L.ERR_BAD_SHAPE
+    bad = ragged_images()
+    bad[2].keep_offset = 5                                          # overlaps image 0's keep
+    assert ragged(bad) == L.ERR_BAD_SHAPE
+    bad = ragged_images()
+    bad[1].keep_offset = 0                                          # K_b = 0: no range
+    assert ragged(bad, ws_bytes=1) == L.ERR_WORKSPACE_TOO_SMALL
+    bad = ragged_images()
+    bad[0].q_offset = 4                                             # bf16: 8-element steps
+    assert ragged(bad) == L.ERR_MISALIGNED
+    bad = ragged_images()
+    bad[2].keep = 65                                                # K_b > N_b
+    assert ragged(bad) == L.ERR_BAD_PARAM
+    bad = ragged_images()
+    bad[0].num_text = 0
+    assert ragged(bad) == L.ERR_BAD_SHAPE
+    bad = ragged_images()
+    bad[0].grid_h, bad[0].grid_w = 200, 100                         # N_b > 16384
+    assert ragged(bad) == L.ERR_UNSUPPORTED
+    bad = ragged_images()
+    bad[1].k_offset = -8
+    assert ragged(bad) == L.ERR_BAD_SHAPE
+    assert ragged(imgs, params=good_params(cells=5)) == L.ERR_BAD_PARAM   # image 1 is 4x9
+    assert ragged(imgs, params=good_params(lam=1.5)) == L.ERR_BAD_PARAM
+    assert ragged(imgs, dev=None) == L.ERR_NULL_POINTER
+    assert ragged(imgs, dev=A + 4) == L.ERR_MISALIGNED
+    assert ragged(imgs, out=None) == L.ERR_NULL_POINTER           # some K_b > 0
+    assert ragged(imgs, q=A + 8) == L.ERR_MISALIGNED
+    assert ragged(imgs, shape=L.RaggedShape(3, 3, 4, 3, 64)) == L.ERR_BAD_SHAPE   # H % Hkv
+    assert ragged(imgs, shape=L.RaggedShape(3, 3, 4, 2, 96)) == L.ERR_UNSUPPORTED
+    # every K_b = 0: keep_idx may be NULL (then only the workspace is missing here)
+    zero = ragged_images([(6, 7, 5, 0), (4, 9, 1, 0)])
+    assert ragged(zero, shape=L.RaggedShape(2, 3, 4, 2, 64), out=None, ws_bytes=1) == \
+        L.ERR_WORKSPACE_TOO_SMALL
+

@@ -80,3 +80,20 @@ def test_hires_near_duplicates():
                     best = min(best, np.linalg.norm(kk[t] - kk[o]))
         close += best < 0.05
     assert close >= int(round(0.1 * n))
+
+
+def test_ragged_workload_is_seeded_and_in_range():
+    rc = synth.ragged_by_name("qwen2vl_dynamic")
+    d1, d2 = synth.ragged_dims(rc), synth.ragged_dims(rc)
+    assert d1 == d2 and len(d1) == rc.batch
+    for gh, gw, nt, keep in d1:
+        assert rc.grid_sides[0] <= gh <= rc.grid_sides[1]
+        assert rc.grid_sides[0] <= gw <= rc.grid_sides[1]
+        assert rc.num_text[0] <= nt <= rc.num_text[1]
+        assert keep == max(1, round(rc.keep_frac * gh * gw))
+    assert len({(gh, gw) for gh, gw, _, _ in d1}) > rc.batch // 2   # grids really differ
+    # image b is gen_image of the base shape with image b's sizes: reproducible alone
+    qs, ks, _, dims = synth.gen_ragged(rc, dims=d1[:3], threads=1)
+    q1, k1, _ = synth.gen_image(synth.image_config(rc, d1[1]), 1)
+    assert np.array_equal(qs[1], q1) and np.array_equal(ks[1], k1)
+    assert qs[1].shape == (4, 28, d1[1][2], 128) and ks[1].shape == (4, 4, d1[1][0] * d1[1][1], 128)

@@ -8,8 +8,9 @@ in HBM: e2s_layer_reliability (score and head reliability, Eq. 1, 8-10) then
 e2s_fuse_select (masses, fusion and selection, Eq. 11-23).  Prints ONE JSON line
 with images/s, a roofline object for the dominant kernel (the score and
 reliability stage, timed alone with HIP events on the launch stream), per-stage
-times of the staged entry points, and the CPU oracle's throughput on a bounded
-sample.
+times of the staged entry points, the ablation variants, the progressive
+schedule, a ragged batch (e2s_prune_ragged on seeded dynamic-resolution images)
+and the CPU oracle's throughput on a bounded sample.
 
 Other modes (used by the profiling commands kept with the results):
     --kernel-only   run only the timed e2s_prune steps (no CPU baseline)
@@ -203,6 +204,44 @@ def bench_variants_and_schedule(args, cfg, qd, kd, stream, timed):
     return {"variants": variants, "progressive": prog}
 
 
+def bench_ragged(args, timed, name="qwen2vl_dynamic"):
+    """e2s_prune_ragged over a seeded ragged batch (every image its own grid, text
+    length and budget): images/s and the Q + K bytes read per second."""
+    import numpy as np
+    import torch
+    import synth
+    import paper_2608_23253_amd as E
+
+    rc = synth.ragged_by_name(name)
+    qs, ks, _, dims = synth.gen_ragged(rc)
+    cfg = rc.base
+    L_, H_, Hkv, D = cfg.num_layers, cfg.num_heads, cfg.num_kv_heads, cfg.head_dim
+    arr, qtot, ktot, _, _ = E.packed_images(dims, L_, H_, Hkv, D)
+    q = np.concatenate([x.reshape(-1) for x in qs])
+    k = np.concatenate([x.reshape(-1) for x in ks])
+    qd = torch.from_numpy(synth.to_bf16_bits(q).view(np.int16)).cuda().view(torch.bfloat16)
+    kd = torch.from_numpy(synth.to_bf16_bits(k).view(np.int16)).cuda().view(torch.bfloat16)
+    rp = E.RaggedPruner(arr, L_, H_, Hkv, D, qd.device, mode=args.mode, cells=cfg.cells,
+                        lam=cfg.lam)
+    n_rep = max(20, args.steps // 4)
+    t = timed([lambda: (rp(qd, kd), 0)[1]], n_rep)[0]
+    us = float(t.mean()) * 1e3
+    qk_bytes = (qtot + ktot) * 2
+    n_tok = [gh * gw for gh, gw, _, _ in dims]
+    out = {
+        "workload": (f"{name}: {rc.batch} images, Qwen2-VL-7B-shaped heads ({H_} over {Hkv}, "
+                     f"d {D}, {L_} layers), grids {rc.grid_sides[0]}..{rc.grid_sides[1]} per "
+                     f"side ({min(n_tok)}..{max(n_tok)} tokens), {rc.num_text[0]}..."
+                     f"{rc.num_text[1]} text queries, keep {rc.keep_frac:.1%}"),
+        "us_per_batch": round(us, 2),
+        "images_per_s": round(rc.batch / (us * 1e-6), 1),
+        "qk_bytes_per_batch": int(qk_bytes),
+        "hbm_frac": round(qk_bytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+    }
+    log(f"[bench] ragged {name}: {us:.1f} us per batch -> {out['images_per_s']:.0f} images/s")
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -340,6 +379,7 @@ def main():
     extras = {}
     if not args.no_extras:
         extras = bench_variants_and_schedule(args, cfg, qd, kd, stream, timed)
+        extras["ragged"] = bench_ragged(args, timed)
 
     # ---- CPU oracle baseline ----------------------------------------------------
     import oracle as O

@@ -9,8 +9,9 @@ e2s_fuse_select (masses, fusion and selection, Eq. 11-23).  Prints ONE JSON line
 with images/s, a roofline object for the dominant kernel (the score and
 reliability stage, timed alone with HIP events on the launch stream), per-stage
 times of the staged entry points, the ablation variants, the progressive
-schedule, a ragged batch (e2s_prune_ragged on seeded dynamic-resolution images)
-and the CPU oracle's throughput on a bounded sample.
+schedule, a ragged batch (e2s_prune_ragged on seeded dynamic-resolution images),
+token compaction of the kept tokens (e2s_compact_tokens) and the CPU oracle's
+throughput on a bounded sample.
 
 Other modes (used by the profiling commands kept with the results):
     --kernel-only   run only the timed e2s_prune steps (no CPU baseline)
@@ -242,6 +243,34 @@ def bench_ragged(args, timed, name="qwen2vl_dynamic"):
     return out
 
 
+def bench_compaction(args, timed, kd, keep_idx):
+    """e2s_compact_tokens after the step: the kept tokens' hidden states (LLaVA-1.5-7B
+    width 4096, bf16) and the kept tokens' keys of the source layers (kd), with the
+    kept indices of the step.  Bytes moved = 2 x the kept vectors (read + write)."""
+    import torch
+    import paper_2608_23253_amd as E
+
+    B, L_, Hkv, N, D = kd.shape
+    K = keep_idx.shape[1]
+    hidden = torch.empty((B, 1, N, 4096), device=kd.device, dtype=torch.bfloat16).normal_()
+    h_out = torch.empty((B, 1, K, 4096), device=kd.device, dtype=torch.bfloat16)
+    kk = kd.reshape(B, L_ * Hkv, N, D)
+    k_out = torch.empty((B, L_ * Hkv, K, D), device=kd.device, dtype=kd.dtype)
+    n_rep = max(20, args.steps // 4)
+    th, tk = timed([lambda: (E.compact_tokens(hidden, keep_idx, h_out), 0)[1],
+                    lambda: (E.compact_tokens(kk, keep_idx, k_out), 0)[1]], n_rep)
+    out = {}
+    for name, t, o in (("hidden_states", th, h_out), ("source_layer_keys", tk, k_out)):
+        us = float(t.mean()) * 1e3
+        moved = 2 * o.numel() * o.element_size()
+        out[name] = {"shape": list(o.shape), "us": round(us, 2), "bytes_moved": int(moved),
+                     "GBps": round(moved / (us * 1e-6) / 1e9, 1),
+                     "hbm_frac": round(moved / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+    log("[bench] compaction: " + ", ".join(f"{k} {v['us']:.1f} us ({v['GBps']:.0f} GB/s)"
+                                             for k, v in out.items()))
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -380,6 +409,7 @@ def main():
     if not args.no_extras:
         extras = bench_variants_and_schedule(args, cfg, qd, kd, stream, timed)
         extras["ragged"] = bench_ragged(args, timed)
+        extras["compaction"] = bench_compaction(args, timed, kd, pr.keep_idx)
 
     # ---- CPU oracle baseline ----------------------------------------------------
     import oracle as O

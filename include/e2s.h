@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define E2S_ABI_VERSION 4
+#define E2S_ABI_VERSION 5
 
 #if defined(__GNUC__) || defined(__clang__)
 #define E2S_API __attribute__((visibility("default")))
@@ -292,6 +292,34 @@ E2S_API e2s_status e2s_prune_ragged(const e2s_ragged_shape* shape, const e2s_par
                                     const void* q, const void* k, void* workspace,
                                     size_t workspace_bytes, int32_t* keep_idx,
                                     float* fused_opt, float* prio_c_opt, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Token compaction: the model side of a pruning operation.  Algorithm 1 goes on
+ * with the retained visual tokens only (its Ensure: V_keep; Sec. 4, and Sec. 5.1
+ * for the layers after each pruning layer), so the caller's per-token vectors -
+ * hidden states, and key/value cache rows - of the kept tokens are gathered
+ * into shorter arrays.  A plain gather: no arithmetic of the method.
+ * ------------------------------------------------------------------------- */
+typedef struct {
+    int32_t batch;          /* B >= 1 images                                          */
+    int32_t rows;           /* R >= 1 rows per image (e.g. layers x KV heads, or 1)   */
+    int32_t num_tokens;     /* N >= 1 tokens per row in src                           */
+    int32_t keep;           /* K >= 0 tokens kept per image                           */
+    int32_t channels;       /* C >= 1 elements per token vector, contiguous           */
+    int32_t elem_bytes;     /* 2 or 4                                                 */
+    int64_t src_stride[3];  /* elements between consecutive images, rows and tokens  */
+    int64_t dst_stride[3];  /* the same for dst                                       */
+} e2s_compact_shape;
+
+/* dst[b, r, j, :] = src[b, r, keep_idx[b*K + j], :] for every image b, row r and
+ * j < K (keep_idx [B, K] int32, e.g. e2s_prune's output; device memory).  An index
+ * outside [0, N) leaves its dst vector unwritten.  src and dst are 16-byte
+ * aligned, C * elem_bytes and every stride * elem_bytes are multiples of 16, and
+ * dst must not overlap src.  Strides let src be a slice of a larger buffer (the
+ * visual tokens of a key/value cache [B, Hkv, S, d] are a [B, Hkv, N, d] slice
+ * with strides Hkv*S*d, S*d, d). */
+E2S_API e2s_status e2s_compact_tokens(const e2s_compact_shape* shape, const int32_t* keep_idx,
+                                      const void* src, void* dst, void* stream);
 
 /* Static description of a status code (never NULL). */
 E2S_API const char* e2s_status_string(e2s_status status);

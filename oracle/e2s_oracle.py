@@ -354,6 +354,15 @@ def prune_progressive(q_ops, k_ops, grid_h: int, grid_w: int, budgets, cells: in
     return out
 
 
+def compact_tokens(x: np.ndarray, keep: np.ndarray) -> np.ndarray:
+    """The retained tokens of a pruning operation (Algorithm 1's output V_keep; the
+    layers after a pruning layer see only them, Sec. 5.1): x[..., keep[j], :] for
+    j = 0..K-1 in order, from per-token vectors x [..., N, C].  A gather, no
+    arithmetic."""
+    keep = np.asarray(keep, dtype=np.int64)
+    return np.take(x, keep, axis=-2)
+
+
 def avg_tokens(num_layers: int, n_visual: int, prune_after, kept) -> float:
     """Eq. (24): mean over the num_layers LLM layers of the visual tokens each
     layer processes, when pruning after layers prune_after[j] (1-based) leaves

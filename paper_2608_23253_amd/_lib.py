@@ -8,7 +8,7 @@ HIP kernels.  Two layers are exposed:
   * functions with the C names minus the ``e2s_`` prefix (``score_heads``,
     ``head_reliability``, ``head_masses``, ``ds_combine_layers``,
     ``fuse_evidence``, ``spatial_select``, ``layer_reliability``, ``fuse_select``,
-    ``prune``, ``prune_stage``, ``prune_ragged``) that take torch tensors on
+    ``prune``, ``prune_stage``, ``prune_ragged``, ``compact_tokens``) that take torch tensors on
     the GPU, allocate the outputs with torch, pass raw device pointers and the
     current torch stream, and raise ``E2SError`` on a non-zero status.
 
@@ -66,6 +66,13 @@ class RaggedShape(ctypes.Structure):
                 ("head_dim", ctypes.c_int32)]
 
 
+class CompactShape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("rows", ctypes.c_int32),
+                ("num_tokens", ctypes.c_int32), ("keep", ctypes.c_int32),
+                ("channels", ctypes.c_int32), ("elem_bytes", ctypes.c_int32),
+                ("src_stride", ctypes.c_int64 * 3), ("dst_stride", ctypes.c_int64 * 3)]
+
+
 class E2SError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
@@ -93,6 +100,7 @@ _SIGNATURES = {
                                         ctypes.POINTER(ctypes.c_size_t)],
     "e2s_prune_ragged": [ctypes.POINTER(RaggedShape), _PA, _P, _P, _P, _P, _P, ctypes.c_size_t,
                          _P, _P, _P, _P],
+    "e2s_compact_tokens": [ctypes.POINTER(CompactShape), _P, _P, _P, _P],
     "e2s_status_string": [ctypes.c_int],
     "e2s_abi_version": [],
 }
@@ -555,4 +563,36 @@ def prune_ragged(q, k, images, num_layers: int, num_heads: int, num_kv_heads: in
     prio = torch.empty(p.tokens, device=q.device, dtype=torch.float32) if want_prio else None
     idx = p(q, k, fused, prio)
     return idx[:p.kept], fused, prio
+
+
+# ---------------------------------------------------------------------------
+# token compaction (e2s_compact_tokens)
+# ---------------------------------------------------------------------------
+
+def compact_tokens(src, keep_idx, out=None):
+    """Gather the kept tokens' vectors: src [B, R, N, C] (any strides, channels
+    contiguous, e.g. a slice of a key/value cache), keep_idx [B, K] int32 ->
+    out [B, R, K, C] with out[b, r, j] = src[b, r, keep_idx[b, j]]."""
+    torch = _torch()
+    if not isinstance(src, torch.Tensor) or src.device.type != "cuda" or src.dim() != 4:
+        raise ValueError("src must be a 4-D GPU tensor [B, R, N, C]")
+    if src.stride(3) != 1:
+        raise ValueError("src's channels must be contiguous")
+    if src.dtype not in (torch.bfloat16, torch.float16, torch.float32):
+        raise TypeError("src must be bfloat16, float16 or float32")
+    _check(keep_idx, "keep_idx", dtype=torch.int32, ndim=2)
+    B, R, N, C = src.shape
+    if keep_idx.shape[0] != B:
+        raise ValueError("keep_idx must be [B, K]")
+    K = keep_idx.shape[1]
+    if out is None:
+        out = torch.empty((B, R, K, C), device=src.device, dtype=src.dtype)
+    if tuple(out.shape) != (B, R, K, C) or out.dtype != src.dtype or out.stride(3) != 1:
+        raise ValueError("out must be [B, R, K, C] of src's dtype with contiguous channels")
+    sh = CompactShape(B, R, N, K, C, src.element_size(),
+                      (ctypes.c_int64 * 3)(*src.stride()[:3]),
+                      (ctypes.c_int64 * 3)(*out.stride()[:3]))
+    _raise(_LIB.e2s_compact_tokens(ctypes.byref(sh), keep_idx.data_ptr(), src.data_ptr(),
+                                   out.data_ptr(), _stream(src.device)), "e2s_compact_tokens")
+    return out
 

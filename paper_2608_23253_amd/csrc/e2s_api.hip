@@ -360,4 +360,18 @@ e2s_status e2s_prune_ragged(const e2s_ragged_shape* shape, const e2s_params* par
                          static_cast<hipStream_t>(stream));
 }
 
+e2s_status e2s_compact_tokens(const e2s_compact_shape* shape, const int32_t* keep_idx,
+                              const void* src, void* dst, void* stream) {
+    E2S_TRY(e2s::check_compact(shape));
+    if (shape->keep == 0) return E2S_OK;
+    E2S_TRY(need(keep_idx));
+    E2S_TRY(need(src));
+    E2S_TRY(need(dst));
+    E2S_TRY(e2s::check_aligned(keep_idx, 4));
+    E2S_TRY(e2s::check_aligned(src, 16));
+    E2S_TRY(e2s::check_aligned(dst, 16));
+    return from_hip(e2s::launch_compact(*shape, keep_idx, src, dst,
+                                        static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -77,4 +77,8 @@ hipError_t launch_ds_select(const Dims& d, const SelectArgs& a, const float* rho
 hipError_t launch_attention_select(const Dims& d, const SelectArgs& a, const float* support_c,
                                    hipStream_t stream);
 
+// Token compaction (e2s_compact_tokens), arguments validated.
+hipError_t launch_compact(const e2s_compact_shape& s, const int32_t* keep, const void* src,
+                          void* dst, hipStream_t stream);
+
 }  // namespace e2s

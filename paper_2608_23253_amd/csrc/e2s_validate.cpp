@@ -135,6 +135,30 @@ e2s_status check_select_params(const e2s_params* p, const Dims& d) {
     return E2S_OK;
 }
 
+e2s_status check_compact(const e2s_compact_shape* s) {
+    if (s == nullptr) return E2S_ERR_NULL_POINTER;
+    if (s->batch < 1 || s->rows < 1 || s->num_tokens < 1 || s->keep < 0 || s->channels < 1)
+        return E2S_ERR_BAD_SHAPE;
+    if (s->elem_bytes != 2 && s->elem_bytes != 4) return E2S_ERR_BAD_PARAM;
+    if ((static_cast<int64_t>(s->channels) * s->elem_bytes) % 16 != 0) return E2S_ERR_MISALIGNED;
+    const double big = static_cast<double>(std::numeric_limits<int64_t>::max() / 16);
+    const double counts[3] = {static_cast<double>(s->batch), static_cast<double>(s->rows),
+                              static_cast<double>(s->num_tokens)};
+    const double dcounts[3] = {static_cast<double>(s->batch), static_cast<double>(s->rows),
+                               static_cast<double>(s->keep)};
+    double src_end = s->channels, dst_end = s->channels;
+    for (int i = 0; i < 3; ++i) {
+        if (s->src_stride[i] < 0 || s->dst_stride[i] < 0) return E2S_ERR_BAD_SHAPE;
+        if ((s->src_stride[i] * s->elem_bytes) % 16 != 0 ||
+            (s->dst_stride[i] * s->elem_bytes) % 16 != 0)
+            return E2S_ERR_MISALIGNED;
+        src_end += (counts[i] - 1) * static_cast<double>(s->src_stride[i]);
+        dst_end += (dcounts[i] - 1) * static_cast<double>(s->dst_stride[i]);
+    }
+    if (src_end * s->elem_bytes > big || dst_end * s->elem_bytes > big) return E2S_ERR_BAD_SHAPE;
+    return E2S_OK;
+}
+
 size_t support_region_bytes(const Dims& d) {
     return align_up(static_cast<size_t>(d.L * d.H * d.tokens) * sizeof(float), 256);
 }

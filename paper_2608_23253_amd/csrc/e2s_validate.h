@@ -36,6 +36,10 @@ e2s_status check_aligned(const void* ptr, size_t align);
 e2s_status check_ragged(const e2s_ragged_shape* s, const e2s_image* images, int elem_bytes,
                         Dims* out, int64_t* min_side);
 
+// Token compaction: counts, element size, 16-byte granularity of the vectors and
+// strides, and that the largest offset of each array fits 63 bits.
+e2s_status check_compact(const e2s_compact_shape* s);
+
 // Workspace of e2s_layer_reliability and e2s_prune: the supports e [B,L,H,N] f32
 // (used only when a layer's supports do not stay on chip), then rho and pbar_c
 // [B,L,N] f32 (e2s_prune), each region rounded up to 256 bytes.

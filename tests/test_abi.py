@@ -67,10 +67,10 @@ def stage(shape, params, ncand, q=A, k=A, pos=A, mprev=None, ws=A, ws_bytes=None
 
 def test_exports_every_declared_entry_point():
     names = L.header_entry_points()
-    assert len(names) == 15
+    assert len(names) == 16
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.e2s_abi_version() == 4
+    assert lib.e2s_abi_version() == 5
 
 
 def test_status_strings():
@@ -291,4 +291,29 @@ def test_ragged_rejects_invalid_records():
     zero = ragged_images([(6, 7, 5, 0), (4, 9, 1, 0)])
     assert ragged(zero, shape=L.RaggedShape(2, 3, 4, 2, 64), out=None, ws_bytes=1) == \
         L.ERR_WORKSPACE_TOO_SMALL
+
+
+# ---------------------------------------------------------------------------
+# token compaction
+# ---------------------------------------------------------------------------
+
+def compact(B=2, R=3, N=10, K=4, C=64, eb=2, ss=None, ds=None, keep=A, src=A, dst=A * 2):
+    ss = (R * N * C, N * C, C) if ss is None else ss
+    ds = (R * K * C, K * C, C) if ds is None else ds
+    sh = L.CompactShape(B, R, N, K, C, eb, (ctypes.c_int64 * 3)(*ss), (ctypes.c_int64 * 3)(*ds))
+    return lib.e2s_compact_tokens(ctypes.byref(sh), keep, src, dst, None)
+
+
+def test_compact_rejects_invalid_calls():
+    assert lib.e2s_compact_tokens(None, A, A, A, None) == L.ERR_NULL_POINTER
+    assert compact(B=0) == L.ERR_BAD_SHAPE
+    assert compact(K=-1) == L.ERR_BAD_SHAPE
+    assert compact(eb=8) == L.ERR_BAD_PARAM
+    assert compact(C=12) == L.ERR_MISALIGNED                   # 24 bytes per vector
+    assert compact(ss=(640, 64, 4)) == L.ERR_MISALIGNED         # token stride 8 bytes
+    assert compact(ds=(-1, 64, 64)) == L.ERR_BAD_SHAPE
+    assert compact(keep=None) == L.ERR_NULL_POINTER
+    assert compact(src=A + 8) == L.ERR_MISALIGNED
+    assert compact(dst=None) == L.ERR_NULL_POINTER
+    assert compact(K=0, keep=None, src=None, dst=None) == L.OK   # nothing to move
 

@@ -467,3 +467,19 @@ def test_keep_zero_and_keep_all():
     assert kept.size == 0
     kept, _, _ = O.spatial_select(q, 6, 6, 2, 0.1, 36)
     assert kept.tolist() == list(range(36))
+
+
+def test_compact_tokens_gather():
+    """Token compaction: a hand-worked case, the identity, and composition of two
+    compactions (keeping b of the survivors of a keeps a[b])."""
+    x = np.arange(2 * 5 * 3, dtype=np.float64).reshape(2, 5, 3)   # [R, N, C]
+    got = O.compact_tokens(x, [4, 0, 2])
+    want = [[[12, 13, 14], [0, 1, 2], [6, 7, 8]], [[27, 28, 29], [15, 16, 17], [21, 22, 23]]]
+    assert got.tolist() == want
+    assert np.array_equal(O.compact_tokens(x, np.arange(5)), x)
+    rng = np.random.default_rng(3)
+    y = rng.standard_normal((3, 4, 40, 8))
+    a = np.sort(rng.choice(40, 17, replace=False))
+    b = np.sort(rng.choice(17, 6, replace=False))
+    assert np.array_equal(O.compact_tokens(O.compact_tokens(y, a), b), O.compact_tokens(y, a[b]))
+    assert O.compact_tokens(y, []).shape == (3, 4, 0, 8)

@@ -35,8 +35,8 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "layer_evidence_llava_traffic.txt")
 # the sources of the score and reliability stage: a counter summary taken on other
 # versions of them is not used
-STAGE_SOURCES = ("layer.hip", "score.hip", "score_prob.hip", "score_common.h", "fuse.hip",
-                 "e2s_device.h")
+STAGE_SOURCES = ("layer.hip", "score.hip", "score_prob.hip", "score_common.h",
+                 "score_prob_common.h", "batch_geom.h", "fuse.hip", "e2s_device.h")
 
 
 def log(*a):

@@ -35,16 +35,20 @@ struct ImageGeom {
 __device__ __forceinline__ ImageGeom image_geom(const BatchGeom& g, int64_t b) {
     ImageGeom r;
     if (g.images != nullptr) {
-        const e2s_image im = g.images[b];
-        r.q_off = im.q_offset;
-        r.k_off = im.k_offset;
-        r.tok = im.token_offset;
-        r.keep_off = im.keep_offset;
-        r.NT = im.num_text;
-        r.gh = im.grid_h;
-        r.gw = im.grid_w;
-        r.N = im.grid_h * im.grid_w;
-        r.K = im.keep;
+        // the table is read-only for the whole launch and b is uniform over the
+        // workgroup: read it through the constant address space (scalar loads,
+        // which do not occupy the vector memory counter the kernels wait on)
+        typedef const __attribute__((address_space(4))) e2s_image ConstImage;
+        ConstImage* im = (ConstImage*)g.images + b;
+        r.q_off = im->q_offset;
+        r.k_off = im->k_offset;
+        r.tok = im->token_offset;
+        r.keep_off = im->keep_offset;
+        r.NT = im->num_text;
+        r.gh = im->grid_h;
+        r.gw = im->grid_w;
+        r.N = r.gh * r.gw;
+        r.K = im->keep;
     } else {
         r.NT = g.NT;
         r.N = g.N;

@@ -31,8 +31,9 @@
 // logit of a query chunk lies further out (peaked attention), the chunk's
 // statistics are recomputed online with the running maximum as reference
 // (m_t = max_n z s, rescaled as it grows; S_t and E_t relative to it) and pass 2
-// uses the library's expm1f wherever a batch of 16 logits leaves the series'
-// range.
+// uses the library's expm1f wherever a 16 x 16 tile of logits leaves the series'
+// range.  The tile is the unit of every such decision (score_prob_common.h), so
+// the results do not depend on how many tiles a wave takes at once.
 // The query-block loops are not unrolled (the per-lane statistics live in LDS),
 // which keeps the kernel's code within the instruction cache.
 //
@@ -42,50 +43,21 @@
 // the shared keys from that XCD's L2.
 #include <type_traits>
 
-#include "e2s_device.h"
 #include "e2s_kernels.h"
+#include "score_prob_common.h"
 
 namespace e2s {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4v __attribute__((ext_vector_type(4)));
-
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / kWave;
+using prob::kThreads;
+using prob::kWaves;
+using prob::ScaledSeries;
+using prob::tile_mma;
 
 __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
     const int q = nblocks / 8, r = nblocks % 8;
     const int x = bid % 8, i = bid / 8;
     return x * q + min(x, r) + i;
-}
-
-// expm1 on [-1/8, 1/8]: Taylor series to degree 5 (truncation below 6e-9, i.e.
-// under one float32 ulp of the result, there).
-constexpr float kSeriesRange = 0.125f;
-__device__ __forceinline__ float expm1_series(float x) {
-    float p = 1.0f / 120.0f;
-    p = fmaf(p, x, 1.0f / 24.0f);
-    p = fmaf(p, x, 1.0f / 6.0f);
-    p = fmaf(p, x, 0.5f);
-    p = fmaf(p, x, 1.0f);
-    return p * x;
-}
-// expm1(x) = x * series_p5(x) on |x| <= 1/8 (degree 5) and x * series_p6(x) on
-// |x| <= 1/4 (degree 6: truncation x^7 / 5040, below 6e-8 relative there); the
-// callers fold the last product into their running sums.
-__device__ __forceinline__ float series_p5(float x) {
-    float p = fmaf(1.0f / 120.0f, x, 1.0f / 24.0f);
-    p = fmaf(p, x, 1.0f / 6.0f);
-    p = fmaf(p, x, 0.5f);
-    return fmaf(p, x, 1.0f);
-}
-__device__ __forceinline__ float series_p6(float x) {
-    float p = fmaf(1.0f / 720.0f, x, 1.0f / 120.0f);
-    p = fmaf(p, x, 1.0f / 24.0f);
-    p = fmaf(p, x, 1.0f / 6.0f);
-    p = fmaf(p, x, 0.5f);
-    return fmaf(p, x, 1.0f);
 }
 
 template <typename T, int D> struct ProbCfg;
@@ -152,45 +124,6 @@ __device__ __forceinline__ void load_queries(float (&b)[D / 4], const float* qs,
     }
 }
 
-// 16 keys x 16 queries: lane (lr, lg) gets the logits of keys 4 lg + r (r = 0..3)
-// against query lr of the block.
-template <int NA>
-__device__ __forceinline__ f32x4v tile_mma(const bf16x8 (&a)[NA], const bf16x8 (&b)[NA]) {
-    f32x4v acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < NA; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s], b[s], acc, 0, 0, 0);
-    return acc;
-}
-template <int NA>
-__device__ __forceinline__ f32x4v tile_mma(const float (&a)[NA], const float (&b)[NA]) {
-    f32x4v acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < NA; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s], acc, 0, 0, 0);
-    return acc;
-}
-// expm1(s y) = s y P(y) with P the series of the scaled argument: coefficients
-// s^k / (k+1)! for k = 1 .. DEG-1 (DEG = 5 or 6), so the scale is applied once per
-// sum instead of once per logit.
-template <int DEG>
-struct ScaledSeries {
-    float c[DEG - 1];
-    __device__ explicit ScaledSeries(float s) {
-        float pk = 1.0f, f = 1.0f;
-#pragma unroll
-        for (int kk = 1; kk < DEG; ++kk) {
-            pk *= s;
-            f *= static_cast<float>(kk + 1);
-            c[kk - 1] = pk / f;
-        }
-    }
-    __device__ __forceinline__ float operator()(float y) const {
-        float p = c[DEG - 2];
-#pragma unroll
-        for (int kk = DEG - 3; kk >= 0; --kk) p = fmaf(p, y, c[kk]);
-        return fmaf(p, y, 1.0f);
-    }
-};
-
 // TG key tiles per group, two groups in flight per wave: 4 tiles (2 workgroups per
 // CU by registers) when a chunk has 8 query blocks, else 2 (3 per CU).
 template <typename T, int D, int TG>
@@ -248,8 +181,6 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
             load_keys<NA>(a[tt], kg + static_cast<int64_t>(min(key, N - 1)) * D + koff);
         }
     };
-    // no key of group j lies past N
-    auto group_full = [&](int j) { return (tile_of(j, TG - 1) + 1) * 16 <= N; };
 
     // body(a, j) for every group j of this wave, the next group's keys requested
     // before the current one is used.  The requests are unconditional (past the
@@ -288,21 +219,16 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
         if (tid == 0) s_far = 0;
         __syncthreads();
 
-        // ---- reference of each query: mean logit Q_t.K_n of keys 0..15 ----------
-        // (pairwise, so that equal logits give exactly their value; the logit of
-        // key 0 when N < 16; zero query rows past N_T get 0); c_t = s times it
+        // ---- reference of each query (block_reference); zero query rows past
+        // N_T get 0
         {
             AFrag a0[NA];
             load_keys<NA>(a0, kg + static_cast<int64_t>(min(lr, N - 1)) * D + koff);
             for (int qb = wave; qb < QB; qb += kWaves) {
                 AFrag bq[NA];
                 load_queries<D>(bq, qs, qb * 16, lr, lg);
-                const f32x4v z = tile_mma<NA>(a0, bq);
-                float sum = (z[0] + z[1]) + (z[2] + z[3]);
-                sum += __shfl_xor(sum, 16);
-                sum += __shfl_xor(sum, 32);
-                const float z0 = __shfl(z[0], lr);              // key 0, from lane (lr, 0)
-                if (lg == 0) st_c[qb * 16 + lr] = (N >= 16) ? sum * (1.0f / 16.0f) : z0;
+                const float c = prob::block_reference(tile_mma<NA>(a0, bq), N, lr);
+                if (lg == 0) st_c[qb * 16 + lr] = c;
             }
         }
         __syncthreads();
@@ -313,29 +239,15 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
         const ScaledSeries<6> p6(scale);
         float amax = 0.f;                                         // largest |y| seen
         stream_groups([&](const AFrag (&a)[TG][NA], int j) {
-            const bool full = group_full(j);
             for (int qb = 0; qb < QB; ++qb) {
                 AFrag bq[NA];
                 load_queries<D>(bq, qs, qb * 16, lr, lg);
                 const float cz = st_c[qb * 16 + lr];
-                float y[TG * 4];
-#pragma unroll
-                for (int tt = 0; tt < TG; ++tt) {
-                    const f32x4v zt = tile_mma<NA>(a[tt], bq);
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) y[tt * 4 + r] = zt[r] - cz;
-                }
-                if (!full) {
-#pragma unroll
-                    for (int i = 0; i < TG * 4; ++i)
-                        y[i] = (tile_of(j, i / 4) * 16 + 4 * lg + i % 4 < N) ? y[i] : 0.f;
-                }
                 float E = lE[qb * kThreads];
 #pragma unroll
-                for (int i = 0; i < TG * 4; ++i) {
-                    amax = fmaxf(amax, fabsf(y[i]));
-                    E = fmaf(p5(y[i]), y[i], E);
-                }
+                for (int tt = 0; tt < TG; ++tt)
+                    prob::series_tile(tile_mma<NA>(a[tt], bq), cz, tile_of(j, tt) * 16 + 4 * lg,
+                                      N, p5, E, amax);
                 lE[qb * kThreads] = E;
             }
         });
@@ -356,12 +268,11 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
             if (tid < QB * 16) {
                 float e = 0.f;
                 for (int w = 0; w < kWaves; ++w) e += wpart[(w * qcap + tid) * 4];
-                // E = s e; S = N + E >= N exp(-1/8) > N / 2, so L = log1p(E / N)
-                // (as log_mean_exp); the shift of pass 2 in logit units: c_t / s + L / s
-                st_m[tid] = (tid < rows) ? st_c[tid] + log1pf((scale * e) / fN) / scale : 0.f;
+                st_m[tid] = (tid < rows) ? prob::near_shift(st_c[tid], e, scale, fN) : 0.f;
             }
         } else {
-            // ---- pass 1 again, online: running maximum as the reference ----------
+            // ---- pass 1 again, online, tile by tile: running maximum as the
+            // reference
             for (int qb = 0; qb < QB; ++qb) {
                 lm[qb * kThreads] = -INFINITY;
                 lE[qb * kThreads] = 0.f;
@@ -371,115 +282,40 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
             for (int j = 0; j < ngw; ++j) {
                 AFrag a[TG][NA];
                 load_group(a, j);
-                bool kval[TG][4];
-#pragma unroll
-                for (int tt = 0; tt < TG; ++tt)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) kval[tt][r] = tile_of(j, tt) * 16 + 4 * lg + r < N;
-                const bool full = group_full(j);
-                float cntg = 0.f;                                 // valid keys of this lane here
-#pragma unroll
-                for (int tt = 0; tt < TG; ++tt)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) cntg += kval[tt][r] ? 1.f : 0.f;
                 for (int qb = 0; qb < QB; ++qb) {
                     AFrag bq[NA];
                     load_queries<D>(bq, qs, qb * 16, lr, lg);
-                    float z[TG * 4];
+                    float m = lm[qb * kThreads], E = lE[qb * kThreads], S = lS[qb * kThreads];
+                    float c = cnt;
 #pragma unroll
                     for (int tt = 0; tt < TG; ++tt) {
-                        const f32x4v zt = tile_mma<NA>(a[tt], bq);
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) z[tt * 4 + r] = zt[r];
-                    }
-                    float zmax = -INFINITY, zmin = INFINITY;
-#pragma unroll
-                    for (int i = 0; i < TG * 4; ++i) {
-                        const bool ok = full || kval[i / 4][i % 4];
-                        zmax = fmaxf(zmax, ok ? z[i] : -INFINITY);
-                        zmin = fminf(zmin, ok ? z[i] : INFINITY);
-                    }
-                    float m = lm[qb * kThreads], E = lE[qb * kThreads], S = lS[qb * kThreads];
-                    const float mx = fmaxf(m, zmax * scale);      // scale > 0
-                    if (__any(mx > m)) {
-                        // rescale the sums to the new maximum (exact no-op where unchanged)
-                        const float dm = (mx > m) ? m - mx : 0.f;
-                        const float sc = expf(dm);
-                        const float em = (cnt > 0.f) ? expm1f(dm) : 0.f;
-                        E = fmaf(cnt, em, E * sc);
-                        S = S * sc;
-                        m = mx;
-                    }
-                    // every x = z * scale - mx lies in [zmin * scale - mx, 0]
-                    const bool near = cntg == 0.f || fmaf(zmin, scale, -mx) >= -kSeriesRange;
-                    if (__all(near)) {
-                        float el = 0.f;
-#pragma unroll
-                        for (int i = 0; i < TG * 4; ++i) {
-                            const float t = expm1_series(fmaf(z[i], scale, -mx));
-                            el += (full || kval[i / 4][i % 4]) ? t : 0.f;
-                        }
-                        E += el;
-                        S += cntg + el;
-                    } else {
-#pragma unroll
-                        for (int i = 0; i < TG * 4; ++i) {
-                            if (full || kval[i / 4][i % 4]) {
-                                const float x = fmaf(z[i], scale, -mx);
-                                const float t = expm1f(x);
-                                E += t;
-                                S += (x < -0.5f) ? expf(x) : 1.0f + t;
-                            }
-                        }
+                        const int key0 = tile_of(j, tt) * 16 + 4 * lg;
+                        prob::online_tile(tile_mma<NA>(a[tt], bq), scale, key0, N, c, m, E, S);
+                        c += prob::tile_count(key0, N);
                     }
                     lm[qb * kThreads] = m;
                     lE[qb * kThreads] = E;
                     lS[qb * kThreads] = S;
                 }
-                cnt += cntg;
+#pragma unroll
+                for (int tt = 0; tt < TG; ++tt) cnt += prob::tile_count(tile_of(j, tt) * 16 + 4 * lg, N);
             }
 
             // ---- merge statistics: the 4 lane groups of a wave, then the waves ----
             for (int qb = 0; qb < QB; ++qb) {
-                const float m = lm[qb * kThreads];
-                float M = fmaxf(m, __shfl_xor(m, 16));
-                M = fmaxf(M, __shfl_xor(M, 32));
-                float e = 0.f, s = 0.f;
-                if (cnt > 0.f) {
-                    const float dm = m - M;
-                    e = fmaf(cnt, expm1f(dm), lE[qb * kThreads] * expf(dm));
-                    s = lS[qb * kThreads] * expf(dm);
-                }
-                float c = cnt;
-                e += __shfl_xor(e, 16);
-                s += __shfl_xor(s, 16);
-                c += __shfl_xor(c, 16);
-                e += __shfl_xor(e, 32);
-                s += __shfl_xor(s, 32);
-                c += __shfl_xor(c, 32);
+                const prob::OnlinePart pt =
+                    prob::online_wave_part(lm[qb * kThreads], lE[qb * kThreads], lS[qb * kThreads], cnt);
                 if (lg == 0) {
                     float* wp = wpart + (wave * qcap + qb * 16 + lr) * 4;
-                    wp[0] = (c > 0.f) ? M : -INFINITY;
-                    wp[1] = e;
-                    wp[2] = s;
-                    wp[3] = c;
+                    wp[0] = pt.M;
+                    wp[1] = pt.e;
+                    wp[2] = pt.s;
+                    wp[3] = pt.c;
                 }
             }
             __syncthreads();
-            if (tid < QB * 16) {
-                float M = -INFINITY;
-                for (int w = 0; w < kWaves; ++w) M = fmaxf(M, wpart[(w * qcap + tid) * 4]);
-                float e = 0.f, s = 0.f;
-                for (int w = 0; w < kWaves; ++w) {
-                    const float* p = wpart + (w * qcap + tid) * 4;
-                    if (p[0] == -INFINITY) continue;     // this wave saw no key
-                    const float dm = p[0] - M;
-                    e += fmaf(p[3], expm1f(dm), p[1] * expf(dm));
-                    s += p[2] * expf(dm);
-                }
-                // one shift per query: z * scale - (m + L) is the centred logit
-                st_m[tid] = (tid < rows) ? M + log_mean_exp(e, s, fN) : 0.f;
-            }
+            if (tid < QB * 16)
+                st_m[tid] = (tid < rows) ? prob::online_shift(wpart + tid * 4, qcap * 4, fN) : 0.f;
         }
         __syncthreads();
 
@@ -497,57 +333,39 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
             // y = z - shift; |s y| <= 1/4: the degree-6 series; the column sums are
             // in units of s
             stream_groups([&](const AFrag (&a)[TG][NA], int j) {
-                float col[TG * 4];
+                float col[TG][4];
 #pragma unroll
-                for (int i = 0; i < TG * 4; ++i) col[i] = 0.f;
+                for (int tt = 0; tt < TG; ++tt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) col[tt][r] = 0.f;
                 for (int qb = 0; qb < QB; ++qb) {
                     AFrag bq[NA];
                     load_queries<D>(bq, qs, qb * 16, lr, lg);
                     const float sz = st_m[qb * 16 + lr];
 #pragma unroll
-                    for (int tt = 0; tt < TG; ++tt) {
-                        const f32x4v zt = tile_mma<NA>(a[tt], bq);
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            const float y = zt[r] - sz;
-                            col[tt * 4 + r] = fmaf(p6(y), y, col[tt * 4 + r]);
-                        }
-                    }
+                    for (int tt = 0; tt < TG; ++tt)
+                        prob::column_series_tile(tile_mma<NA>(a[tt], bq), sz, p6, col[tt]);
                 }
-                add_columns(col, j, scale);
+                add_columns(reinterpret_cast<const float(&)[TG * 4]>(col), j, scale);
             });
         } else {
             for (int j = 0; j < ngw; ++j) {
                 AFrag a[TG][NA];
                 load_group(a, j);
-                float col[TG * 4];
+                float col[TG][4];
 #pragma unroll
-                for (int i = 0; i < TG * 4; ++i) col[i] = 0.f;
+                for (int tt = 0; tt < TG; ++tt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) col[tt][r] = 0.f;
                 for (int qb = 0; qb < QB; ++qb) {
                     AFrag bq[NA];
                     load_queries<D>(bq, qs, qb * 16, lr, lg);
                     const float shift = st_m[qb * 16 + lr];
-                    float x[TG * 4];
-                    float xmin = INFINITY, xmax = -INFINITY;
 #pragma unroll
-                    for (int tt = 0; tt < TG; ++tt) {
-                        const f32x4v z = tile_mma<NA>(a[tt], bq);
-#pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            x[tt * 4 + r] = fmaf(z[r], scale, -shift);
-                            xmin = fminf(xmin, x[tt * 4 + r]);
-                            xmax = fmaxf(xmax, x[tt * 4 + r]);
-                        }
-                    }
-                    if (__all(fmaxf(-xmin, xmax) <= kSeriesRange)) {
-#pragma unroll
-                        for (int i = 0; i < TG * 4; ++i) col[i] += expm1_series(x[i]);
-                    } else {
-#pragma unroll
-                        for (int i = 0; i < TG * 4; ++i) col[i] += expm1f(x[i]);
-                    }
+                    for (int tt = 0; tt < TG; ++tt)
+                        prob::column_far_tile(tile_mma<NA>(a[tt], bq), scale, shift, col[tt]);
                 }
-                add_columns(col, j, 1.0f);
+                add_columns(reinterpret_cast<const float(&)[TG * 4]>(col), j, 1.0f);
             }
         }
     }

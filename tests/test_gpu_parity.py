@@ -66,6 +66,11 @@ CASES = [
                               num_kv_heads=8, head_dim=128, num_text=16, grid_h=12, grid_w=12,
                               keep=24, salient_count=8, clusters=2)),
     synth.heavy_tailed(synth.config_by_name("llava").replace(batch=1), name="heavy_llava"),
+    # peaked attention with d = 128 and 100 queries: the mean-of-probabilities
+    # kernel's online statistics with a query chunk of 112 rows
+    synth.heavy_tailed(_small("heavy_text100_d128", config_id=63, num_layers=2, num_heads=4,
+                              num_kv_heads=4, head_dim=128, num_text=100, grid_h=12,
+                              grid_w=12, keep=24, salient_count=8), name="heavy_text100"),
     _small("max_grid_16384", config_id=56, batch=1, num_layers=1, num_heads=2, num_kv_heads=1,
            num_text=2, grid_h=128, grid_w=128, keep=1000, salient_count=40, clusters=4),
     # batch x layers >= the CU count: e2s_prune / e2s_layer_reliability take the

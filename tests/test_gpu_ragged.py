@@ -7,10 +7,11 @@ oracle under the same rule as the uniform path (fused masses within 1e-4 absolut
 kept sets exact or differing only inside the 1e-5 tie window).
 
 Cases mix grids (ragged tails, a 2x3 grid at G = 2), text lengths (1 to 150, so the
-mean-of-probabilities kernel takes one or two query chunks), budgets (0 to N_b), one
-query head per key head and grouped-query heads (groups of 7 and 16), bf16 and fp32
-storage, d = 64 and 128, packed and gapped layouts, and a batch large enough that
-every (image, layer) gets its own workgroup on the on-chip layer path.
+mean-of-probabilities kernel takes one or two query chunks, 2 or 4 key tiles at a
+time), budgets (0 to N_b), one query head per key head and grouped-query heads
+(groups of 4, 7 and 16), bf16 and fp32 storage, d = 64 and 128, near-uniform and
+peaked attention, packed and gapped layouts, and a batch large enough that every
+(image, layer) gets its own workgroup on the on-chip layer path.
 """
 import ctypes
 
@@ -54,6 +55,14 @@ CASES = {
     "mha_f32_d128": (_base("mha_f32_d128", config_id=75, dtype="f32", num_heads=3,
                            num_kv_heads=3, head_dim=128),
                      [(6, 7, 4, 10), (9, 9, 17, 20)], 3),
+    # peaked attention (the online statistics of the mean-of-probabilities kernel);
+    # N_T = 100 gives the batch query chunks of 112 rows, the images alone smaller
+    # ones
+    "heavy_mixed_bf16_d128": (_base("heavy_mixed_bf16_d128", config_id=78, num_heads=4,
+                                    num_kv_heads=4, head_dim=128, value_std=2.0,
+                                    shift_sigmas=4.0, salient_count=6),
+                              [(12, 12, 16, 24), (24, 24, 64, 100), (9, 11, 100, 20),
+                               (5, 7, 3, 0), (3, 5, 1, 4)], 3),
 }
 
 
@@ -241,3 +250,45 @@ def test_ragged_validation_on_device_pointers():
         E.prune_ragged(q, k, bad, L, H, Hkv, D, cells)
     with pytest.raises(E.E2SError):                           # G above the 6x6 image's side
         E.prune_ragged(q, k, arr, L, H, Hkv, D, 7)
+
+
+@pytest.mark.parametrize("heavy", [False, True], ids=["near_uniform", "peaked"])
+def test_mean_prob_group_size_does_not_change_bits(heavy):
+    """The mean-of-probabilities kernel takes 2 key tiles at a time when a query chunk
+    holds at most 112 queries and 4 when it holds 128; an image's bits must not
+    depend on which.  40 images with N_T <= 64 alone run with 2; one more image with
+    N_T = 130 (two query chunks) makes the same images run with 4."""
+    extra = dict(value_std=2.0, shift_sigmas=4.0) if heavy else {}
+    cfg = _base("mp_group_size", config_id=79 + int(heavy), num_layers=2, num_heads=8,
+                num_kv_heads=2, head_dim=128, salient_count=5, **extra)
+    rng = np.random.default_rng(79)
+    dims = [(int(rng.integers(2, 25)), int(rng.integers(2, 25)), int(rng.integers(1, 65)), 0)
+            for _ in range(40)]
+    dims = [(gh, gw, nt, int(rng.integers(0, gh * gw + 1))) for gh, gw, nt, _ in dims]
+    dims[0] = (24, 24, 64, 100)
+    log(f"[case] mean_prob group size heavy={heavy}")
+    imgs, arr_a, keep_a, fused_a, prio_a = _run(cfg, dims, 2, "mean_prob")
+    _, arr_b, keep_b, fused_b, prio_b = _run(cfg, dims + [(6, 6, 130, 5)], 2, "mean_prob")
+    keep_a, fused_a, prio_a = keep_a.cpu().numpy(), fused_a.cpu().numpy(), prio_a.cpu().numpy()
+    keep_b, fused_b, prio_b = keep_b.cpu().numpy(), fused_b.cpu().numpy(), prio_b.cpu().numpy()
+    for b, (gh, gw, nt, K) in enumerate(dims):
+        a, c = arr_a[b], arr_b[b]
+        n = gh * gw
+        np.testing.assert_array_equal(fused_a[a.token_offset:a.token_offset + n],
+                                      fused_b[c.token_offset:c.token_offset + n])
+        np.testing.assert_array_equal(prio_a[a.token_offset:a.token_offset + n],
+                                      prio_b[c.token_offset:c.token_offset + n])
+        assert keep_a[a.keep_offset:a.keep_offset + K].tolist() == \
+            keep_b[c.keep_offset:c.keep_offset + K].tolist()
+    for b in (0, 17, 33):
+        gh, gw, nt, K = dims[b]
+        qb, kb = imgs[b]
+        a = arr_a[b]
+        ref = O.prune_image(qb, kb, gh, gw, K, 2, 0.1, "mean_prob")
+        got = fused_a[a.token_offset:a.token_offset + gh * gw].astype(np.float64)
+        err = np.abs(got - ref.fused)
+        assert (err <= 1e-4 + 2e-3 * np.abs(ref.fused)).all(), f"image {b}: fused masses"
+        cmp = compare_sets(keep_a[a.keep_offset:a.keep_offset + K], ref)
+        log(f"  image {b} {gh}x{gw} N_T={nt} K={K}: set {cmp.verdict} "
+            f"max|d fused|={err.max():.2e}")
+        assert cmp.verdict != "fail"

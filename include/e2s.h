@@ -81,7 +81,7 @@ typedef struct {
     int32_t head_dim;      /* d: 64 or 128                             */
     int32_t num_text;      /* N_T >= 1                                 */
     int32_t grid_h;        /* visual grid rows >= 1                    */
-    int32_t grid_w;        /* visual grid cols >= 1; N = grid_h*grid_w <= 16384 */
+    int32_t grid_w;        /* visual grid cols >= 1; N = grid_h*grid_w <= 2^20  */
 } e2s_shape;
 
 /* The full method and the ablation variants of the paper's ablation study (Sec. 5,
@@ -108,7 +108,8 @@ typedef struct {
     int32_t dtype;   /* e2s_dtype of q and k                                     */
     int32_t mode;    /* e2s_score_mode                                           */
     float scale;     /* logit scale of Eq. 1; 0 selects 1/sqrt(head_dim)         */
-    int32_t cells;   /* G: cells per side, 1 <= G <= min(grid_h, grid_w) (paper: 4) */
+    int32_t cells;   /* G: cells per side, 1 <= G <= min(grid_h, grid_w, 128) (paper: 4);
+                        above 128: E2S_ERR_UNSUPPORTED */
     float lambda;    /* novelty weight of Eq. 22, finite, in [0, 1] (paper: 0.1) */
     int32_t keep;    /* K of Eq. 23, 0 <= K <= N                                 */
     int32_t variant; /* an e2s_variant; 0 is the full method                       */
@@ -249,7 +250,7 @@ E2S_API e2s_status e2s_prune_stage(const e2s_shape* shape, const e2s_params* par
  * of 8 elements for bf16, 4 for f32). */
 typedef struct {
     int32_t grid_h;        /* image b's grid rows >= 1                             */
-    int32_t grid_w;        /* grid cols >= 1; N_b = grid_h * grid_w <= 16384       */
+    int32_t grid_w;        /* grid cols >= 1; N_b = grid_h * grid_w <= 2^20        */
     int32_t num_text;      /* N_T,b >= 1 text queries                              */
     int32_t keep;          /* K_b, 0 <= K_b <= N_b                                 */
     int64_t q_offset;      /* q + q_offset: the image's Q block [L, H, N_T,b, d]   */

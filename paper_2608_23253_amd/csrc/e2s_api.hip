@@ -344,6 +344,7 @@ e2s_status e2s_prune_ragged(const e2s_ragged_shape* shape, const e2s_params* par
     if (workspace_bytes < e2s::prune_workspace_bytes(d)) return E2S_ERR_WORKSPACE_TOO_SMALL;
     // selection parameters: cells within every image's grid; keep is per image
     if (params->cells < 1 || params->cells > min_side) return E2S_ERR_BAD_PARAM;
+    if (params->cells > e2s::kMaxCells) return E2S_ERR_UNSUPPORTED;
     if (!std::isfinite(params->lambda) || params->lambda < 0.0f || params->lambda > 1.0f)
         return E2S_ERR_BAD_PARAM;
     if (params->variant < E2S_VARIANT_FULL || params->variant > E2S_VARIANT_NO_SPATIAL_NOVELTY)

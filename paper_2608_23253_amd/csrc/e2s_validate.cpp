@@ -127,6 +127,7 @@ e2s_status check_score_params(const e2s_params* p) {
 e2s_status check_select_params(const e2s_params* p, const Dims& d) {
     if (p == nullptr) return E2S_ERR_NULL_POINTER;
     if (p->cells < 1 || p->cells > d.gh || p->cells > d.gw) return E2S_ERR_BAD_PARAM;
+    if (p->cells > kMaxCells) return E2S_ERR_UNSUPPORTED;
     if (!std::isfinite(p->lambda) || p->lambda < 0.0f || p->lambda > 1.0f)
         return E2S_ERR_BAD_PARAM;
     if (p->keep < 0 || p->keep > d.N) return E2S_ERR_BAD_PARAM;

@@ -21,7 +21,13 @@ struct Dims {
     int64_t tokens = 0;
 };
 
-constexpr int64_t kMaxVisual = 16384;  // one image's scores fit in a workgroup's LDS
+// Visual tokens per image.  Up to 16384 the per-image kernels keep an image's
+// values on chip; beyond, they stream it (logits and column sums in the output
+// rows, the selection in segments of 16384 tokens).
+constexpr int64_t kMaxVisual = 1 << 20;
+// Cells per side of the spatial grid: the selection keeps one 64-bit word per cell
+// in LDS (128 KiB at G = 128).
+constexpr int64_t kMaxCells = 128;
 constexpr int64_t kMaxHeads = 128;     // per-token head supports held in registers
 
 e2s_status check_shape(const e2s_shape* s, Dims* out);

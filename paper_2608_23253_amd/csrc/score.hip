@@ -61,7 +61,7 @@ constexpr int kLdsBudget = 96 * 1024;         // bytes of dynamic LDS per workgr
 //      head of the chunk (row_logit), written to LDS;
 //   3. wave j runs head j's softmax and supports (wave_softmax).
 // Per head the arithmetic is that of the one-head-per-key-head kernels.
-template <typename T, int D, int HC>
+template <typename T, int D, int HC, bool GLOBAL>
 __global__ __launch_bounds__(kGroupKernelThreads) void score_group_kernel(
     const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
     float* __restrict__ r_out, BatchGeom bg, int group, int hchunk, int nchunks, float scale) {
@@ -78,16 +78,17 @@ __global__ __launch_bounds__(kGroupKernelThreads) void score_group_kernel(
     const int H = bg.H, NT = ig.NT, N = ig.N;
     const float qscale = mean_query_scale(scale, NT);
     extern __shared__ float smem[];
-    float* qbar = smem;                   // [hchunk][D]
-    float* a = smem + hchunk * D;         // [hchunk][N]
-
     const int h0 = g * group + ci * hchunk;
     const int nh = min(hchunk, group - ci * hchunk);
+    const int64_t erow = bg.L * bg.H * ig.tok + static_cast<int64_t>(l) * H * N;
+    float* qbar = smem;                   // [hchunk][D]
+    // [hchunk][N] logits: LDS, or (GLOBAL) the chunk's output rows, overwritten
+    float* a = GLOBAL ? e_out + erow + static_cast<int64_t>(h0) * N : smem + hchunk * D;
+
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int wrow = lane / G::LPR, wl = lane % G::LPR;
     const T* kg = k + ig.k_off + static_cast<int64_t>(lkv) * N * D + wl * 8;
     const T* ql = q + ig.q_off + static_cast<int64_t>(l) * H * NT * D;
-    const int64_t erow = bg.L * bg.H * ig.tok + static_cast<int64_t>(l) * H * N;
 
     Packet<T> ka[KU], kb[KU];
     load_key_batch<T, D>(ka, kg, wave * BATCH, wrow, N);
@@ -117,7 +118,7 @@ __global__ __launch_bounds__(kGroupKernelThreads) void score_group_kernel(
             for (int j = 0; j < HC; ++j) {
                 if (j < nh) {
                     const float sj = row_logit<G::LPR>(qb[j], x);
-                    if (wl == 0 && n < N) a[j * N + n] = sj;
+                    if (wl == 0 && n < N) a[static_cast<int64_t>(j) * N + n] = sj;
                 }
             }
         }
@@ -130,11 +131,14 @@ __global__ __launch_bounds__(kGroupKernelThreads) void score_group_kernel(
         if (base + 2 * STRIDE < N) load_key_batch<T, D>(ka, kg, base + 2 * STRIDE, wrow, N);
         consume(kb, base + STRIDE);
     }
+    if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
+    if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
     for (int j = wave; j < nh; j += NW) {
         const int64_t row = erow + static_cast<int64_t>(h0 + j) * N;
-        wave_softmax_store(a + j * N, N, lane, e_out + row, r_out ? r_out + row : nullptr);
+        wave_softmax_store(a + static_cast<int64_t>(j) * N, N, lane, e_out + row,
+                           r_out ? r_out + row : nullptr);
     }
 }
 
@@ -181,7 +185,7 @@ __device__ __forceinline__ void split_bf16x3(float x, uint16_t& hi, uint16_t& mi
 // 32 s + 8 lg .. + 7 of step s in both operands, so one wave-wide key load reads 64
 // contiguous bytes of each of 16 rows.
 // Two workgroups per CU (at most 128 VGPRs): a launch has about two per CU.
-template <int D>
+template <int D, bool GLOBAL>
 __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, float* __restrict__ e_out,
     float* __restrict__ r_out, BatchGeom bg, int group, int hchunk, int nchunks, float scale) {
@@ -200,15 +204,16 @@ __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kerne
     extern __shared__ __align__(16) float smem_mfma[];
     uint16_t* bsplit = reinterpret_cast<uint16_t*>(smem_mfma);   // [3][16][BS] bf16 bits
     float* qbar = smem_mfma + 3 * 16 * BS / 2;                    // [hchunk][D]
-    float* a = qbar + hchunk * D;         // [hchunk][N], rows 16-byte aligned if 4 | N
-
     const int h0 = g * group + ci * hchunk;
     const int nh = min(hchunk, group - ci * hchunk);
+    const int64_t erow = bg.L * bg.H * ig.tok + static_cast<int64_t>(l) * H * N;
+    // [hchunk][N] logits: LDS (rows 16-byte aligned if 4 | N), or (GLOBAL) the
+    // chunk's output rows, overwritten in place
+    float* a = GLOBAL ? e_out + erow + static_cast<int64_t>(h0) * N : qbar + hchunk * D;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int lr = lane % 16, lg = lane / 16;
     const uint16_t* kg = k + ig.k_off + static_cast<int64_t>(lkv) * N * D + 8 * lg;
     const uint16_t* ql = q + ig.q_off + static_cast<int64_t>(l) * H * NT * D;
-    const int64_t erow = bg.L * bg.H * ig.tok + static_cast<int64_t>(l) * H * N;
     const int tiles = (N + 15) / 16;
     const int cnt = wave < tiles ? (tiles - wave + NW - 1) / NW : 0;   // this wave's tiles
 
@@ -254,7 +259,7 @@ __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kerne
 
     // ---- 2. logits of every head of the chunk, 16 keys per tile ----------------
     const uint16_t* bq = bsplit + lr * BS + 8 * lg;
-    const bool vec_store = (N & 3) == 0;
+    const bool vec_store = !GLOBAL && (N & 3) == 0;
     for (int i0 = 0; i0 < cnt; i0 += P) {
 #pragma unroll
         for (int p = 0; p < P; ++p) {
@@ -277,7 +282,7 @@ __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kerne
 #pragma unroll
                 for (int r = 0; r < 4; ++r) z[r] = (co[r] + cm[r]) + ch[r];
                 if (lr < nh) {
-                    float* dst = a + lr * N + key0;
+                    float* dst = a + static_cast<int64_t>(lr) * N + key0;
                     if (vec_store && key0 + 3 < N) {
                         *reinterpret_cast<f32x4*>(dst) = z;
                     } else {
@@ -289,22 +294,25 @@ __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kerne
             }
         }
     }
+    if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
+    if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
     // ---- 3. softmax and supports per head ----------------------------------------
     for (int j = wave; j < nh; j += NW) {
         const int64_t row = erow + static_cast<int64_t>(h0 + j) * N;
-        wave_softmax_store(a + j * N, N, lane, e_out + row, r_out ? r_out + row : nullptr);
+        wave_softmax_store(a + static_cast<int64_t>(j) * N, N, lane, e_out + row,
+                           r_out ? r_out + row : nullptr);
     }
 }
 
-template <int D>
+template <int D, bool GLOBAL>
 hipError_t launch_group_mfma(const Dims& d, float scale, const void* q, const void* k, float* e,
                              float* r, int hchunk, hipStream_t st) {
     const int nchunks = static_cast<int>((d.group + hchunk - 1) / hchunk);
     const size_t lds = 3 * 16 * (D + 8) * sizeof(uint16_t) +
-                       static_cast<size_t>(hchunk) * (D + d.N) * sizeof(float);
-    auto kern = score_group_mfma_kernel<D>;
+                       static_cast<size_t>(hchunk) * (D + (GLOBAL ? 0 : d.N)) * sizeof(float);
+    auto kern = score_group_mfma_kernel<D, GLOBAL>;
     if (lds > 64 * 1024) {
         hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                              hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -318,12 +326,12 @@ hipError_t launch_group_mfma(const Dims& d, float scale, const void* q, const vo
     return hipGetLastError();
 }
 
-template <typename T, int D, int HC>
+template <typename T, int D, int HC, bool GLOBAL>
 hipError_t launch_group(const Dims& d, float scale, const void* q, const void* k, float* e,
                         float* r, int hchunk, hipStream_t st) {
     const int nchunks = static_cast<int>((d.group + hchunk - 1) / hchunk);
-    const size_t lds = static_cast<size_t>(hchunk) * (D + d.N) * sizeof(float);
-    auto kern = score_group_kernel<T, D, HC>;
+    const size_t lds = static_cast<size_t>(hchunk) * (D + (GLOBAL ? 0 : d.N)) * sizeof(float);
+    auto kern = score_group_kernel<T, D, HC, GLOBAL>;
     if (lds > 64 * 1024) {
         hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                              hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -340,7 +348,7 @@ hipError_t launch_group(const Dims& d, float scale, const void* q, const void* k
 // One query head per key head: one wave per (image, layer, head) unit, no
 // workgroup barrier (wave_head); the workgroup only packs up to 4 independent
 // waves together.
-template <typename T, int D>
+template <typename T, int D, bool GLOBAL>
 __global__ __launch_bounds__(kThreads) void score_wave_kernel(
     const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
     float* __restrict__ r_out, BatchGeom bg, int64_t units, int nmax, float scale) {
@@ -352,9 +360,10 @@ __global__ __launch_bounds__(kThreads) void score_wave_kernel(
     const int lh = static_cast<int>(unit - b * bg.L * bg.H);
     const ImageGeom ig = image_geom(bg, b);
     const int NT = ig.NT, N = ig.N;
-    float* a = smem + wave * nmax;
     const int64_t row = bg.L * bg.H * ig.tok + static_cast<int64_t>(lh) * N;
-    wave_head<T, D>(q + ig.q_off + static_cast<int64_t>(lh) * NT * D,
+    // logits in LDS, or (GLOBAL) in the head's output row, overwritten in place
+    float* a = GLOBAL ? e_out + row : smem + wave * nmax;
+    wave_head<T, D, GLOBAL>(q + ig.q_off + static_cast<int64_t>(lh) * NT * D,
                     k + ig.k_off + static_cast<int64_t>(lh) * N * D, NT, N,
                     mean_query_scale(scale, NT), a, lane, e_out + row,
                     r_out ? r_out + row : nullptr);
@@ -363,12 +372,15 @@ __global__ __launch_bounds__(kThreads) void score_wave_kernel(
 template <typename T, int D>
 hipError_t launch_wave(const Dims& d, float scale, const void* q, const void* k, float* e,
                        float* r, hipStream_t st) {
+    // a head's logits in LDS when one fits the budget, else in its output row
     const int64_t per_wave = d.N * static_cast<int64_t>(sizeof(float));
-    const int wpg = static_cast<int>(std::clamp<int64_t>(kLdsBudget / per_wave, 1, kWaves));
+    const bool global = per_wave > kLdsBudget;
+    const int wpg = global ? kWaves
+                           : static_cast<int>(std::clamp<int64_t>(kLdsBudget / per_wave, 1, kWaves));
     const int64_t units = d.B * d.L * d.H;
     const int64_t blocks = (units + wpg - 1) / wpg;
-    const size_t lds = static_cast<size_t>(wpg * per_wave);
-    auto kern = score_wave_kernel<T, D>;
+    const size_t lds = global ? 0 : static_cast<size_t>(wpg * per_wave);
+    auto kern = global ? score_wave_kernel<T, D, true> : score_wave_kernel<T, D, false>;
     if (lds > 64 * 1024) {
         hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                              hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -387,17 +399,27 @@ hipError_t dispatch(const Dims& d, float scale, const void* q, const void* k, fl
     if (d.group == 1) return launch_wave<T, D>(d, scale, q, k, e, r, st);
     // query heads per workgroup: all of the group, at most one MFMA tile's columns
     // (bf16) or kMaxChunk (fp32), and as many as fit the LDS budget with their
-    // logits; chunks balanced
+    // logits; chunks balanced.  When not even one head's logits fit, they go to
+    // the output rows instead and the chunk is bounded by the first two limits.
     constexpr bool mfma = std::is_same<T, uint16_t>::value;
-    const int64_t fit = std::max<int64_t>(1, kLdsBudget / ((D + d.N) * 4));
-    int hchunk = static_cast<int>(
-        std::min<int64_t>({d.group, mfma ? kMfmaMaxChunk : kMaxChunk, fit}));
+    const int64_t fit = kLdsBudget / ((D + d.N) * 4);
+    const bool global = fit < 1;
+    int hchunk = static_cast<int>(std::min<int64_t>(
+        {d.group, mfma ? kMfmaMaxChunk : kMaxChunk, global ? d.group : fit}));
     const int nchunks = static_cast<int>((d.group + hchunk - 1) / hchunk);
     hchunk = static_cast<int>((d.group + nchunks - 1) / nchunks);
-    if constexpr (mfma) return launch_group_mfma<D>(d, scale, q, k, e, r, hchunk, st);
-    if (hchunk <= 2) return launch_group<T, D, 2>(d, scale, q, k, e, r, hchunk, st);
-    if (hchunk <= 4) return launch_group<T, D, 4>(d, scale, q, k, e, r, hchunk, st);
-    return launch_group<T, D, 8>(d, scale, q, k, e, r, hchunk, st);
+    if constexpr (mfma) {
+        if (global) return launch_group_mfma<D, true>(d, scale, q, k, e, r, hchunk, st);
+        return launch_group_mfma<D, false>(d, scale, q, k, e, r, hchunk, st);
+    } else {
+        auto run = [&](auto tag) {
+            constexpr bool G = decltype(tag)::value;
+            if (hchunk <= 2) return launch_group<T, D, 2, G>(d, scale, q, k, e, r, hchunk, st);
+            if (hchunk <= 4) return launch_group<T, D, 4, G>(d, scale, q, k, e, r, hchunk, st);
+            return launch_group<T, D, 8, G>(d, scale, q, k, e, r, hchunk, st);
+        };
+        return global ? run(std::true_type{}) : run(std::false_type{});
+    }
 }
 
 }  // namespace

@@ -51,6 +51,14 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// The same for logits kept in global memory (an image whose logits do not fit in
+// LDS): the stores complete and the vector L1 is invalidated before the reads.
+__device__ __forceinline__ void global_logits_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
 // Lane geometry of the per-wave score stage: 8 elements per lane, LPR lanes per
 // row, RPW rows per wave-wide load, KU rows per lane in flight (16 B per lane per
 // row for bf16, 32 B for fp32).
@@ -213,9 +221,10 @@ __device__ __forceinline__ void wave_softmax_store(float* a, int N, int lane,
 
 // Eq. 1, 8 and 9 for one query head, computed by one wave with no workgroup
 // barrier.  qh: the head's [N_T, d] queries; kh: its key head's [N, d] keys; a: N
-// floats of LDS owned by the wave.  The first key batch is requested before the
-// query mean, and each later batch before the previous one is used.
-template <typename T, int D>
+// floats owned by the wave, in LDS or (GLOBAL) in global memory (the head's own
+// output row, overwritten in place).  The first key batch is requested before
+// the query mean, and each later batch before the previous one is used.
+template <typename T, int D, bool GLOBAL = false>
 __device__ __forceinline__ void wave_head(const T* __restrict__ qh, const T* __restrict__ kh,
                                           int NT, int N, float qscale, float* a, int lane,
                                           float* __restrict__ eo, float* __restrict__ ro) {
@@ -236,7 +245,8 @@ __device__ __forceinline__ void wave_head(const T* __restrict__ qh, const T* __r
         load_key_batch<T, D>(ka, kh, base + 2 * G::BATCH, wrow, N);
         key_batch_logits<T, D>(kb, qb, a, base + G::BATCH, wrow, wl, N);
     }
-    wave_lds_sync();
+    if constexpr (GLOBAL) global_logits_sync();
+    else wave_lds_sync();
     wave_softmax_store(a, N, lane, eo, ro);
 }
 

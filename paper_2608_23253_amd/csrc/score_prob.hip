@@ -60,6 +60,8 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
     return x * q + min(x, r) + i;
 }
 
+constexpr int64_t kColumnsInLds = 16384;
+
 template <typename T, int D> struct ProbCfg;
 template <int D> struct ProbCfg<uint16_t, D> {
     static constexpr int QC = 128;           // query rows per LDS chunk
@@ -126,7 +128,7 @@ __device__ __forceinline__ void load_queries(float (&b)[D / 4], const float* qs,
 
 // TG key tiles per group, two groups in flight per wave: 4 tiles (2 workgroups per
 // CU by registers) when a chunk has 8 query blocks, else 2 (3 per CU).
-template <typename T, int D, int TG>
+template <typename T, int D, int TG, bool GLOBAL>
 __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_kernel(
     const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
     float* __restrict__ r_out, BatchGeom bg, int group, float scale, int nblocks, int qcap) {
@@ -142,7 +144,6 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
     float* st_c = st_m + qcap;                                   // [qcap] reference c_t
     float* wpart = st_c + qcap;                                  // [kWaves][qcap][4]
     float* lstat = wpart + kWaves * qcap * 4;                    // [3][qbcap][kThreads]
-    float* colsum = lstat + 3 * qbcap * kThreads;                // [N]
     __shared__ int s_far;                                        // some |z s - c_t| > 1/8
 
     const int64_t bid = xcd_remap(blockIdx.x, nblocks);          // (b*L + l)*H + h
@@ -154,6 +155,9 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
     const int NT = ig.NT, N = ig.N;
     const T* qh = q + ig.q_off + static_cast<int64_t>(lh) * NT * D;
     const T* kg = k + ig.k_off + static_cast<int64_t>(l * bg.Hkv + g) * N * D;
+    const int64_t row = bg.L * bg.H * ig.tok + static_cast<int64_t>(lh) * N;
+    // [N] column sums: LDS, or (GLOBAL) the head's output row, overwritten at the end
+    float* colsum = GLOBAL ? e_out + row : lstat + 3 * qbcap * kThreads;
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const int lr = lane % 16, lg = lane / 16;
     // Key tiles of 16 rows go to the waves round-robin (wave w: tiles w, w + 4,
@@ -199,7 +203,8 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
         }
     };
 
-    for (int n = tid; n < N; n += kThreads) colsum[n] = 0.f;
+    if constexpr (!GLOBAL)
+        for (int n = tid; n < N; n += kThreads) colsum[n] = 0.f;
 
     for (int t0 = 0; t0 < NT; t0 += qcap) {
         const int rows = min(qcap, NT - t0);
@@ -326,7 +331,12 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
             for (int i = 0; i < TG * 4; ++i) {
                 const float sum = group_sum<16>(col[i]);
                 const int key = tile_of(j, i / 4) * 16 + 4 * lg + i % 4;
-                if (lr == 0 && key < N) colsum[key] += unit * sum;
+                // a key's sums are kept by one lane through every chunk; in global
+                // memory its first chunk starts the sum, as the zeroed LDS does
+                if (lr == 0 && key < N) {
+                    const float prev = (GLOBAL && t0 == 0) ? 0.f : colsum[key];
+                    colsum[key] = prev + unit * sum;
+                }
             }
         };
         if (!far) {
@@ -369,9 +379,10 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
             }
         }
     }
+    if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
+    if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
-    const int64_t row = bg.L * bg.H * ig.tok + static_cast<int64_t>(lh) * N;
     const float inv_nt = 1.0f / static_cast<float>(NT);
     for (int n = tid; n < N; n += kThreads) {
         const float u = colsum[n] * inv_nt;
@@ -384,10 +395,13 @@ template <typename T, int D, int TG>
 hipError_t launch_mp(const Dims& d, float scale, const void* q, const void* k, float* e,
                      float* r, int qcap, hipStream_t st) {
     using C = ProbCfg<T, D>;
+    // the column sums in LDS up to kColumnsInLds keys, else in the output rows
+    const bool global = d.N > kColumnsInLds;
     const size_t lds = static_cast<size_t>(qcap) * C::QS * sizeof(T) +
                        (2 * qcap + kWaves * qcap * 4 + 3 * (qcap / 16) * kThreads) * sizeof(float) +
-                       static_cast<size_t>(d.N) * sizeof(float);
-    auto kern = score_mean_prob_kernel<T, D, TG>;
+                       (global ? 0 : static_cast<size_t>(d.N) * sizeof(float));
+    auto kern = global ? score_mean_prob_kernel<T, D, TG, true>
+                       : score_mean_prob_kernel<T, D, TG, false>;
     if (lds > 64 * 1024) {
         hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                              hipFuncAttributeMaxDynamicSharedMemorySize,

@@ -5,7 +5,9 @@
 // (chunk = ceil(N / 1024), one token for N <= 1024) and keeps their values in
 // registers throughout.  The work per image is a few KB, so the kernel is bound
 // by latency: every step below is shaped to need few dependent LDS round trips
-// and workgroup barriers.
+// and workgroup barriers.  An image of more than 16384 tokens is taken in
+// segments of 16384 (16 per thread), every pass below visiting the segments in
+// order and reloading (or recomputing) their values.
 //
 //  1. cell representatives (Eq. 20-21): the 64-bit key
 //     (order-preserving bits of c) << 32 | index is minimised per cell, i.e. the
@@ -45,7 +47,7 @@ namespace {
 
 constexpr int kThreads = 1024;
 constexpr int kWaves = kThreads / kWave;
-constexpr int kMaxChunk = 16;          // tokens per thread: N <= 16384
+constexpr int kMaxChunk = 16;          // tokens per thread and segment
 constexpr int kRowShl1 = 0x101;
 
 template <int CTRL>
@@ -124,47 +126,82 @@ struct SelectShared {
     uint64_t found;
 };
 
-// Selection of one image (Eq. 20-23).  cv[j] = c and posv[j] = raster position
-// of token n0 + j for j < cnt (registers of the calling thread, tokens owned as
-// described above); best: G*G words of LDS; tok: the image's first token in the
-// optional per-token outputs.  Calls keep(slot, j) once for every
-// kept token (slot = its rank in ascending token order).  All threads of the
+// Token layout of one image's selection.  An image of at most kSegment tokens is
+// one segment: thread t owns tokens n0 = t * chunk .. n0 + chunk - 1 (chunk =
+// ceil(N / 1024)) and keeps their values in registers through every pass.  A
+// larger image is cut into segments of kSegment tokens (chunk = kMaxChunk); each
+// pass visits the segments in order and has the caller load the segment's values
+// again.  Every decision is an exact comparison of integer keys, so the kept set
+// does not depend on the layout.
+constexpr int kSegment = kThreads * kMaxChunk;
+
+// Selection of one image (Eq. 20-23).  load(n0, cnt, first) fills the caller's
+// registers for the tokens n0 .. n0 + cnt - 1 (cnt <= chunk; entries past cnt
+// are never used): cv[j] = c, posv[j] = raster position, and whatever keep()
+// reads; first is set on the first visit of each token (per-token outputs are
+// written then).  best: G*G words of LDS; tok: the image's first token in the
+// optional per-token outputs.  Calls keep(slot, n, j) once for every kept token n
+// (slot = its rank in ascending token order; j its register).  All threads of the
 // workgroup call it.
-template <int MAXC, typename Keep>
-__device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], int n0, int cnt,
-                             int chunk, uint64_t* best, SelectShared& sh, int64_t tok,
+template <int MAXC, typename Load, typename Keep>
+__device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], Load&& load,
+                             uint64_t* best, SelectShared& sh, int64_t tok,
                              double* __restrict__ adj_out, uint8_t* __restrict__ rep_out, int N,
                              int gh, int gw, int G, float lambda, int K, Keep&& keep) {
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    const int nseg = MAXC == kMaxChunk ? (N + kSegment - 1) / kSegment : 1;
+    const bool streamed = nseg > 1;
+    const int chunk = streamed ? kMaxChunk : (N + kThreads - 1) / kThreads;
+    auto first_of = [&](int s) { return min(N, s * kSegment + tid * chunk); };
+    auto count_of = [&](int n0) { return max(0, min(N - n0, chunk)); };
+    // the tokens of segment s in the registers (one segment: loaded once)
+    auto visit = [&](int s, bool first) {
+        if (streamed || first) {
+            const int n0 = first_of(s);
+            load(n0, count_of(n0), first);
+        }
+    };
 
     for (int i = tid; i < G * G; i += kThreads) best[i] = ~0ull;
     if (tid < 256) sh.hist[0][tid] = 0u;
     __syncthreads();
 
-    // ---- cell representatives (Eq. 20) -----------------------------------
     int cell[MAXC];
+    auto cells_of = [&](int cnt) {
 #pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-        if (j >= chunk) break;
-        const int n = n0 + j;
-        const int pos = posv[j];
-        const bool placed = j < cnt && pos >= 0 && pos < gh * gw;
-        const int row = pos / gw, col = pos - (pos / gw) * gw;
-        cell[j] = placed ? (row * G / gh) * G + col * G / gw : -1 - lane;
-        uint64_t key = j < cnt ? (static_cast<uint64_t>(ordered_bits(cv[j])) << 32) |
-                                     static_cast<uint32_t>(n)
-                               : ~0ull;
-        seg_min_step<kRowShr1>(key, cell[j]);
-        seg_min_step<kRowShr2>(key, cell[j]);
-        seg_min_step<kRowShr4>(key, cell[j]);
-        seg_min_step<kRowShr8>(key, cell[j]);
-        // the last lane of each run inside the row holds the run's minimum
-        const int next = static_cast<int>(
-            __builtin_amdgcn_update_dpp(-1, cell[j], kRowShl1, 0xF, 0xF, false));
-        const bool last = next != cell[j];   // lane 15 of a row reads -1
-        if (placed && last)
-            atomicMin(reinterpret_cast<unsigned long long*>(best + cell[j]),
-                      static_cast<unsigned long long>(key));
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= chunk) break;
+            const int pos = posv[j];
+            const bool placed = j < cnt && pos >= 0 && pos < gh * gw;
+            const int row = pos / gw, col = pos - (pos / gw) * gw;
+            cell[j] = placed ? (row * G / gh) * G + col * G / gw : -1 - lane;
+        }
+    };
+
+    // ---- cell representatives (Eq. 20) -----------------------------------
+    for (int s = 0; s < nseg; ++s) {
+        visit(s, true);
+        const int n0 = first_of(s), cnt = count_of(n0);
+        cells_of(cnt);
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= chunk) break;
+            const bool placed = cell[j] >= 0;
+            uint64_t key = j < cnt ? (static_cast<uint64_t>(ordered_bits(cv[j])) << 32) |
+                                         static_cast<uint32_t>(n0 + j)
+                                   : ~0ull;
+            seg_min_step<kRowShr1>(key, cell[j]);
+            seg_min_step<kRowShr2>(key, cell[j]);
+            seg_min_step<kRowShr4>(key, cell[j]);
+            seg_min_step<kRowShr8>(key, cell[j]);
+            // the last lane of each run inside the row holds the run's minimum
+            const int next = static_cast<int>(
+                __builtin_amdgcn_update_dpp(-1, cell[j], kRowShl1, 0xF, 0xF, false));
+            const bool last = next != cell[j];   // lane 15 of a row reads -1
+            if (placed && last)
+                atomicMin(reinterpret_cast<unsigned long long*>(best + cell[j]),
+                          static_cast<unsigned long long>(key));
+        }
     }
     __syncthreads();
 
@@ -172,22 +209,44 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], i
     const double lam = static_cast<double>(lambda);
     const double oml = 1.0 - lam;
     uint64_t kk[MAXC];
-    uint64_t kmin = ~0ull, kmax = 0ull;
+    auto keys_of = [&](int n0, int cnt, bool outputs) {
+        cells_of(cnt);
 #pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-        kk[j] = ~0ull;
-        if (j >= chunk) break;
-        if (j < cnt) {
-            const int n = n0 + j;
-            const bool rep = cell[j] >= 0 &&
-                             static_cast<uint32_t>(best[cell[j]]) == static_cast<uint32_t>(n);
-            const double t = __dmul_rn(oml, static_cast<double>(cv[j]));
-            const double adj = rep ? t : __dadd_rn(t, lam);
-            kk[j] = ordered_bits(adj);
-            kmin = kk[j] < kmin ? kk[j] : kmin;
-            kmax = kk[j] > kmax ? kk[j] : kmax;
-            if (adj_out) adj_out[tok + n] = adj;
-            if (rep_out) rep_out[tok + n] = rep ? 1 : 0;
+        for (int j = 0; j < MAXC; ++j) {
+            kk[j] = ~0ull;
+            if (j >= chunk) break;
+            if (j < cnt) {
+                const int n = n0 + j;
+                const bool rep = cell[j] >= 0 &&
+                                 static_cast<uint32_t>(best[cell[j]]) == static_cast<uint32_t>(n);
+                const double t = __dmul_rn(oml, static_cast<double>(cv[j]));
+                const double adj = rep ? t : __dadd_rn(t, lam);
+                kk[j] = ordered_bits(adj);
+                if (outputs && adj_out) adj_out[tok + n] = adj;
+                if (outputs && rep_out) rep_out[tok + n] = rep ? 1 : 0;
+            }
+        }
+    };
+    // later passes over a streamed image recompute the keys of each segment
+    auto revisit = [&](int s) {
+        if (streamed) {
+            visit(s, false);
+            const int n0 = first_of(s);
+            keys_of(n0, count_of(n0), false);
+        }
+    };
+    uint64_t kmin = ~0ull, kmax = 0ull;
+    for (int s = 0; s < nseg; ++s) {
+        visit(s, false);
+        const int n0 = first_of(s), cnt = count_of(n0);
+        keys_of(n0, cnt, true);
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= chunk) break;
+            if (j < cnt) {
+                kmin = kk[j] < kmin ? kk[j] : kmin;
+                kmax = kk[j] > kmax ? kk[j] : kmax;
+            }
         }
     }
     if (K <= 0) return;
@@ -217,20 +276,24 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], i
             uint32_t* h = sh.hist[round % 3];
             // the buffer after this one was last read before the previous barrier
             if (tid < 256) sh.hist[(round + 1) % 3][tid] = 0u;
+            for (int s = 0; s < nseg; ++s) {
+                revisit(s);
+                const int cnt = count_of(first_of(s));
 #pragma unroll
-            for (int j = 0; j < MAXC; ++j) {
-                if (j >= chunk) break;
-                const bool match = j < cnt && (kk[j] & mask) == prefix;
-                const uint32_t digit = static_cast<uint32_t>(kk[j] >> shift) & 255u;
-                uint64_t mb = __ballot(match);
-                for (int it = 0; it < 2 && mb; ++it) {
-                    const int leader = __ffsll(static_cast<unsigned long long>(mb)) - 1;
-                    const uint32_t d0 = readlane_u32(digit, leader);
-                    const uint64_t same = __ballot(match && digit == d0);
-                    if (lane == leader) atomicAdd(&h[d0], static_cast<uint32_t>(__popcll(same)));
-                    mb &= ~same;
+                for (int j = 0; j < MAXC; ++j) {
+                    if (j >= chunk) break;
+                    const bool match = j < cnt && (kk[j] & mask) == prefix;
+                    const uint32_t digit = static_cast<uint32_t>(kk[j] >> shift) & 255u;
+                    uint64_t mb = __ballot(match);
+                    for (int it = 0; it < 2 && mb; ++it) {
+                        const int leader = __ffsll(static_cast<unsigned long long>(mb)) - 1;
+                        const uint32_t d0 = readlane_u32(digit, leader);
+                        const uint64_t same = __ballot(match && digit == d0);
+                        if (lane == leader) atomicAdd(&h[d0], static_cast<uint32_t>(__popcll(same)));
+                        mb &= ~same;
+                    }
+                    if ((mb >> lane) & 1ull) atomicAdd(&h[digit], 1u);
                 }
-                if ((mb >> lane) & 1ull) atomicAdd(&h[digit], 1u);
             }
             __syncthreads();
             // every wave finds the bin that holds the rank-th matching key
@@ -263,10 +326,14 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], i
             mask |= 0xFFull << shift;
             if (cnt_d == 1u) {
                 // one key carries this prefix: it is the K-th key
+                for (int s = 0; s < nseg; ++s) {
+                    revisit(s);
+                    const int cnt = count_of(first_of(s));
 #pragma unroll
-                for (int j = 0; j < MAXC; ++j) {
-                    if (j >= chunk) break;
-                    if (j < cnt && (kk[j] & mask) == prefix) sh.found = kk[j];
+                    for (int j = 0; j < MAXC; ++j) {
+                        if (j >= chunk) break;
+                        if (j < cnt && (kk[j] & mask) == prefix) sh.found = kk[j];
+                    }
                 }
                 __syncthreads();
                 T = sh.found;
@@ -283,37 +350,50 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], i
     }
 
     // ---- ordered compaction ----------------------------------------------------
-    // counts below 2^16 (N <= 16384): both prefix sums ride in one word
-    uint32_t lt = 0, eq = 0;
+    // per segment (at most 16384 tokens) both prefix sums ride in one word; the
+    // counts of earlier segments are carried
+    uint32_t lt_carry = 0, eq_carry = 0;
+    for (int s = 0; s < nseg; ++s) {
+        revisit(s);
+        const int n0 = first_of(s), cnt = count_of(n0);
+        uint32_t lt = 0, eq = 0;
 #pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-        if (j >= chunk) break;
-        if (j < cnt) {
-            lt += kk[j] < T;
-            eq += kk[j] == T;
-        }
-    }
-    const uint32_t packed = (lt << 16) | eq;
-    const uint32_t incl = wave_inclusive_scan(packed, lane);
-    if (lane == kWave - 1) sh.scan[wave] = incl;
-    __syncthreads();
-    uint32_t before = incl - packed;
-    for (int w = 0; w < wave; ++w) before += sh.scan[w];
-    uint32_t lt_run = before >> 16, eq_run = before & 0xFFFFu;
-#pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-        if (j >= chunk) break;
-        if (j < cnt) {
-            uint32_t pos = static_cast<uint32_t>(K);
-            if (kk[j] < T) {
-                pos = lt_run + (eq_run < need_eq ? eq_run : need_eq);
-                ++lt_run;
-            } else if (kk[j] == T) {
-                if (eq_run < need_eq) pos = lt_run + eq_run;
-                ++eq_run;
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= chunk) break;
+            if (j < cnt) {
+                lt += kk[j] < T;
+                eq += kk[j] == T;
             }
-            if (pos < static_cast<uint32_t>(K)) keep(static_cast<int>(pos), j);
         }
+        const uint32_t packed = (lt << 16) | eq;
+        const uint32_t incl = wave_inclusive_scan(packed, lane);
+        if (lane == kWave - 1) sh.scan[wave] = incl;
+        __syncthreads();
+        uint32_t before = incl - packed, total = 0;
+        for (int w = 0; w < kWaves; ++w) {
+            const uint32_t v = sh.scan[w];
+            if (w < wave) before += v;
+            total += v;
+        }
+        uint32_t lt_run = lt_carry + (before >> 16), eq_run = eq_carry + (before & 0xFFFFu);
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= chunk) break;
+            if (j < cnt) {
+                uint32_t pos = static_cast<uint32_t>(K);
+                if (kk[j] < T) {
+                    pos = lt_run + (eq_run < need_eq ? eq_run : need_eq);
+                    ++lt_run;
+                } else if (kk[j] == T) {
+                    if (eq_run < need_eq) pos = lt_run + eq_run;
+                    ++eq_run;
+                }
+                if (pos < static_cast<uint32_t>(K)) keep(static_cast<int>(pos), n0 + j, j);
+            }
+        }
+        lt_carry += total >> 16;
+        eq_carry += total & 0xFFFFu;
+        if (streamed) __syncthreads();      // sh.scan is written again for the next segment
     }
 }
 
@@ -324,31 +404,28 @@ __global__ __launch_bounds__(kThreads) void spatial_select_kernel(
     extern __shared__ uint64_t best[];
     __shared__ SelectShared sh;
     const int64_t b = blockIdx.x;
-    const int chunk = (N + kThreads - 1) / kThreads;
-    const int n0 = min(N, static_cast<int>(threadIdx.x) * chunk);
-    const int cnt = min(N - n0, chunk);
     const float* cb = prio_c + b * N;
     float cv[MAXC];
     int posv[MAXC];
+    auto load = [&](int n0, int cnt, bool) {
 #pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-        if (j >= chunk) break;
-        cv[j] = cb[min(n0 + j, N - 1)];     // in bounds; unused past cnt
-        posv[j] = n0 + j;
-    }
-    select_image<MAXC>(cv, posv, n0, cnt, chunk, best, sh, b * N, adj_out, rep_out, N, gh, gw, G,
-                       lambda, K, [&](int slot, int j) { keep_idx[b * K + slot] = n0 + j; });
+        for (int j = 0; j < MAXC; ++j) {
+            cv[j] = j < cnt ? cb[n0 + j] : 0.f;
+            posv[j] = n0 + j;
+        }
+    };
+    select_image<MAXC>(cv, posv, load, best, sh, b * N, adj_out, rep_out, N, gh, gw, G, lambda, K,
+                       [&](int slot, int n, int) { keep_idx[b * K + slot] = n; });
 }
 
-// Raster positions of the owned tokens (candidate positions when given).
+// Raster positions of the tokens n0 .. n0 + cnt - 1 (candidate positions when
+// given).
 template <int MAXC>
-__device__ __forceinline__ void owned_positions(int (&posv)[MAXC], const int32_t* cand_pos,
-                                                int64_t tok, int n0, int cnt, int chunk) {
+__device__ __forceinline__ void token_positions(int (&posv)[MAXC], const int32_t* cand_pos,
+                                                int64_t tok, int n0, int cnt) {
 #pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-        if (j >= chunk) break;
+    for (int j = 0; j < MAXC; ++j)
         posv[j] = cand_pos ? (j < cnt ? cand_pos[tok + n0 + j] : -1) : n0 + j;
-    }
 }
 
 // Dempster fusion across the layers (Eq. 11-19) from per-layer reliability and
@@ -357,7 +434,9 @@ __device__ __forceinline__ void owned_positions(int (&posv)[MAXC], const int32_t
 // Dempster kernels.  Each layer's inputs are requested together (and, with up to
 // 4 tokens per thread, before the previous layer is combined).  m_prev, when
 // given, is the candidates' fused mass from earlier operations: every layer is
-// combined onto it.  The ablation variants change one step each (e2s.h).
+// combined onto it.  The ablation variants change one step each (e2s.h).  For an
+// image of more than 16384 tokens the fusion is recomputed on every visit of a
+// segment (the same arithmetic, so the same values).
 template <int MAXC>
 __global__ __launch_bounds__(kThreads) void ds_select_kernel(
     const float* __restrict__ rho, const float* __restrict__ pbar_c,
@@ -368,85 +447,85 @@ __global__ __launch_bounds__(kThreads) void ds_select_kernel(
     const ImageGeom ig = image_geom(bg, b);
     const int L = bg.L, N = ig.N, gh = ig.gh, gw = ig.gw, K = ig.K;
     const int64_t tok = ig.tok;
-    const int chunk = (N + kThreads - 1) / kThreads;
-    const int n0 = min(N, static_cast<int>(threadIdx.x) * chunk);
-    const int cnt = min(N - n0, chunk);
     const bool unit_rho = a.variant == E2S_VARIANT_NO_HEAD_RELIABILITY;
     const bool last_only = a.variant == E2S_VARIANT_NO_LAYER_FUSION;
     const bool carried = m_prev != nullptr && !last_only;
-    const int l_first = last_only ? L - 1 : 0;          // first layer read
-
-    float r[MAXC], e[MAXC];      // current layer's inputs
-    float aI[MAXC], aU[MAXC], aT[MAXC], kl[MAXC];
-    auto load_layer = [&](int l, float (&rr)[MAXC], float (&ee)[MAXC]) {
-        const int64_t base = L * tok + static_cast<int64_t>(l) * N;
-#pragma unroll
-        for (int j = 0; j < MAXC; ++j) {
-            if (j >= chunk) break;
-            const int64_t i = base + min(n0 + j, N - 1);   // in bounds; unused past cnt
-            rr[j] = unit_rho ? 1.0f : rho[i];
-            ee[j] = pbar_c[i];
-        }
-    };
-    load_layer(l_first, r, e);
-#pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-        if (j >= chunk) break;
-        kl[j] = 0.f;
-        if (carried) {
-            const int64_t i = 3 * (tok + min(n0 + j, N - 1));
-            aI[j] = m_prev[i];
-            aU[j] = m_prev[i + 1];
-            aT[j] = m_prev[i + 2];
-            float mI, mU, mT;
-            masses_from_reliability(r[j], e[j], mI, mU, mT);
-            kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
-        } else {
-            masses_from_reliability(r[j], e[j], aI[j], aU[j], aT[j]);
-        }
-    }
-    // with many tokens per thread the prefetch would not fit in registers
-    constexpr bool kPrefetch = MAXC <= 4;
-    const int l_end = last_only ? l_first + 1 : L;
-    if (kPrefetch && l_first + 1 < l_end) load_layer(l_first + 1, r, e);
-    for (int l = l_first + 1; l < l_end; ++l) {
-        float r2[MAXC], e2[MAXC];
-        if (!kPrefetch) load_layer(l, r, e);
-        else if (l + 1 < l_end) load_layer(l + 1, r2, e2);
-#pragma unroll
-        for (int j = 0; j < MAXC; ++j) {
-            if (j >= chunk) break;
-            float mI, mU, mT;
-            masses_from_reliability(r[j], e[j], mI, mU, mT);
-            kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
-            if (kPrefetch && l + 1 < l_end) {
-                r[j] = r2[j];
-                e[j] = e2[j];
-            }
-        }
-    }
     const bool protect = a.variant != E2S_VARIANT_NO_CONFLICT;
+    const int l_first = last_only ? L - 1 : 0;          // first layer read
+    const int l_end = last_only ? l_first + 1 : L;
+
+    float aI[MAXC], aU[MAXC], aT[MAXC];
     float cv[MAXC];
     int posv[MAXC];
-    owned_positions<MAXC>(posv, a.cand_pos, tok, n0, cnt, chunk);
+    auto load = [&](int n0, int cnt, bool first) {
+        float r[MAXC], e[MAXC];      // current layer's inputs
+        float kl[MAXC];
+        auto load_layer = [&](int l, float (&rr)[MAXC], float (&ee)[MAXC]) {
+            const int64_t base = L * tok + static_cast<int64_t>(l) * N;
 #pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-        if (j >= chunk) break;
-        cv[j] = priority_complement(aU[j], protect ? kl[j] : 0.0f);
-        if (j < cnt) {
-            const int64_t i = tok + n0 + j;
-            if (a.fused) {
-                a.fused[3 * i + 0] = aI[j];
-                a.fused[3 * i + 1] = aU[j];
-                a.fused[3 * i + 2] = aT[j];
+            for (int j = 0; j < MAXC; ++j) {
+                if (j >= cnt) break;
+                const int64_t i = base + n0 + j;
+                rr[j] = unit_rho ? 1.0f : rho[i];
+                ee[j] = pbar_c[i];
             }
-            if (a.prio_c) a.prio_c[i] = cv[j];
+        };
+        load_layer(l_first, r, e);
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= cnt) break;
+            kl[j] = 0.f;
+            if (carried) {
+                const int64_t i = 3 * (tok + n0 + j);
+                aI[j] = m_prev[i];
+                aU[j] = m_prev[i + 1];
+                aT[j] = m_prev[i + 2];
+                float mI, mU, mT;
+                masses_from_reliability(r[j], e[j], mI, mU, mT);
+                kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
+            } else {
+                masses_from_reliability(r[j], e[j], aI[j], aU[j], aT[j]);
+            }
         }
-    }
-    select_image<MAXC>(cv, posv, n0, cnt, chunk, best, sh, tok, nullptr, nullptr, N, gh, gw,
-                       a.cells, a.lambda, K, [&](int slot, int j) {
+        // with many tokens per thread the prefetch would not fit in registers
+        constexpr bool kPrefetch = MAXC <= 4;
+        if (kPrefetch && l_first + 1 < l_end) load_layer(l_first + 1, r, e);
+        for (int l = l_first + 1; l < l_end; ++l) {
+            float r2[MAXC], e2[MAXC];
+            if (!kPrefetch) load_layer(l, r, e);
+            else if (l + 1 < l_end) load_layer(l + 1, r2, e2);
+#pragma unroll
+            for (int j = 0; j < MAXC; ++j) {
+                if (j >= cnt) break;
+                float mI, mU, mT;
+                masses_from_reliability(r[j], e[j], mI, mU, mT);
+                kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
+                if (kPrefetch && l + 1 < l_end) {
+                    r[j] = r2[j];
+                    e[j] = e2[j];
+                }
+            }
+        }
+        token_positions<MAXC>(posv, a.cand_pos, tok, n0, cnt);
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= cnt) break;
+            cv[j] = priority_complement(aU[j], protect ? kl[j] : 0.0f);
+            if (first) {
+                const int64_t i = tok + n0 + j;
+                if (a.fused) {
+                    a.fused[3 * i + 0] = aI[j];
+                    a.fused[3 * i + 1] = aU[j];
+                    a.fused[3 * i + 2] = aT[j];
+                }
+                if (a.prio_c) a.prio_c[i] = cv[j];
+            }
+        }
+    };
+    select_image<MAXC>(cv, posv, load, best, sh, tok, nullptr, nullptr, N, gh, gw, a.cells,
+                       a.lambda, K, [&](int slot, int n, int j) {
                            const int64_t o = ig.keep_off + slot;
-                           a.keep_idx[o] = n0 + j;
+                           a.keep_idx[o] = n;
                            if (a.keep_pos) a.keep_pos[o] = posv[j];
                            if (a.m_out) {
                                a.m_out[3 * o + 0] = aI[j];
@@ -470,31 +549,31 @@ __global__ __launch_bounds__(kThreads) void attention_select_kernel(
     const ImageGeom ig = image_geom(bg, b);
     const int L = bg.L, H = bg.H, N = ig.N, gh = ig.gh, gw = ig.gw, K = ig.K;
     const int64_t tok = ig.tok;
-    const int chunk = (N + kThreads - 1) / kThreads;
-    const int n0 = min(N, static_cast<int>(threadIdx.x) * chunk);
-    const int cnt = min(N - n0, chunk);
     float cv[MAXC];
-#pragma unroll
-    for (int j = 0; j < MAXC; ++j) {
-        if (j >= chunk) break;
-        const float* eb = support_c + L * H * tok + min(n0 + j, N - 1);
-        float s = 0.f;
-        for (int lh = 0; lh < L * H; lh += 8) {
-            float ev[8];
-#pragma unroll
-            for (int u = 0; u < 8; ++u) ev[u] = lh + u < L * H ? eb[(lh + u) * static_cast<int64_t>(N)] : 0.f;
-#pragma unroll
-            for (int u = 0; u < 8; ++u)
-                if (lh + u < L * H) s += (4.0f * ev[u]) / (1.0f - 2.0f * ev[u]);
-        }
-        cv[j] = -s;
-    }
     int posv[MAXC];
-    owned_positions<MAXC>(posv, a.cand_pos, tok, n0, cnt, chunk);
-    select_image<MAXC>(cv, posv, n0, cnt, chunk, best, sh, tok, nullptr, nullptr, N, gh, gw,
-                       a.cells, 0.0f, K, [&](int slot, int j) {
+    auto load = [&](int n0, int cnt, bool) {
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= cnt) break;
+            const float* eb = support_c + L * H * tok + n0 + j;
+            float s = 0.f;
+            for (int lh = 0; lh < L * H; lh += 8) {
+                float ev[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    ev[u] = lh + u < L * H ? eb[(lh + u) * static_cast<int64_t>(N)] : 0.f;
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    if (lh + u < L * H) s += (4.0f * ev[u]) / (1.0f - 2.0f * ev[u]);
+            }
+            cv[j] = -s;
+        }
+        token_positions<MAXC>(posv, a.cand_pos, tok, n0, cnt);
+    };
+    select_image<MAXC>(cv, posv, load, best, sh, tok, nullptr, nullptr, N, gh, gw, a.cells, 0.0f,
+                       K, [&](int slot, int n, int j) {
                            const int64_t o = ig.keep_off + slot;
-                           a.keep_idx[o] = n0 + j;
+                           a.keep_idx[o] = n;
                            if (a.keep_pos) a.keep_pos[o] = posv[j];
                            if (a.m_out) {
                                a.m_out[3 * o + 0] = 0.0f;

@@ -86,14 +86,24 @@ def test_status_strings():
     ("num_kv_heads", 0, L.ERR_BAD_SHAPE), ("head_dim", 96, L.ERR_UNSUPPORTED),
     ("head_dim", 0, L.ERR_BAD_SHAPE), ("num_text", 0, L.ERR_BAD_SHAPE),
     ("grid_h", 0, L.ERR_BAD_SHAPE), ("grid_w", -1, L.ERR_BAD_SHAPE),
-    ("grid_h", 200, L.ERR_UNSUPPORTED),          # with grid_w = 100: N = 20000 > 16384
+    ("grid_h", 2000, L.ERR_UNSUPPORTED),         # with grid_w = 1000: N = 2e6 > 2^20
     ("num_heads", 130, L.ERR_UNSUPPORTED),       # with num_kv_heads = 2: H > 128
 ])
 def test_bad_shapes(field, value, expect):
     kw = {field: value}
-    if field == "grid_h" and value == 200:
-        kw["grid_w"] = 100                        # N = 20000 > 16384
+    if field == "grid_h" and value == 2000:
+        kw["grid_w"] = 1000                       # N = 2e6 > 2^20
     assert score(good_shape(**kw), good_params()) == expect
+
+
+def test_large_grids_accepted_and_cells_capped():
+    """Up to 2^20 visual tokens per image; at most 128 cells per side."""
+    big = good_shape(grid_h=1024, grid_w=1024)                    # N = 2^20
+    assert score(big, good_params(), q=None) == L.ERR_NULL_POINTER  # validated, not rejected
+    assert score(good_shape(grid_h=1024, grid_w=1025), good_params()) == L.ERR_UNSUPPORTED
+    wide = good_shape(grid_h=130, grid_w=130)
+    assert select(wide, good_params(cells=128, keep=5), c=None) == L.ERR_NULL_POINTER
+    assert select(wide, good_params(cells=129, keep=5)) == L.ERR_UNSUPPORTED
 
 
 @pytest.mark.parametrize("field,value", [
@@ -274,7 +284,7 @@ def test_ragged_rejects_invalid_records():
     bad[0].num_text = 0
     assert ragged(bad) == L.ERR_BAD_SHAPE
     bad = ragged_images()
-    bad[0].grid_h, bad[0].grid_w = 200, 100                         # N_b > 16384
+    bad[0].grid_h, bad[0].grid_w = 2000, 1000                       # N_b > 2^20
     assert ragged(bad) == L.ERR_UNSUPPORTED
     bad = ragged_images()
     bad[1].k_offset = -8

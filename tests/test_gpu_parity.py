@@ -73,6 +73,20 @@ CASES = [
                               grid_w=12, keep=24, salient_count=8), name="heavy_text100"),
     _small("max_grid_16384", config_id=56, batch=1, num_layers=1, num_heads=2, num_kv_heads=1,
            num_text=2, grid_h=128, grid_w=128, keep=1000, salient_count=40, clusters=4),
+    # more than 16384 visual tokens: the selection streams the image in segments;
+    # above 24576 the logits of the one-head-per-key-head and grouped-query kernels
+    # go to the output rows, and above 16384 the mean-of-probabilities column sums
+    _small("large_grid_22500", config_id=64, batch=1, num_layers=2, num_heads=4, num_kv_heads=4,
+           head_dim=128, num_text=6, grid_h=150, grid_w=150, keep=3000, salient_count=60,
+           clusters=4),
+    _small("large_mha_33000", config_id=65, batch=2, num_layers=1, num_heads=2, num_kv_heads=2,
+           num_text=4, grid_h=150, grid_w=220, keep=4000, salient_count=50, clusters=3),
+    _small("large_gqa_27200", config_id=66, batch=1, num_layers=1, num_heads=8, num_kv_heads=2,
+           head_dim=128, num_text=5, grid_h=160, grid_w=170, keep=5000, salient_count=80,
+           clusters=5),
+    _small("large_f32_gqa_40000", config_id=67, dtype="f32", batch=1, num_layers=1,
+           num_heads=4, num_kv_heads=1, num_text=3, grid_h=200, grid_w=200, keep=20000,
+           cells=8, salient_count=100, clusters=6),
     # batch x layers >= the CU count: e2s_prune / e2s_layer_reliability take the
     # on-chip layer path (one workgroup per image and layer)
     _small("layer_path_ragged", config_id=57, batch=64, num_layers=4, num_heads=6,

@@ -35,6 +35,10 @@ CASES = [
           grid_w=11, num_text=6), [40, 17, 9]),
     (synth.config_by_name("llava").replace(batch=2, num_layers=3), [122, 48, 42]),
     (synth.config_by_name("llava").replace(batch=2, num_layers=3), [20, 8, 0]),
+    # 24000 tokens, then 18000 candidates: selections in segments, with candidate
+    # positions and carried masses
+    (_cfg("large_grid", config_id=72, batch=1, num_heads=2, num_kv_heads=2, grid_h=150,
+          grid_w=160, num_text=4, salient_count=50, clusters=3), [18000, 5000, 900]),
 ]
 
 

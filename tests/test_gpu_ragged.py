@@ -55,6 +55,14 @@ CASES = {
     "mha_f32_d128": (_base("mha_f32_d128", config_id=75, dtype="f32", num_heads=3,
                            num_kv_heads=3, head_dim=128),
                      [(6, 7, 4, 10), (9, 9, 17, 20)], 3),
+    # more than 16384 tokens: the batch streams every image's selection in segments
+    # and (above 24576 tokens) keeps its logits in the output rows, the images alone
+    # mostly not
+    "large_gqa2_bf16_d128": (_base("large_gqa2_bf16_d128", config_id=81, num_layers=1,
+                                   num_heads=4, num_kv_heads=2, head_dim=128, salient_count=40,
+                                   clusters=3),
+                             [(160, 170, 5, 2000), (12, 9, 7, 20), (140, 130, 30, 900),
+                              (4, 4, 2, 3)], 4),
     # peaked attention (the online statistics of the mean-of-probabilities kernel);
     # N_T = 100 gives the batch query chunks of 112 rows, the images alone smaller
     # ones

@@ -4,7 +4,7 @@ Each variant runs through e2s_prune (and, except attention top-K, through
 e2s_fuse_select on the staged reliability outputs, which must give the same bits)
 on seeded cases covering one query head per key head (the on-chip layer path at
 full size, the staged path at small batch), grouped-query heads, fp32 and bf16,
-both score readings.  Kept sets: exact or tie-excused (R-A16's rule on the
+an image of 20000 tokens (selection in segments), both score readings.  Kept sets: exact or tie-excused (R-A16's rule on the
 variant's ranking score)."""
 import numpy as np
 import pytest
@@ -32,6 +32,9 @@ CASES = [
     _small("gqa_d128", config_id=61, num_heads=6, num_kv_heads=2, head_dim=128, grid_h=7,
            grid_w=9, keep=20, cells=3),
     synth.config_by_name("llava").replace(batch=2),
+    # 20000 visual tokens: the selections stream the image in segments
+    _small("large_20000", config_id=62, batch=1, num_layers=2, num_heads=2, num_kv_heads=2,
+           grid_h=100, grid_w=200, keep=2500, cells=4, salient_count=40, clusters=3),
 ]
 VARIANTS = [v for v in O.VARIANTS]
 

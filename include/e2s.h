@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define E2S_ABI_VERSION 5
+#define E2S_ABI_VERSION 6
 
 #if defined(__GNUC__) || defined(__clang__)
 #define E2S_API __attribute__((visibility("default")))
@@ -321,6 +321,43 @@ typedef struct {
  * with strides Hkv*S*d, S*d, d). */
 E2S_API e2s_status e2s_compact_tokens(const e2s_compact_shape* shape, const int32_t* keep_idx,
                                       const void* src, void* dst, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Inputs in place: the source layers' text queries and visual keys read where the
+ * model holds them.  Algorithm 1 takes, at every source layer, the attention
+ * queries of the text tokens and the keys of the visual tokens (Sec. 3.1 Eq. 1);
+ * in a running model these are per-layer projection outputs and key/value-cache
+ * rows (after the rotary embedding), which e2s_prune would need copied into its
+ * packed [B, L, H, N_T, d] and [B, L, Hkv, N, d] arrays.  Here each layer has a
+ * base pointer and the rows are found by element strides, so no copy is made.
+ * ------------------------------------------------------------------------- */
+#define E2S_MAX_VIEW_LAYERS 16
+
+typedef struct {
+    /* Per source layer l < L: Q[b, l, h, t, :] = q[l] + b * q_stride_image +
+     * h * q_stride_head + t * q_stride_text, and K[b, l, g, n, :] = k[l] +
+     * b * k_stride_image + g * k_stride_head + n * k_stride_token, each a row of
+     * d contiguous elements of params->dtype.  Every base and every stride times
+     * the element size must be 16-byte aligned; strides are >= 0 and may differ
+     * from the packed ones (the visual tokens of a cache [B, Hkv, S, d] starting
+     * at token v0: k[l] = cache_l + v0 * d, strides Hkv*S*d, S*d, d; token-major
+     * projections [B, T, H, d]: strides T*H*d, d, H*d).  Entries l >= L unused. */
+    const void* q[E2S_MAX_VIEW_LAYERS];
+    const void* k[E2S_MAX_VIEW_LAYERS];
+    int64_t q_stride_image, q_stride_head, q_stride_text;
+    int64_t k_stride_image, k_stride_head, k_stride_token;
+} e2s_qk_views;
+
+/* e2s_prune with Q and K given as views (L <= E2S_MAX_VIEW_LAYERS, else
+ * E2S_ERR_UNSUPPORTED); everything else as e2s_prune, including the workspace
+ * (e2s_prune_workspace_size) and the results, which equal e2s_prune's on packed
+ * copies of the same values bit for bit.  The views struct is read on the host
+ * during the call; the rows it points to are device memory that the call only
+ * reads. */
+E2S_API e2s_status e2s_prune_views(const e2s_shape* shape, const e2s_params* params,
+                                   const e2s_qk_views* views, void* workspace,
+                                   size_t workspace_bytes, int32_t* keep_idx, float* fused_opt,
+                                   float* prio_c_opt, void* stream);
 
 /* Static description of a status code (never NULL). */
 E2S_API const char* e2s_status_string(e2s_status status);

@@ -73,6 +73,17 @@ class CompactShape(ctypes.Structure):
                 ("src_stride", ctypes.c_int64 * 3), ("dst_stride", ctypes.c_int64 * 3)]
 
 
+MAX_VIEW_LAYERS = 16
+
+
+class QKViews(ctypes.Structure):
+    """e2s_qk_views: per-layer base pointers and element strides of Q and K."""
+    _fields_ = [("q", ctypes.c_void_p * MAX_VIEW_LAYERS), ("k", ctypes.c_void_p * MAX_VIEW_LAYERS),
+                ("q_stride_image", ctypes.c_int64), ("q_stride_head", ctypes.c_int64),
+                ("q_stride_text", ctypes.c_int64), ("k_stride_image", ctypes.c_int64),
+                ("k_stride_head", ctypes.c_int64), ("k_stride_token", ctypes.c_int64)]
+
+
 class E2SError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
@@ -101,6 +112,7 @@ _SIGNATURES = {
     "e2s_prune_ragged": [ctypes.POINTER(RaggedShape), _PA, _P, _P, _P, _P, _P, ctypes.c_size_t,
                          _P, _P, _P, _P],
     "e2s_compact_tokens": [ctypes.POINTER(CompactShape), _P, _P, _P, _P],
+    "e2s_prune_views": [_SH, _PA, ctypes.POINTER(QKViews), _P, ctypes.c_size_t, _P, _P, _P, _P],
     "e2s_status_string": [ctypes.c_int],
     "e2s_abi_version": [],
 }
@@ -109,7 +121,7 @@ _SIGNATURES = {
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with "
-                          "`python -m paper_2608_23253_amd.build` (or __graft_entry__.build())")
+                          "`python paper_2608_23253_amd/build.py` (or __graft_entry__.build())")
     # Device memory and streams come from torch, whose wheel ships its own HIP
     # runtime (libamdhip64.so, libhsa-runtime64.so).  Load it before the library:
     # the library's libamdhip64.so.7 dependency then binds to that runtime.  Loaded
@@ -158,13 +170,13 @@ def _torch():
     return torch
 
 
-def _check(t, name, dtype=None, ndim=None):
+def _check(t, name, dtype=None, ndim=None, contiguous=True):
     torch = _torch()
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
     if t.device.type != "cuda":
         raise ValueError(f"{name} must be a GPU tensor (got {t.device})")
-    if not t.is_contiguous():
+    if contiguous and not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if dtype is not None and t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype} (got {t.dtype})")
@@ -410,6 +422,53 @@ def prune(q, k, grid_h: int, grid_w: int, keep: int, cells: int = 4, lam: float 
     prio = torch.empty((B, N), device=q.device, dtype=torch.float32) if want_prio else None
     idx = p(q, k, fused, prio)
     return idx, fused, prio
+
+
+def qk_views(q_layers, k_layers) -> QKViews:
+    """e2s_qk_views of per-layer tensors q_layers[l] [B, H, N_T, d] and k_layers[l]
+    [B, Hkv, N, d]: any views (slices of a key/value cache, token-major projection
+    outputs) with the last dimension contiguous and the same strides in every
+    layer.  The tensors must stay alive while the call's kernels run."""
+    if len(q_layers) != len(k_layers) or not 1 <= len(q_layers) <= MAX_VIEW_LAYERS:
+        raise ValueError(f"need 1..{MAX_VIEW_LAYERS} layers of q and of k")
+    v = QKViews()
+    for name, ts in (("q", q_layers), ("k", k_layers)):
+        st = ts[0].stride()
+        for t in ts:
+            _check(t, name, dtype=q_layers[0].dtype, ndim=4, contiguous=False)
+            if t.stride() != st or t.stride(3) != 1 or t.shape != ts[0].shape:
+                raise ValueError(f"{name} views need one shape, one set of strides, and "
+                                 "contiguous rows")
+    for l, (tq, tk) in enumerate(zip(q_layers, k_layers)):
+        v.q[l] = tq.data_ptr()
+        v.k[l] = tk.data_ptr()
+    v.q_stride_image, v.q_stride_head, v.q_stride_text = q_layers[0].stride()[:3]
+    v.k_stride_image, v.k_stride_head, v.k_stride_token = k_layers[0].stride()[:3]
+    return v
+
+
+def prune_views(q_layers, k_layers, grid_h: int, grid_w: int, keep: int, cells: int = 4,
+                lam: float = 0.1, mode="mean_logit", scale: float = 0.0, want_fused=False,
+                want_prio=False, variant="full"):
+    """e2s_prune_views on per-layer views (see qk_views): (keep_idx, fused, prio_c)
+    as from prune() on packed copies."""
+    torch = _torch()
+    q0, k0 = q_layers[0], k_layers[0]
+    B, H, NT, D = q0.shape
+    Hkv, N = k0.shape[1], k0.shape[2]
+    if k0.shape[0] != B or k0.shape[3] != D or N != grid_h * grid_w:
+        raise ValueError("k views do not match q views and the grid")
+    views = qk_views(q_layers, k_layers)
+    shape = make_shape(B, len(q_layers), H, Hkv, D, NT, grid_h, grid_w)
+    params = make_params(_dtype_code(q0), mode, scale, cells, lam, keep, variant)
+    ws = torch.empty(workspace_size(shape, params), device=q0.device, dtype=torch.uint8)
+    out = torch.empty((B, keep), device=q0.device, dtype=torch.int32)
+    fused = torch.empty((B, N, 3), device=q0.device, dtype=torch.float32) if want_fused else None
+    prio = torch.empty((B, N), device=q0.device, dtype=torch.float32) if want_prio else None
+    _raise(_LIB.e2s_prune_views(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(views),
+                                ws.data_ptr(), ws.numel(), out.data_ptr() if keep > 0 else None,
+                                _ptr(fused), _ptr(prio), _stream(q0.device)), "e2s_prune_views")
+    return out, fused, prio
 
 
 class StagePruner:

@@ -1,6 +1,6 @@
 """Build libe2s.so (HIP for gfx950) in-tree with hipcc.
 
-    python -m paper_2608_23253_amd.build [-v]
+    python paper_2608_23253_amd/build.py [-v]
 
 Every translation unit is compiled for gfx950 only, without fast-math, without
 floating-point contraction (every rounding happens as written), and with packed

@@ -22,6 +22,8 @@ struct BatchGeom {
     const e2s_image* images;   // device table (ragged), or null (uniform)
     int L, H, Hkv, D;          // shared by every image
     int NT, N, gh, gw, K;      // the uniform batch's per-image sizes
+    bool has_views;            // Q and K given as per-layer views (uniform batch)
+    e2s_qk_views views;
 };
 
 struct ImageGeom {
@@ -61,6 +63,32 @@ __device__ __forceinline__ ImageGeom image_geom(const BatchGeom& g, int64_t b) {
         r.keep_off = b * g.K;
     }
     return r;
+}
+
+// First element of the rows [N_T, d] of query head h (image b, layer l), and the
+// element stride between consecutive rows: packed blocks, or the caller's views.
+template <typename T>
+__device__ __forceinline__ const T* query_rows(const T* q, const BatchGeom& g, const ImageGeom& ig,
+                                               int64_t b, int l, int h) {
+    if (g.has_views)
+        return static_cast<const T*>(g.views.q[l]) + b * g.views.q_stride_image +
+               h * g.views.q_stride_head;
+    return q + ig.q_off + (static_cast<int64_t>(l) * g.H + h) * ig.NT * g.D;
+}
+__device__ __forceinline__ int64_t query_ld(const BatchGeom& g) {
+    return g.has_views ? g.views.q_stride_text : g.D;
+}
+// The same for the rows [N, d] of key head kv.
+template <typename T>
+__device__ __forceinline__ const T* key_rows(const T* k, const BatchGeom& g, const ImageGeom& ig,
+                                             int64_t b, int l, int kv) {
+    if (g.has_views)
+        return static_cast<const T*>(g.views.k[l]) + b * g.views.k_stride_image +
+               kv * g.views.k_stride_head;
+    return k + ig.k_off + (static_cast<int64_t>(l) * g.Hkv + kv) * ig.N * g.D;
+}
+__device__ __forceinline__ int64_t key_ld(const BatchGeom& g) {
+    return g.has_views ? g.views.k_stride_token : g.D;
 }
 
 }  // namespace e2s

@@ -287,6 +287,28 @@ e2s_status e2s_prune(const e2s_shape* shape, const e2s_params* params, const voi
                          static_cast<hipStream_t>(stream));
 }
 
+e2s_status e2s_prune_views(const e2s_shape* shape, const e2s_params* params,
+                           const e2s_qk_views* views, void* workspace, size_t workspace_bytes,
+                           int32_t* keep_idx, float* fused_opt, float* prio_c_opt, void* stream) {
+    Dims d;
+    E2S_TRY(e2s::check_shape(shape, &d));
+    E2S_TRY(e2s::check_score_params(params));
+    E2S_TRY(e2s::check_views(views, d, params->dtype == E2S_DTYPE_BF16 ? 2 : 4));
+    E2S_TRY(need(workspace));
+    E2S_TRY(e2s::check_aligned(workspace, 256));
+    if (workspace_bytes < e2s::prune_workspace_bytes(d)) return E2S_ERR_WORKSPACE_TOO_SMALL;
+    E2S_TRY(e2s::check_select_params(params, d));
+    if (params->keep > 0) E2S_TRY(need(keep_idx));
+    E2S_TRY(aligned_opt(keep_idx, 4));
+    E2S_TRY(aligned_opt(fused_opt, 4));
+    E2S_TRY(aligned_opt(prio_c_opt, 4));
+    d.views = views;
+    // the kernels read Q and K through the views; the packed pointers are unused
+    return run_operation(d, params, nullptr, nullptr, workspace,
+                         select_args(params, keep_idx, fused_opt, prio_c_opt), nullptr,
+                         static_cast<hipStream_t>(stream));
+}
+
 e2s_status e2s_prune_stage(const e2s_shape* shape, const e2s_params* params, int32_t num_cand,
                            const void* q, const void* k, const int32_t* cand_pos_opt,
                            const float* m_prev_opt, void* workspace, size_t workspace_bytes,

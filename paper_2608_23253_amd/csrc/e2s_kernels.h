@@ -12,16 +12,20 @@ namespace e2s {
 
 // The kernels' view of a validated call's batch (keep: K of a uniform selection).
 inline BatchGeom batch_geom(const Dims& d, int keep = 0) {
-    return BatchGeom{d.images,
-                     static_cast<int>(d.L),
-                     static_cast<int>(d.H),
-                     static_cast<int>(d.Hkv),
-                     static_cast<int>(d.D),
-                     static_cast<int>(d.NT),
-                     static_cast<int>(d.N),
-                     static_cast<int>(d.gh),
-                     static_cast<int>(d.gw),
-                     keep};
+    BatchGeom g{};
+    g.images = d.images;
+    g.L = static_cast<int>(d.L);
+    g.H = static_cast<int>(d.H);
+    g.Hkv = static_cast<int>(d.Hkv);
+    g.D = static_cast<int>(d.D);
+    g.NT = static_cast<int>(d.NT);
+    g.N = static_cast<int>(d.N);
+    g.gh = static_cast<int>(d.gh);
+    g.gw = static_cast<int>(d.gw);
+    g.K = keep;
+    g.has_views = d.views != nullptr;
+    if (d.views) g.views = *d.views;
+    return g;
 }
 
 // Score stage, mean-of-logits reading (Eq. 1 then Eq. 8, 9).

@@ -48,6 +48,33 @@ e2s_status check_shape(const e2s_shape* s, Dims* out) {
     return E2S_OK;
 }
 
+e2s_status check_views(const e2s_qk_views* v, const Dims& d, int elem_bytes) {
+    if (v == nullptr) return E2S_ERR_NULL_POINTER;
+    if (d.L > E2S_MAX_VIEW_LAYERS) return E2S_ERR_UNSUPPORTED;
+    for (int64_t l = 0; l < d.L; ++l) {
+        if (v->q[l] == nullptr || v->k[l] == nullptr) return E2S_ERR_NULL_POINTER;
+        if (check_aligned(v->q[l], 16) != E2S_OK || check_aligned(v->k[l], 16) != E2S_OK)
+            return E2S_ERR_MISALIGNED;
+    }
+    const int64_t strides[6] = {v->q_stride_image, v->q_stride_head, v->q_stride_text,
+                                v->k_stride_image, v->k_stride_head, v->k_stride_token};
+    for (int64_t st : strides) {
+        if (st < 0) return E2S_ERR_BAD_SHAPE;
+        if (st > std::numeric_limits<int64_t>::max() / 64) return E2S_ERR_BAD_SHAPE;
+        if ((st * elem_bytes) % 16 != 0) return E2S_ERR_MISALIGNED;
+    }
+    // element offsets of the last row of each view stay in 63-bit range
+    const double big = static_cast<double>(std::numeric_limits<int64_t>::max() / 16);
+    const double qend = static_cast<double>(d.B) * v->q_stride_image +
+                        static_cast<double>(d.H) * v->q_stride_head +
+                        static_cast<double>(d.NT) * v->q_stride_text;
+    const double kend = static_cast<double>(d.B) * v->k_stride_image +
+                        static_cast<double>(d.Hkv) * v->k_stride_head +
+                        static_cast<double>(d.N) * v->k_stride_token;
+    if (qend > big || kend > big) return E2S_ERR_BAD_SHAPE;
+    return E2S_OK;
+}
+
 namespace {
 // Ranges [start, start + len) of the records with len > 0 must not overlap.
 bool disjoint(std::vector<std::pair<int64_t, int64_t>> r) {

@@ -16,6 +16,9 @@ struct Dims {
     // Ragged batch: the device table of per-image records; NT and N are then the
     // largest N_T,b and N_b (launch sizes), gh and gw unused.  Null: uniform.
     const e2s_image* images = nullptr;
+    // Q and K as per-layer views (host struct, copied into the kernel arguments),
+    // or null (packed arrays).
+    const e2s_qk_views* views = nullptr;
     // Token span of the per-token arrays: B * N (uniform), or the largest
     // token_offset + N_b (ragged); sizes the workspace.
     int64_t tokens = 0;
@@ -31,6 +34,8 @@ constexpr int64_t kMaxCells = 128;
 constexpr int64_t kMaxHeads = 128;     // per-token head supports held in registers
 
 e2s_status check_shape(const e2s_shape* s, Dims* out);
+// Views of Q and K for dtype (element size) and the validated shape.
+e2s_status check_views(const e2s_qk_views* v, const Dims& d, int elem_bytes);
 e2s_status check_score_params(const e2s_params* p);
 e2s_status check_select_params(const e2s_params* p, const Dims& d);
 e2s_status check_aligned(const void* ptr, size_t align);

@@ -69,8 +69,9 @@ __global__ __launch_bounds__(kMaxWaves * kWave) void layer_evidence_kernel(
     const int wave = tid / kWave, lane = tid % kWave, nwaves = nthreads / kWave;
     const int wrow = lane / G::LPR, wl = lane % G::LPR;
     const int nch = (N + CR - 1) / CR, units = H * nch;
-    const T* ql = q + ig.q_off + static_cast<int64_t>(l) * H * NT * D;
-    const T* kl = k + ig.k_off + static_cast<int64_t>(l) * H * N * D + wl * 8;
+    const int64_t qld = query_ld(bg), kld = key_ld(bg);
+    // key rows of head h, offset by this lane's 8 elements (one key head per head)
+    auto key_head = [&](int h) { return key_rows(k, bg, ig, b, l, h) + wl * 8; };
     float* rho_l = rho_out + bg.L * ig.tok + static_cast<int64_t>(l) * N;
     float* pbar_l = pbar_out + bg.L * ig.tok + static_cast<int64_t>(l) * N;
 
@@ -85,14 +86,13 @@ __global__ __launch_bounds__(kMaxWaves * kWave) void layer_evidence_kernel(
     Packet<T> ka[G::KU], kb[G::KU];
     {
         const int uc = min(u, units - 1), h = uc / nch;
-        load_key_batch<T, D>(ka, kl + static_cast<int64_t>(h) * N * D, (uc - h * nch) * CR, wrow,
-                             N);
+        load_key_batch<T, D>(ka, key_head(h), (uc - h * nch) * CR, wrow, N, kld);
     }
 
     // ---- 1. query means ---------------------------------------------------------
     for (int h = wave; h < H; h += nwaves) {
         float qb[8];
-        wave_query_mean<T, D>(ql + static_cast<int64_t>(h) * NT * D + wl * 8, NT, wrow, qscale, qb);
+        wave_query_mean<T, D>(query_rows(q, bg, ig, b, l, h) + wl * 8, NT, wrow, qscale, qb, qld);
         if (wrow == 0) {
 #pragma unroll
             for (int m = 0; m < 8; ++m) qbar[h * D + wl * 8 + m] = qb[m];
@@ -106,18 +106,17 @@ __global__ __launch_bounds__(kMaxWaves * kWave) void layer_evidence_kernel(
         if (lane == 0) un = atomicAdd(&s_next, 1);
         un = wave_uniform(un);
         const int h = u / nch, base = (u - h * nch) * CR;
-        const T* kh = kl + static_cast<int64_t>(h) * N * D;
+        const T* kh = key_head(h);
         float* a = buf + h * N;
         float qb[8];
 #pragma unroll
         for (int m = 0; m < 8; ++m) qb[m] = qbar[h * D + wl * 8 + m];
         const bool second = base + G::BATCH < N;
-        load_key_batch<T, D>(kb, kh, base + G::BATCH, wrow, N);
+        load_key_batch<T, D>(kb, kh, base + G::BATCH, wrow, N, kld);
         key_batch_logits<T, D>(ka, qb, a, base, wrow, wl, N);
         {
             const int uc = min(un, units - 1), hn = uc / nch;
-            load_key_batch<T, D>(ka, kl + static_cast<int64_t>(hn) * N * D, (uc - hn * nch) * CR,
-                                 wrow, N);
+            load_key_batch<T, D>(ka, key_head(hn), (uc - hn * nch) * CR, wrow, N, kld);
         }
         if (second) key_batch_logits<T, D>(kb, qb, a, base + G::BATCH, wrow, wl, N);
 

@@ -87,15 +87,15 @@ __global__ __launch_bounds__(kGroupKernelThreads) void score_group_kernel(
 
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int wrow = lane / G::LPR, wl = lane % G::LPR;
-    const T* kg = k + ig.k_off + static_cast<int64_t>(lkv) * N * D + wl * 8;
-    const T* ql = q + ig.q_off + static_cast<int64_t>(l) * H * NT * D;
+    const T* kg = key_rows(k, bg, ig, b, l, g) + wl * 8;
+    const int64_t qld = query_ld(bg), kld = key_ld(bg);
 
     Packet<T> ka[KU], kb[KU];
-    load_key_batch<T, D>(ka, kg, wave * BATCH, wrow, N);
+    load_key_batch<T, D>(ka, kg, wave * BATCH, wrow, N, kld);
     for (int j = wave; j < nh; j += NW) {
         float qb[8];
-        wave_query_mean<T, D>(ql + static_cast<int64_t>(h0 + j) * NT * D + wl * 8, NT, wrow, qscale,
-                              qb);
+        wave_query_mean<T, D>(query_rows(q, bg, ig, b, l, h0 + j) + wl * 8, NT, wrow, qscale, qb,
+                              qld);
         if (wrow == 0) {
 #pragma unroll
             for (int m = 0; m < 8; ++m) qbar[j * D + wl * 8 + m] = qb[m];
@@ -125,10 +125,10 @@ __global__ __launch_bounds__(kGroupKernelThreads) void score_group_kernel(
     };
     constexpr int STRIDE = NW * BATCH;
     for (int base = wave * BATCH; base < N; base += 2 * STRIDE) {
-        if (base + STRIDE < N) load_key_batch<T, D>(kb, kg, base + STRIDE, wrow, N);
+        if (base + STRIDE < N) load_key_batch<T, D>(kb, kg, base + STRIDE, wrow, N, kld);
         consume(ka, base);
         if (base + STRIDE >= N) break;
-        if (base + 2 * STRIDE < N) load_key_batch<T, D>(ka, kg, base + 2 * STRIDE, wrow, N);
+        if (base + 2 * STRIDE < N) load_key_batch<T, D>(ka, kg, base + 2 * STRIDE, wrow, N, kld);
         consume(kb, base + STRIDE);
     }
     if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
@@ -212,15 +212,15 @@ __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kerne
     float* a = GLOBAL ? e_out + erow + static_cast<int64_t>(h0) * N : qbar + hchunk * D;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int lr = lane % 16, lg = lane / 16;
-    const uint16_t* kg = k + ig.k_off + static_cast<int64_t>(lkv) * N * D + 8 * lg;
-    const uint16_t* ql = q + ig.q_off + static_cast<int64_t>(l) * H * NT * D;
+    const uint16_t* kg = key_rows(k, bg, ig, b, l, g) + 8 * lg;
+    const int64_t qld = query_ld(bg), kld = key_ld(bg);
     const int tiles = (N + 15) / 16;
     const int cnt = wave < tiles ? (tiles - wave + NW - 1) / NW : 0;   // this wave's tiles
 
     bf16x8 kt[P][NS];
     auto load_tile = [&](bf16x8 (&f)[NS], int i) {
         const int row = min((wave + i * NW) * 16 + lr, N - 1);
-        const uint16_t* src = kg + static_cast<int64_t>(row) * D;
+        const uint16_t* src = kg + static_cast<int64_t>(row) * kld;
 #pragma unroll
         for (int s = 0; s < NS; ++s)
             f[s] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(src + 32 * s));
@@ -236,7 +236,7 @@ __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kerne
         for (int j = wave; j < nh; j += NW) {
             float qb[8];
             wave_query_mean<uint16_t, D, kQueryRows>(
-                ql + static_cast<int64_t>(h0 + j) * NT * D + wl * 8, NT, wrow, qscale, qb);
+                query_rows(q, bg, ig, b, l, h0 + j) + wl * 8, NT, wrow, qscale, qb, qld);
             if (wrow == 0) {
 #pragma unroll
                 for (int m = 0; m < 8; ++m) qbar[j * D + wl * 8 + m] = qb[m];
@@ -363,10 +363,10 @@ __global__ __launch_bounds__(kThreads) void score_wave_kernel(
     const int64_t row = bg.L * bg.H * ig.tok + static_cast<int64_t>(lh) * N;
     // logits in LDS, or (GLOBAL) in the head's output row, overwritten in place
     float* a = GLOBAL ? e_out + row : smem + wave * nmax;
-    wave_head<T, D, GLOBAL>(q + ig.q_off + static_cast<int64_t>(lh) * NT * D,
-                    k + ig.k_off + static_cast<int64_t>(lh) * N * D, NT, N,
-                    mean_query_scale(scale, NT), a, lane, e_out + row,
-                    r_out ? r_out + row : nullptr);
+    const int l = lh / bg.H, h = lh - l * bg.H;              // one query head per key head
+    wave_head<T, D, GLOBAL>(query_rows(q, bg, ig, b, l, h), key_rows(k, bg, ig, b, l, h), NT, N,
+                            mean_query_scale(scale, NT), a, lane, e_out + row,
+                            r_out ? r_out + row : nullptr, query_ld(bg), key_ld(bg));
 }
 
 template <typename T, int D>

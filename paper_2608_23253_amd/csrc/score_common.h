@@ -68,15 +68,16 @@ struct WaveRows {
     static constexpr int BATCH = KU * RPW;   // rows per wave-wide batch
 };
 
-// KU key rows base + wrow + u * RPW of one head (kh offset by 8*wl elements);
-// rows past the end are clamped to the last row (in bounds) and discarded later.
+// KU key rows base + wrow + u * RPW of one head (kh offset by 8*wl elements; ld
+// elements from one row to the next); rows past the end are clamped to the last
+// row (in bounds) and discarded later.
 template <typename T, int D, int KU>
 __device__ __forceinline__ void load_key_batch(Packet<T> (&p)[KU], const T* __restrict__ kh,
-                                               int base, int wrow, int N) {
+                                               int base, int wrow, int N, int64_t ld) {
     constexpr int RPW = WaveRows<T, D>::RPW;
 #pragma unroll
     for (int u = 0; u < KU; ++u)
-        load_packet(p[u], kh + static_cast<int64_t>(min(base + wrow + u * RPW, N - 1)) * D);
+        load_packet(p[u], kh + static_cast<int64_t>(min(base + wrow + u * RPW, N - 1)) * ld);
 }
 
 // Logits of one batch: a[n] = qbar . K[n] for the rows of load_key_batch.
@@ -104,18 +105,19 @@ __device__ __forceinline__ float mean_query_scale(float scale, int NT) {
 // Query mean of one head by one wave: lane (wrow, wl) sums rows wrow, wrow + RPW,
 // ... of dims 8*wl .. 8*wl+7 in increasing row order; the RPW row sums are then
 // combined by a butterfly, so every lane holds the same qbar (times qscale).  qh is
-// offset by 8*wl elements.  QU rows per lane are requested at once; the order of the
-// sums, hence the result, does not depend on QU.
+// offset by 8*wl elements; ld elements from one row to the next.  QU rows per lane
+// are requested at once; the order of the sums, hence the result, does not depend
+// on QU.
 template <typename T, int D, int QU = WaveRows<T, D>::KU>
 __device__ __forceinline__ void wave_query_mean(const T* __restrict__ qh, int NT, int wrow,
-                                                float qscale, float (&qb)[8]) {
+                                                float qscale, float (&qb)[8], int64_t ld) {
     constexpr int LPR = WaveRows<T, D>::LPR, RPW = WaveRows<T, D>::RPW;
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     for (int t0 = 0; t0 < NT; t0 += QU * RPW) {
         Packet<T> p[QU];
 #pragma unroll
         for (int u = 0; u < QU; ++u)
-            load_packet(p[u], qh + static_cast<int64_t>(min(t0 + wrow + u * RPW, NT - 1)) * D);
+            load_packet(p[u], qh + static_cast<int64_t>(min(t0 + wrow + u * RPW, NT - 1)) * ld);
 #pragma unroll
         for (int u = 0; u < QU; ++u) {
             float x[8];
@@ -227,22 +229,23 @@ __device__ __forceinline__ void wave_softmax_store(float* a, int N, int lane,
 template <typename T, int D, bool GLOBAL = false>
 __device__ __forceinline__ void wave_head(const T* __restrict__ qh, const T* __restrict__ kh,
                                           int NT, int N, float qscale, float* a, int lane,
-                                          float* __restrict__ eo, float* __restrict__ ro) {
+                                          float* __restrict__ eo, float* __restrict__ ro,
+                                          int64_t qld, int64_t kld) {
     using G = WaveRows<T, D>;
     const int wrow = lane / G::LPR, wl = lane % G::LPR;
     qh += wl * 8;
     kh += wl * 8;
     Packet<T> ka[G::KU], kb[G::KU];
-    load_key_batch<T, D>(ka, kh, 0, wrow, N);
+    load_key_batch<T, D>(ka, kh, 0, wrow, N, kld);
     float qb[8];
-    wave_query_mean<T, D>(qh, NT, wrow, qscale, qb);
+    wave_query_mean<T, D>(qh, NT, wrow, qscale, qb, qld);
     // the requests are unconditional (rows past N are clamped and never used), so
     // the wait before a batch's first use leaves the next batch's loads pending
     for (int base = 0; base < N; base += 2 * G::BATCH) {
-        load_key_batch<T, D>(kb, kh, base + G::BATCH, wrow, N);
+        load_key_batch<T, D>(kb, kh, base + G::BATCH, wrow, N, kld);
         key_batch_logits<T, D>(ka, qb, a, base, wrow, wl, N);
         if (base + G::BATCH >= N) break;
-        load_key_batch<T, D>(ka, kh, base + 2 * G::BATCH, wrow, N);
+        load_key_batch<T, D>(ka, kh, base + 2 * G::BATCH, wrow, N, kld);
         key_batch_logits<T, D>(kb, qb, a, base + G::BATCH, wrow, wl, N);
     }
     if constexpr (GLOBAL) global_logits_sync();

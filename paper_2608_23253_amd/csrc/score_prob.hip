@@ -153,8 +153,9 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
     const int g = h / group;
     const ImageGeom ig = image_geom(bg, b);
     const int NT = ig.NT, N = ig.N;
-    const T* qh = q + ig.q_off + static_cast<int64_t>(lh) * NT * D;
-    const T* kg = k + ig.k_off + static_cast<int64_t>(l * bg.Hkv + g) * N * D;
+    const T* qh = query_rows(q, bg, ig, b, l, h);
+    const T* kg = key_rows(k, bg, ig, b, l, g);
+    const int64_t qld = query_ld(bg), kld = key_ld(bg);
     const int64_t row = bg.L * bg.H * ig.tok + static_cast<int64_t>(lh) * N;
     // [N] column sums: LDS, or (GLOBAL) the head's output row, overwritten at the end
     float* colsum = GLOBAL ? e_out + row : lstat + 3 * qbcap * kThreads;
@@ -182,7 +183,7 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
 #pragma unroll
         for (int tt = 0; tt < TG; ++tt) {
             const int key = tile_of(j, tt) * 16 + lr;
-            load_keys<NA>(a[tt], kg + static_cast<int64_t>(min(key, N - 1)) * D + koff);
+            load_keys<NA>(a[tt], kg + static_cast<int64_t>(min(key, N - 1)) * kld + koff);
         }
     };
 
@@ -216,7 +217,7 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
             const int row = idx / (D / EPV), c = idx % (D / EPV);
             f32x4v v = {0.f, 0.f, 0.f, 0.f};
             if (row < rows)
-                v = *reinterpret_cast<const f32x4v*>(qh + static_cast<int64_t>(t0 + row) * D +
+                v = *reinterpret_cast<const f32x4v*>(qh + static_cast<int64_t>(t0 + row) * qld +
                                                      c * EPV);
             *reinterpret_cast<f32x4v*>(qs + row * QS + c * EPV) = v;
         }
@@ -228,7 +229,7 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
         // N_T get 0
         {
             AFrag a0[NA];
-            load_keys<NA>(a0, kg + static_cast<int64_t>(min(lr, N - 1)) * D + koff);
+            load_keys<NA>(a0, kg + static_cast<int64_t>(min(lr, N - 1)) * kld + koff);
             for (int qb = wave; qb < QB; qb += kWaves) {
                 AFrag bq[NA];
                 load_queries<D>(bq, qs, qb * 16, lr, lg);

@@ -431,8 +431,9 @@ __device__ __forceinline__ void token_positions(int (&posv)[MAXC], const int32_t
 // Dempster fusion across the layers (Eq. 11-19) from per-layer reliability and
 // mean support, then the selection: the tail of a pruning operation after the
 // per-layer evidence.  The per-token arithmetic is that of the staged mass and
-// Dempster kernels.  Each layer's inputs are requested together (and, with up to
-// 4 tokens per thread, before the previous layer is combined).  m_prev, when
+// Dempster kernels.  With up to 2 tokens per thread every layer's inputs are
+// requested at once; with up to 4, each layer's before the previous layer is
+// combined.  m_prev, when
 // given, is the candidates' fused mass from earlier operations: every layer is
 // combined onto it.  The ablation variants change one step each (e2s.h).  For an
 // image of more than 16384 tokens the fusion is recomputed on every visit of a
@@ -458,7 +459,6 @@ __global__ __launch_bounds__(kThreads) void ds_select_kernel(
     float cv[MAXC];
     int posv[MAXC];
     auto load = [&](int n0, int cnt, bool first) {
-        float r[MAXC], e[MAXC];      // current layer's inputs
         float kl[MAXC];
         auto load_layer = [&](int l, float (&rr)[MAXC], float (&ee)[MAXC]) {
             const int64_t base = L * tok + static_cast<int64_t>(l) * N;
@@ -470,39 +470,66 @@ __global__ __launch_bounds__(kThreads) void ds_select_kernel(
                 ee[j] = pbar_c[i];
             }
         };
-        load_layer(l_first, r, e);
+        // the first layer's masses (combined onto the carried mass, if any)
+        auto start = [&](const float (&r)[MAXC], const float (&e)[MAXC]) {
 #pragma unroll
-        for (int j = 0; j < MAXC; ++j) {
-            if (j >= cnt) break;
-            kl[j] = 0.f;
-            if (carried) {
-                const int64_t i = 3 * (tok + n0 + j);
-                aI[j] = m_prev[i];
-                aU[j] = m_prev[i + 1];
-                aT[j] = m_prev[i + 2];
-                float mI, mU, mT;
-                masses_from_reliability(r[j], e[j], mI, mU, mT);
-                kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
-            } else {
-                masses_from_reliability(r[j], e[j], aI[j], aU[j], aT[j]);
+            for (int j = 0; j < MAXC; ++j) {
+                if (j >= cnt) break;
+                kl[j] = 0.f;
+                if (carried) {
+                    const int64_t i = 3 * (tok + n0 + j);
+                    aI[j] = m_prev[i];
+                    aU[j] = m_prev[i + 1];
+                    aT[j] = m_prev[i + 2];
+                    float mI, mU, mT;
+                    masses_from_reliability(r[j], e[j], mI, mU, mT);
+                    kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
+                } else {
+                    masses_from_reliability(r[j], e[j], aI[j], aU[j], aT[j]);
+                }
             }
-        }
-        // with many tokens per thread the prefetch would not fit in registers
-        constexpr bool kPrefetch = MAXC <= 4;
-        if (kPrefetch && l_first + 1 < l_end) load_layer(l_first + 1, r, e);
-        for (int l = l_first + 1; l < l_end; ++l) {
-            float r2[MAXC], e2[MAXC];
-            if (!kPrefetch) load_layer(l, r, e);
-            else if (l + 1 < l_end) load_layer(l + 1, r2, e2);
+        };
+        // one further layer combined (Eq. 13-16)
+        auto step = [&](const float (&r)[MAXC], const float (&e)[MAXC]) {
 #pragma unroll
             for (int j = 0; j < MAXC; ++j) {
                 if (j >= cnt) break;
                 float mI, mU, mT;
                 masses_from_reliability(r[j], e[j], mI, mU, mT);
                 kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
+            }
+        };
+        // With at most two tokens per thread and kAhead layers, every layer's
+        // inputs are requested at once (one memory latency instead of one per
+        // layer); otherwise the next layer's while the current one is combined,
+        // or (many tokens per thread) none ahead.
+        constexpr int kAhead = MAXC <= 2 ? 8 : 0;
+        if (kAhead > 0 && l_end - l_first <= kAhead) {
+            float ra[kAhead > 0 ? kAhead : 1][MAXC], ea[kAhead > 0 ? kAhead : 1][MAXC];
+#pragma unroll
+            for (int t = 0; t < kAhead; ++t)
+                if (l_first + t < l_end) load_layer(l_first + t, ra[t], ea[t]);
+            start(ra[0], ea[0]);
+#pragma unroll
+            for (int t = 1; t < kAhead; ++t)
+                if (l_first + t < l_end) step(ra[t], ea[t]);
+        } else {
+            constexpr bool kPrefetch = MAXC <= 4;
+            float r[MAXC], e[MAXC];
+            load_layer(l_first, r, e);
+            start(r, e);
+            if (kPrefetch && l_first + 1 < l_end) load_layer(l_first + 1, r, e);
+            for (int l = l_first + 1; l < l_end; ++l) {
+                float r2[MAXC], e2[MAXC];
+                if (!kPrefetch) load_layer(l, r, e);
+                else if (l + 1 < l_end) load_layer(l + 1, r2, e2);
+                step(r, e);
                 if (kPrefetch && l + 1 < l_end) {
-                    r[j] = r2[j];
-                    e[j] = e2[j];
+#pragma unroll
+                    for (int j = 0; j < MAXC; ++j) {
+                        r[j] = r2[j];
+                        e[j] = e2[j];
+                    }
                 }
             }
         }

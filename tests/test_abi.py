@@ -67,10 +67,10 @@ def stage(shape, params, ncand, q=A, k=A, pos=A, mprev=None, ws=A, ws_bytes=None
 
 def test_exports_every_declared_entry_point():
     names = L.header_entry_points()
-    assert len(names) == 16
+    assert len(names) == 17
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.e2s_abi_version() == 5
+    assert lib.e2s_abi_version() == 6
 
 
 def test_status_strings():
@@ -327,3 +327,44 @@ def test_compact_rejects_invalid_calls():
     assert compact(dst=None) == L.ERR_NULL_POINTER
     assert compact(K=0, keep=None, src=None, dst=None) == L.OK   # nothing to move
 
+
+
+def good_views(L_=3, q_strides=(3 * 4 * 5 * 64, 5 * 64, 64), k_strides=(3 * 2 * 42 * 64, 42 * 64, 64)):
+    v = L.QKViews()
+    for l in range(L_):
+        v.q[l] = A + l * (1 << 16)
+        v.k[l] = A + (1 << 24) + l * (1 << 16)
+    v.q_stride_image, v.q_stride_head, v.q_stride_text = q_strides
+    v.k_stride_image, v.k_stride_head, v.k_stride_token = k_strides
+    return v
+
+
+def views(shape, params, v, ws=A, ws_bytes=None, out=A):
+    if ws_bytes is None:
+        ws_bytes = L.workspace_size(shape, params)
+    return lib.e2s_prune_views(ctypes.byref(shape), ctypes.byref(params),
+                               ctypes.byref(v) if v is not None else None, ws, ws_bytes, out,
+                               None, None, None)
+
+
+def test_views_validation():
+    sh, pa = good_shape(), good_params()
+    assert views(sh, pa, good_views(), out=None) == L.ERR_NULL_POINTER      # K > 0
+    assert views(sh, pa, None) == L.ERR_NULL_POINTER
+    v = good_views()
+    v.k[2] = None                                                             # layer 2 < L
+    assert views(sh, pa, v) == L.ERR_NULL_POINTER
+    v = good_views()
+    v.q[1] = A + 8                                                            # unaligned base
+    assert views(sh, pa, v) == L.ERR_MISALIGNED
+    v = good_views(q_strides=(3 * 4 * 5 * 64, 5 * 64, 68))                  # 136-byte rows
+    assert views(sh, pa, v) == L.ERR_MISALIGNED
+    v = good_views(k_strides=(-64, 42 * 64, 64))
+    assert views(sh, pa, v) == L.ERR_BAD_SHAPE
+    assert views(good_shape(num_layers=17), pa, good_views(L_=16)) == L.ERR_UNSUPPORTED
+    assert views(sh, pa, good_views(), ws_bytes=1) == L.ERR_WORKSPACE_TOO_SMALL
+    assert views(sh, good_params(cells=7), good_views()) == L.ERR_BAD_PARAM
+    assert views(sh, good_params(mode=2), good_views()) == L.ERR_BAD_PARAM
+    # the packed strides of f32 rows (d = 64: 256 bytes) are accepted by validation
+    v = good_views()
+    assert views(sh, good_params(dtype=L.DTYPE_F32), v, out=None) == L.ERR_NULL_POINTER

@@ -2,9 +2,11 @@
 
 Shapes span several tiles and ragged tails (token counts that are not multiples
 of 16 or 64, query-head groups of 1, 2, 7, 8, 12 and 16, head_dim 64 and 128, fp32
-and bf16 storage, one to eight source layers) and include the largest supported
-grid (128 x 128 = 16384 tokens) and batches with at least one (image, layer) per
-compute unit, where the whole path keeps each layer's supports on chip.  Each stage is checked twice: fed the GPU's own
+and bf16 storage, one to eight source layers) and include the largest grid whose
+selection stays in registers (128 x 128 = 16384 tokens), larger grids up to 40000
+tokens (selection in segments, logits or column sums in the output rows), and
+batches with at least one (image, layer) per compute unit, where the whole path
+keeps each layer's supports on chip.  Each stage is checked twice: fed the GPU's own
 upstream output (isolates that stage's arithmetic) and end to end from Q and K.
 
 Tolerances (absolute + relative to the oracle value), all float32 arithmetic on

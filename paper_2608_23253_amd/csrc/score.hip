@@ -131,9 +131,7 @@ __global__ __launch_bounds__(kGroupKernelThreads) void score_group_kernel(
         if (base + 2 * STRIDE < N) load_key_batch<T, D>(ka, kg, base + 2 * STRIDE, wrow, N, kld);
         consume(kb, base + STRIDE);
     }
-    if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
-    if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
     for (int j = wave; j < nh; j += NW) {
         const int64_t row = erow + static_cast<int64_t>(h0 + j) * N;
@@ -294,9 +292,7 @@ __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kerne
             }
         }
     }
-    if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
-    if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
     // ---- 3. softmax and supports per head ----------------------------------------
     for (int j = wave; j < nh; j += NW) {

@@ -52,11 +52,13 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 // The same for logits kept in global memory (an image whose logits do not fit in
-// LDS): the stores complete and the vector L1 is invalidated before the reads.
+// LDS): workgroup-scope release and acquire order the wave's stores before its
+// later loads of other lanes' values (as a workgroup barrier does for global
+// memory).
 __device__ __forceinline__ void global_logits_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
 // Lane geometry of the per-wave score stage: 8 elements per lane, LPR lanes per

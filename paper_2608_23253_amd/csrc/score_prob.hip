@@ -380,9 +380,7 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
             }
         }
     }
-    if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
     __syncthreads();
-    if constexpr (GLOBAL) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
     const float inv_nt = 1.0f / static_cast<float>(NT);
     for (int n = tid; n < N; n += kThreads) {

@@ -26,7 +26,8 @@
 //     after one barrier every wave scans the histogram itself and takes the same
 //     digit; three histograms in rotation let a round clear the next round's
 //     buffer without a second barrier.  The rounds stop once T's bin holds a
-//     single key;
+//     single key: T is then the one key with the digits chosen so far, and the
+//     compaction compares keys with those high bits only (no search for T);
 //  4. tokens with key < T, plus the lowest-index tokens with key == T, are kept
 //     (Eq. 23); one block-wide scan of the per-thread counts places them in
 //     ascending token order.
@@ -123,7 +124,6 @@ struct SelectShared {
     uint32_t hist[3][256];
     uint32_t scan[kWaves];
     uint64_t wlo[kWaves], whi[kWaves];
-    uint64_t found;
 };
 
 // Token layout of one image's selection.  An image of at most kSegment tokens is
@@ -256,20 +256,21 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], L
         sh.whi[wave] = kmax;
     }
     __syncthreads();
-    uint64_t lo = sh.wlo[0], hi = sh.whi[0];
-#pragma unroll
-    for (int w = 1; w < kWaves; ++w) {
-        lo = sh.wlo[w] < lo ? sh.wlo[w] : lo;
-        hi = sh.whi[w] > hi ? sh.whi[w] : hi;
-    }
+    // the waves' ranges, combined across lanes of every wave at once
+    uint64_t lo = lane < kWaves ? sh.wlo[lane] : ~0ull, hi = lane < kWaves ? sh.whi[lane] : 0ull;
+    wave_minmax_u64(lo, hi);
 
     // ---- radix select of the K-th smallest key (Eq. 23) -----------------------
-    uint64_t T = lo;                        // all keys equal: T = lo, take K of them
+    // The K-th key T is known as (mask, prefix): T & mask == prefix, and no other
+    // key carries that prefix unless mask covers every bit (then T == prefix).  So
+    // a key is below T iff (key & mask) < prefix, and equals T iff
+    // (key & mask) == prefix.  need_eq: how many keys equal to T are taken.
+    uint64_t mask = ~0ull, prefix = lo;     // all keys equal: T = lo, take K of them
     uint32_t need_eq = static_cast<uint32_t>(K);
     if (lo != hi) {
         const int top = 63 - __clzll(static_cast<long long>(lo ^ hi));
-        uint64_t mask = top == 63 ? 0ull : (~0ull << (top + 1));
-        uint64_t prefix = lo & mask;        // bits above top: common to every key
+        mask = top == 63 ? 0ull : (~0ull << (top + 1));
+        prefix = lo & mask;                 // bits above top: common to every key
         uint32_t rank = static_cast<uint32_t>(K);
         int shift = top >= 7 ? top - 7 : 0;
         for (int round = 0;; ++round) {
@@ -324,24 +325,11 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], L
             prefix |= static_cast<uint64_t>(digit) << shift;
             rank -= cum;
             mask |= 0xFFull << shift;
-            if (cnt_d == 1u) {
-                // one key carries this prefix: it is the K-th key
-                for (int s = 0; s < nseg; ++s) {
-                    revisit(s);
-                    const int cnt = count_of(first_of(s));
-#pragma unroll
-                    for (int j = 0; j < MAXC; ++j) {
-                        if (j >= chunk) break;
-                        if (j < cnt && (kk[j] & mask) == prefix) sh.found = kk[j];
-                    }
-                }
-                __syncthreads();
-                T = sh.found;
+            if (cnt_d == 1u) {              // one key carries this prefix: the K-th
                 need_eq = 1u;
                 break;
             }
-            if (shift == 0) {
-                T = prefix;                 // every bit is fixed
+            if (shift == 0) {               // every bit is fixed: T == prefix
                 need_eq = rank;
                 break;
             }
@@ -361,8 +349,8 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], L
         for (int j = 0; j < MAXC; ++j) {
             if (j >= chunk) break;
             if (j < cnt) {
-                lt += kk[j] < T;
-                eq += kk[j] == T;
+                lt += (kk[j] & mask) < prefix;
+                eq += (kk[j] & mask) == prefix;
             }
         }
         const uint32_t packed = (lt << 16) | eq;
@@ -381,10 +369,11 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], L
             if (j >= chunk) break;
             if (j < cnt) {
                 uint32_t pos = static_cast<uint32_t>(K);
-                if (kk[j] < T) {
+                const uint64_t hk = kk[j] & mask;
+                if (hk < prefix) {
                     pos = lt_run + (eq_run < need_eq ? eq_run : need_eq);
                     ++lt_run;
-                } else if (kk[j] == T) {
+                } else if (hk == prefix) {
                     if (eq_run < need_eq) pos = lt_run + eq_run;
                     ++eq_run;
                 }

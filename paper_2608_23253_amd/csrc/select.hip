@@ -154,13 +154,17 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], L
     const int chunk = streamed ? kMaxChunk : (N + kThreads - 1) / kThreads;
     auto first_of = [&](int s) { return min(N, s * kSegment + tid * chunk); };
     auto count_of = [&](int n0) { return max(0, min(N - n0, chunk)); };
-    // the tokens of segment s in the registers (one segment: loaded once)
-    auto visit = [&](int s, bool first) {
-        if (streamed || first) {
-            const int n0 = first_of(s);
-            load(n0, count_of(n0), first);
-        }
+    // the tokens of segment s in the registers: a single segment is loaded once,
+    // before the barrier below (its memory latency overlaps the LDS set-up), the
+    // segments of a larger image on every visit
+    auto load_segment = [&](int s, bool first) {
+        const int n0 = first_of(s);
+        load(n0, count_of(n0), first);
     };
+    auto visit = [&](int s, bool first) {
+        if (streamed) load_segment(s, first);
+    };
+    if (!streamed) load_segment(0, true);
 
     for (int i = tid; i < G * G; i += kThreads) best[i] = ~0ull;
     if (tid < 256) sh.hist[0][tid] = 0u;

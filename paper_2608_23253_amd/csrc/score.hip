@@ -155,28 +155,10 @@ __global__ __launch_bounds__(kGroupKernelThreads) void score_group_kernel(
 // kTilesEarly key tiles already requested), then kTilesInFlight key tiles, a
 // tile's registers being refilled with the tile kTilesInFlight positions ahead as
 // soon as its products are issued.
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int kMfmaMaxChunk = 16;             // query heads per MFMA tile (B columns)
 constexpr int kTilesInFlight = 4;
 constexpr int kTilesEarly = 2;
 constexpr int kQueryRows = 8;
-
-__device__ __forceinline__ uint32_t bf16_bits_rne(float x) {
-    const uint32_t u = __float_as_uint(x);
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-}
-
-// x = hi + mid + lo exactly for finite x of normal range: each residual is exact in
-// fp32 and carries at most 16, then 8, significant bits.
-__device__ __forceinline__ void split_bf16x3(float x, uint16_t& hi, uint16_t& mid, uint16_t& lo) {
-    const uint32_t h = bf16_bits_rne(x);
-    const float r1 = x - __uint_as_float(h << 16);
-    const uint32_t m = bf16_bits_rne(r1);
-    const float r2 = r1 - __uint_as_float(m << 16);
-    hi = static_cast<uint16_t>(h);
-    mid = static_cast<uint16_t>(m);
-    lo = static_cast<uint16_t>(bf16_bits_rne(r2));
-}
 
 // MFMA operand layout (k = 32 per step): lane (lr, lg) = (lane % 16, lane / 16)
 // supplies row lr and elements 8 lg .. 8 lg + 7 of the step, i.e. head dims
@@ -263,22 +245,10 @@ __global__ __launch_bounds__(kGroupKernelThreads, 2) void score_group_mfma_kerne
         for (int p = 0; p < P; ++p) {
             const int i = i0 + p;
             if (i < cnt) {
-                f32x4 ch = {0.f, 0.f, 0.f, 0.f}, cm = ch, co = ch;
-#pragma unroll
-                for (int s = 0; s < NS; ++s) {
-                    const bf16x8 bh = *reinterpret_cast<const bf16x8*>(bq + 32 * s);
-                    const bf16x8 bm = *reinterpret_cast<const bf16x8*>(bq + 16 * BS + 32 * s);
-                    const bf16x8 bo = *reinterpret_cast<const bf16x8*>(bq + 32 * BS + 32 * s);
-                    ch = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[p][s], bh, ch, 0, 0, 0);
-                    cm = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[p][s], bm, cm, 0, 0, 0);
-                    co = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[p][s], bo, co, 0, 0, 0);
-                }
+                const f32x4 z = split_tile_logits<NS>(kt[p], bq, bq + 16 * BS, bq + 32 * BS);
                 if (i + P < cnt) load_tile(kt[p], i + P);
                 // lane (lr, lg): keys 4 lg + r of the tile against head lr
                 const int key0 = (wave + i * NW) * 16 + 4 * lg;
-                f32x4 z;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) z[r] = (co[r] + cm[r]) + ch[r];
                 if (lr < nh) {
                     float* dst = a + static_cast<int64_t>(lr) * N + key0;
                     if (vec_store && key0 + 3 < N) {

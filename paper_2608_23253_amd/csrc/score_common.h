@@ -61,6 +61,57 @@ __device__ __forceinline__ void global_logits_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
+// ---------------------------------------------------------------------------
+// Logits on the matrix cores for grouped-query heads (bf16 keys): the fp32 query
+// means of up to 16 heads are split exactly into three bf16 terms
+// (hi + mid + lo = qbar: each term takes the next 8 significant bits, 24 in all),
+// and a 16-key tile meets the three terms in three fp32 accumulators
+// (v_mfma_f32_16x16x32_bf16), so a logit carries the same information as the
+// fp32 dot product; only the rounding of the sums differs.
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ uint32_t bf16_bits_rne(float x) {
+    const uint32_t u = __float_as_uint(x);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// x = hi + mid + lo exactly for finite x of normal range: each residual is exact in
+// fp32 and carries at most 16, then 8, significant bits.
+__device__ __forceinline__ void split_bf16x3(float x, uint16_t& hi, uint16_t& mid, uint16_t& lo) {
+    const uint32_t h = bf16_bits_rne(x);
+    const float r1 = x - __uint_as_float(h << 16);
+    const uint32_t m = bf16_bits_rne(r1);
+    const float r2 = r1 - __uint_as_float(m << 16);
+    hi = static_cast<uint16_t>(h);
+    mid = static_cast<uint16_t>(m);
+    lo = static_cast<uint16_t>(bf16_bits_rne(r2));
+}
+
+// Logits of one 16-key tile (A operand kt: lane (lr, lg) holds key lr, elements
+// 32 s + 8 lg .. + 7 of step s) against up to 16 heads: bh, bm, bo point at this
+// lane's head lr row of the hi, mid and lo terms (offset by 8 lg elements; a zero
+// row for a column without a head).  Lane (lr, lg) gets the logits of keys
+// 4 lg + r against head lr, summed as (lo + mid) + hi.
+template <int NS>
+__device__ __forceinline__ f32x4 split_tile_logits(const bf16x8 (&kt)[NS], const uint16_t* bh,
+                                                   const uint16_t* bm, const uint16_t* bo) {
+    f32x4 ch = {0.f, 0.f, 0.f, 0.f}, cm = ch, co = ch;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        const bf16x8 vh = *reinterpret_cast<const bf16x8*>(bh + 32 * s);
+        const bf16x8 vm = *reinterpret_cast<const bf16x8*>(bm + 32 * s);
+        const bf16x8 vo = *reinterpret_cast<const bf16x8*>(bo + 32 * s);
+        ch = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[s], vh, ch, 0, 0, 0);
+        cm = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[s], vm, cm, 0, 0, 0);
+        co = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[s], vo, co, 0, 0, 0);
+    }
+    f32x4 z;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) z[r] = (co[r] + cm[r]) + ch[r];
+    return z;
+}
+
 // Lane geometry of the per-wave score stage: 8 elements per lane, LPR lanes per
 // row, RPW rows per wave-wide load, KU rows per lane in flight (16 B per lane per
 // row for bf16, 32 B for fp32).

@@ -15,7 +15,6 @@
 
 namespace e2s {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 
 namespace prob {

@@ -33,6 +33,9 @@ CASES = [
     # batch x layers >= the CU count: the on-chip layer path
     _cfg("layer_path_d128", config_id=91, batch=64, num_layers=4, num_heads=6, num_kv_heads=6,
          head_dim=128, num_text=12, grid_h=9, grid_w=10, keep=25),
+    # grouped-query heads over many workgroups
+    _cfg("gqa4_batch32", config_id=99, batch=32, num_layers=4, num_heads=8, num_kv_heads=2,
+         head_dim=128, num_text=10, grid_h=8, grid_w=12, keep=20),
     _cfg("gqa7_d128", config_id=92, num_heads=14, num_kv_heads=2, head_dim=128, grid_h=11,
          grid_w=7, keep=20),
     _cfg("gqa4_f32", config_id=93, dtype="f32", num_layers=2, num_heads=8, num_kv_heads=2,

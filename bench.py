@@ -335,7 +335,7 @@ def main():
         if cfg.dtype == "bf16":
             bits = synth.to_bf16_bits(x).view(np.int16)
             return torch.from_numpy(bits).cuda().view(torch.bfloat16)
-        return torch.from_numpy(x).cuda()
+        return torch.from_numpy(synth.storage_view(x, cfg.dtype)).cuda()
 
     qd, kd = upload(q_np), upload(k_np)
     torch.cuda.synchronize()

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define E2S_ABI_VERSION 6
+#define E2S_ABI_VERSION 7
 
 #if defined(__GNUC__) || defined(__clang__)
 #define E2S_API __attribute__((visibility("default")))
@@ -66,7 +66,7 @@ typedef enum {
     E2S_ERR_LAUNCH = 7                /* the HIP runtime refused a kernel launch       */
 } e2s_status;
 
-typedef enum { E2S_DTYPE_F32 = 0, E2S_DTYPE_BF16 = 1 } e2s_dtype;
+typedef enum { E2S_DTYPE_F32 = 0, E2S_DTYPE_BF16 = 1, E2S_DTYPE_F16 = 2 } e2s_dtype;
 
 /* The two readings of how the text queries are reduced (Sec. 3.1, Eq. 1 and Eq. 8):
  *  MEAN_LOGIT: a_n = mean_t Q_t.K_n * scale (Eq. 1), r = softmax over n of a (Eq. 8).

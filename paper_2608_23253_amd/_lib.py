@@ -31,7 +31,7 @@ HEADER = os.path.join(os.path.dirname(PKG), "include", "e2s.h")
 # status codes (e2s_status)
 OK, ERR_NULL_POINTER, ERR_BAD_SHAPE, ERR_BAD_PARAM, ERR_UNSUPPORTED, ERR_MISALIGNED, \
     ERR_WORKSPACE_TOO_SMALL, ERR_LAUNCH = range(8)
-DTYPE_F32, DTYPE_BF16 = 0, 1
+DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
 MEAN_LOGIT, MEAN_PROB = 0, 1
 MODES = {"mean_logit": MEAN_LOGIT, "mean_prob": MEAN_PROB}
 # e2s_variant: the full method and the ablation variants A1-A5
@@ -227,7 +227,9 @@ def _dtype_code(t) -> int:
         return DTYPE_BF16
     if t.dtype == torch.float32:
         return DTYPE_F32
-    raise TypeError(f"q/k must be bfloat16 or float32 (got {t.dtype})")
+    if t.dtype == torch.float16:
+        return DTYPE_F16
+    raise TypeError(f"q/k must be bfloat16, float16 or float32 (got {t.dtype})")
 
 
 def score_heads(q, k, grid_h: int, grid_w: int, mode="mean_logit", scale: float = 0.0,

@@ -293,7 +293,7 @@ e2s_status e2s_prune_views(const e2s_shape* shape, const e2s_params* params,
     Dims d;
     E2S_TRY(e2s::check_shape(shape, &d));
     E2S_TRY(e2s::check_score_params(params));
-    E2S_TRY(e2s::check_views(views, d, params->dtype == E2S_DTYPE_BF16 ? 2 : 4));
+    E2S_TRY(e2s::check_views(views, d, params->dtype == E2S_DTYPE_F32 ? 4 : 2));
     E2S_TRY(need(workspace));
     E2S_TRY(e2s::check_aligned(workspace, 256));
     if (workspace_bytes < e2s::prune_workspace_bytes(d)) return E2S_ERR_WORKSPACE_TOO_SMALL;
@@ -353,7 +353,7 @@ e2s_status e2s_prune_ragged(const e2s_ragged_shape* shape, const e2s_params* par
     E2S_TRY(e2s::check_score_params(params));
     Dims d;
     int64_t min_side = 0;
-    const int elem = params->dtype == E2S_DTYPE_BF16 ? 2 : 4;
+    const int elem = params->dtype == E2S_DTYPE_F32 ? 4 : 2;
     E2S_TRY(e2s::check_ragged(shape, images_host, elem, &d, &min_side));
     E2S_TRY(need(images_dev));
     E2S_TRY(need(q));

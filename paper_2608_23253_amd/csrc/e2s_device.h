@@ -19,11 +19,16 @@ __device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w &
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// Element types: uint16_t holds bfloat16 bits, _Float16 is IEEE half, float.
 template <typename T> struct Packet;
 template <> struct Packet<uint16_t> { u32x4 a; };
+template <> struct Packet<_Float16> { u32x4 a; };
 template <> struct Packet<float> { f32x4 a, b; };
 
 __device__ __forceinline__ void load_packet(Packet<uint16_t>& p, const uint16_t* src) {
+    p.a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src));
+}
+__device__ __forceinline__ void load_packet(Packet<_Float16>& p, const _Float16* src) {
     p.a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src));
 }
 __device__ __forceinline__ void load_packet(Packet<float>& p, const float* src) {
@@ -35,6 +40,18 @@ __device__ __forceinline__ void unpack(const Packet<uint16_t>& p, float* x) {
     x[2] = bf16lo(p.a.y); x[3] = bf16hi(p.a.y);
     x[4] = bf16lo(p.a.z); x[5] = bf16hi(p.a.z);
     x[6] = bf16lo(p.a.w); x[7] = bf16hi(p.a.w);
+}
+__device__ __forceinline__ float f16lo(uint32_t w) {
+    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w & 0xFFFFu)));
+}
+__device__ __forceinline__ float f16hi(uint32_t w) {
+    return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(w >> 16)));
+}
+__device__ __forceinline__ void unpack(const Packet<_Float16>& p, float* x) {
+    x[0] = f16lo(p.a.x); x[1] = f16hi(p.a.x);
+    x[2] = f16lo(p.a.y); x[3] = f16hi(p.a.y);
+    x[4] = f16lo(p.a.z); x[5] = f16hi(p.a.z);
+    x[6] = f16lo(p.a.w); x[7] = f16hi(p.a.w);
 }
 __device__ __forceinline__ void unpack(const Packet<float>& p, float* x) {
     x[0] = p.a.x; x[1] = p.a.y; x[2] = p.a.z; x[3] = p.a.w;

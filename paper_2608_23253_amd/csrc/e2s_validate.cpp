@@ -144,7 +144,8 @@ e2s_status check_ragged(const e2s_ragged_shape* s, const e2s_image* images, int 
 
 e2s_status check_score_params(const e2s_params* p) {
     if (p == nullptr) return E2S_ERR_NULL_POINTER;
-    if (p->dtype != E2S_DTYPE_F32 && p->dtype != E2S_DTYPE_BF16) return E2S_ERR_BAD_PARAM;
+    if (p->dtype != E2S_DTYPE_F32 && p->dtype != E2S_DTYPE_BF16 && p->dtype != E2S_DTYPE_F16)
+        return E2S_ERR_BAD_PARAM;
     if (p->mode != E2S_SCORE_MEAN_LOGIT && p->mode != E2S_SCORE_MEAN_PROB)
         return E2S_ERR_BAD_PARAM;
     if (!std::isfinite(p->scale) || p->scale < 0.0f) return E2S_ERR_BAD_PARAM;

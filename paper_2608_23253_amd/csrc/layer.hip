@@ -186,6 +186,10 @@ hipError_t launch_layer_evidence(const Dims& d, int dtype, float scale, const vo
         if (d.D == 128) return launch_layer<uint16_t, 128>(d, scale, q, k, rho, pbar_c, stream);
         return launch_layer<uint16_t, 64>(d, scale, q, k, rho, pbar_c, stream);
     }
+    if (dtype == E2S_DTYPE_F16) {
+        if (d.D == 128) return launch_layer<_Float16, 128>(d, scale, q, k, rho, pbar_c, stream);
+        return launch_layer<_Float16, 64>(d, scale, q, k, rho, pbar_c, stream);
+    }
     if (d.D == 128) return launch_layer<float, 128>(d, scale, q, k, rho, pbar_c, stream);
     return launch_layer<float, 64>(d, scale, q, k, rho, pbar_c, stream);
 }

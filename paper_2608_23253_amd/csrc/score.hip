@@ -398,6 +398,11 @@ hipError_t launch_score_mean_logit(const Dims& d, int dtype, float scale, const 
             return dispatch<uint16_t, 128>(d, scale, q, k, support_c, r_opt, stream);
         return dispatch<uint16_t, 64>(d, scale, q, k, support_c, r_opt, stream);
     }
+    if (dtype == E2S_DTYPE_F16) {
+        if (d.D == 128)
+            return dispatch<_Float16, 128>(d, scale, q, k, support_c, r_opt, stream);
+        return dispatch<_Float16, 64>(d, scale, q, k, support_c, r_opt, stream);
+    }
     if (d.D == 128) return dispatch<float, 128>(d, scale, q, k, support_c, r_opt, stream);
     return dispatch<float, 64>(d, scale, q, k, support_c, r_opt, stream);
 }

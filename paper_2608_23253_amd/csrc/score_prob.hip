@@ -4,8 +4,8 @@
 //
 // Unlike the mean-of-logits reading this is a genuine dense contraction
 // (N_T x N_V logits per head), computed on the matrix cores with
-// v_mfma_f32_16x16x32_bf16 (bf16 storage) or v_mfma_f32_16x16x4_f32 (fp32
-// storage), fp32 accumulation.  One workgroup owns one (image, layer, query head).
+// v_mfma_f32_16x16x32_bf16 / _f16 (bf16 / fp16 storage) or v_mfma_f32_16x16x4_f32
+// (fp32 storage), fp32 accumulation.  One workgroup owns one (image, layer, query head).
 // Its text queries (chunks of up to 128 rows) are staged in LDS as the B operand;
 // key tiles of 16 rows are loaded from HBM straight into A-operand registers, so a
 // 16x16 result tile holds 16 keys (4 per lane) x 16 queries (one per lane).  Two
@@ -69,6 +69,12 @@ template <int D> struct ProbCfg<uint16_t, D> {
     static constexpr int NA = D / 32;        // A registers (bf16x8) per key tile
     using AFrag = bf16x8;
 };
+template <int D> struct ProbCfg<_Float16, D> {
+    static constexpr int QC = 128;
+    static constexpr int QS = D + 8;
+    static constexpr int NA = D / 32;        // A registers (f16x8) per key tile
+    using AFrag = f16x8;
+};
 template <int D> struct ProbCfg<float, D> {
     static constexpr int QC = 64;
     static constexpr int QS = D + 4;
@@ -77,7 +83,7 @@ template <int D> struct ProbCfg<float, D> {
 };
 
 // A operand (keys) of one 16-key tile for all k steps.
-//   bf16: lane (lr, lg) holds key lr, elements 32 s + 8 lg .. +7 of step s.
+//   bf16, fp16: lane (lr, lg) holds key lr, elements 32 s + 8 lg .. +7 of step s.
 //   fp32: lane holds key lr, element d(s, lg) = 16 (s/4) + 4 lg + s%4 of step s.
 // The B operand (queries, from LDS) uses the same element mapping.
 // Loads are unconditional (callers clamp the row into range and discard the
@@ -90,6 +96,11 @@ template <int NS>
 __device__ __forceinline__ void load_keys(bf16x8 (&a)[NS], const uint16_t* row) {
 #pragma unroll
     for (int s = 0; s < NS; ++s) a[s] = *reinterpret_cast<const bf16x8*>(row + 32 * s);
+}
+template <int NS>
+__device__ __forceinline__ void load_keys(f16x8 (&a)[NS], const _Float16* row) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) a[s] = *reinterpret_cast<const f16x8*>(row + 32 * s);
 }
 template <int NS>
 __device__ __forceinline__ void load_keys(float (&a)[NS], const float* row) {
@@ -111,6 +122,13 @@ __device__ __forceinline__ void load_queries(bf16x8 (&b)[D / 32], const uint16_t
     const uint16_t* brow = qs + (qrow + lr) * (D + 8) + 8 * lg;
 #pragma unroll
     for (int s = 0; s < D / 32; ++s) b[s] = *reinterpret_cast<const bf16x8*>(brow + 32 * s);
+}
+template <int D>
+__device__ __forceinline__ void load_queries(f16x8 (&b)[D / 32], const _Float16* qs, int qrow,
+                                             int lr, int lg) {
+    const _Float16* brow = qs + (qrow + lr) * (D + 8) + 8 * lg;
+#pragma unroll
+    for (int s = 0; s < D / 32; ++s) b[s] = *reinterpret_cast<const f16x8*>(brow + 32 * s);
 }
 template <int D>
 __device__ __forceinline__ void load_queries(float (&b)[D / 4], const float* qs, int qrow, int lr,
@@ -438,6 +456,10 @@ hipError_t launch_score_mean_prob(const Dims& d, int dtype, float scale, const v
     if (dtype == E2S_DTYPE_BF16) {
         if (d.D == 128) return dispatch_mp<uint16_t, 128>(d, scale, q, k, support_c, r_opt, stream);
         return dispatch_mp<uint16_t, 64>(d, scale, q, k, support_c, r_opt, stream);
+    }
+    if (dtype == E2S_DTYPE_F16) {
+        if (d.D == 128) return dispatch_mp<_Float16, 128>(d, scale, q, k, support_c, r_opt, stream);
+        return dispatch_mp<_Float16, 64>(d, scale, q, k, support_c, r_opt, stream);
     }
     if (d.D == 128) return dispatch_mp<float, 128>(d, scale, q, k, support_c, r_opt, stream);
     return dispatch_mp<float, 64>(d, scale, q, k, support_c, r_opt, stream);

@@ -16,6 +16,7 @@
 namespace e2s {
 
 typedef float f32x4v __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 namespace prob {
 
@@ -53,6 +54,13 @@ __device__ __forceinline__ f32x4v tile_mma(const bf16x8 (&a)[NA], const bf16x8 (
     f32x4v acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < NA; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s], b[s], acc, 0, 0, 0);
+    return acc;
+}
+template <int NA>
+__device__ __forceinline__ f32x4v tile_mma(const f16x8 (&a)[NA], const f16x8 (&b)[NA]) {
+    f32x4v acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < NA; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[s], b[s], acc, 0, 0, 0);
     return acc;
 }
 template <int NA>

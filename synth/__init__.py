@@ -53,7 +53,7 @@ class Config:
     keep: int                # K of the final top-K
     lambdas: tuple           # novelty weights run on this workload (first = default)
     cells: int = 4           # G: cells per side of the spatial partition
-    dtype: str = "bf16"      # storage type of Q and K: "bf16" or "f32"
+    dtype: str = "bf16"      # storage type of Q and K: "bf16", "f16" or "f32"
     salient_frac: float = 0.05
     salient_count: int = -1  # explicit count (overrides salient_frac when >= 0)
     clusters: int = 3        # 0 = uniformly scattered salient tokens
@@ -81,7 +81,7 @@ class Config:
 
     @property
     def elem_bytes(self) -> int:
-        return 2 if self.dtype == "bf16" else 4
+        return 4 if self.dtype == "f32" else 2
 
     def q_shape(self, batch: int | None = None):
         b = self.batch if batch is None else batch
@@ -158,6 +158,8 @@ def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
 def _round_storage(x: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "bf16":
         return bf16_bits_to_f32(to_bf16_bits(x))
+    if dtype == "f16":
+        return x.astype(np.float16).astype(np.float32)
     return x
 
 
@@ -290,9 +292,12 @@ def gen_batch(cfg: Config, images: Iterable[int] | None = None, threads: int | N
 
 
 def storage_view(x: np.ndarray, dtype: str) -> np.ndarray:
-    """The bits a device buffer should hold: uint16 bf16 bits or the float32 array."""
+    """The bits a device buffer should hold: uint16 bf16 bits, the float16 array or
+    the float32 array."""
     if dtype == "bf16":
         return to_bf16_bits(x)
+    if dtype == "f16":
+        return np.ascontiguousarray(x, dtype=np.float16)
     return np.ascontiguousarray(x, dtype=np.float32)
 
 

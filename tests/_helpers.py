@@ -27,6 +27,8 @@ def to_device(x: np.ndarray, dtype: str):
     if dtype == "bf16":
         bits = synth.to_bf16_bits(x).view(np.int16)
         return torch.from_numpy(bits).cuda().view(torch.bfloat16)
+    if dtype == "f16":
+        return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float16)).cuda()
     return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()
 
 

@@ -70,7 +70,7 @@ def test_exports_every_declared_entry_point():
     assert len(names) == 17
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.e2s_abi_version() == 6
+    assert lib.e2s_abi_version() == 7
 
 
 def test_status_strings():
@@ -104,6 +104,13 @@ def test_large_grids_accepted_and_cells_capped():
     wide = good_shape(grid_h=130, grid_w=130)
     assert select(wide, good_params(cells=128, keep=5), c=None) == L.ERR_NULL_POINTER
     assert select(wide, good_params(cells=129, keep=5)) == L.ERR_UNSUPPORTED
+
+
+def test_fp16_dtype_accepted():
+    """E2S_DTYPE_F16 = 2 passes validation (the call then stops at a missing pointer)."""
+    assert L.DTYPE_F16 == 2
+    assert score(good_shape(), good_params(dtype=L.DTYPE_F16), q=None) == L.ERR_NULL_POINTER
+    assert score(good_shape(), good_params(dtype=3)) == L.ERR_BAD_PARAM
 
 
 @pytest.mark.parametrize("field,value", [

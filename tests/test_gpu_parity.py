@@ -1,8 +1,8 @@
 """GPU parity of every stage against the CPU oracle on small seeded cases.
 
 Shapes span several tiles and ragged tails (token counts that are not multiples
-of 16 or 64, query-head groups of 1, 2, 7, 8, 12 and 16, head_dim 64 and 128, fp32
-and bf16 storage, one to eight source layers) and include the largest grid whose
+of 16 or 64, query-head groups of 1, 2, 4, 7, 8, 12 and 16, head_dim 64 and 128,
+fp32, bf16 and fp16 storage, one to eight source layers) and include the largest grid whose
 selection stays in registers (128 x 128 = 16384 tokens), larger grids up to 40000
 tokens (selection in segments, logits or column sums in the output rows), and
 batches with at least one (image, layer) per compute unit, where the whole path
@@ -89,6 +89,14 @@ CASES = [
     _small("large_f32_gqa_40000", config_id=67, dtype="f32", batch=1, num_layers=1,
            num_heads=4, num_kv_heads=1, num_text=3, grid_h=200, grid_w=200, keep=20000,
            cells=8, salient_count=100, clusters=6),
+    # fp16 storage: per-head kernel, grouped-query vector kernel, the layer path, and
+    # the mean-of-probabilities kernel on v_mfma_f32_16x16x32_f16
+    _small("f16_mha_d128", config_id=40, dtype="f16", num_heads=4, num_kv_heads=4,
+           head_dim=128, num_text=10, grid_h=9, grid_w=11, keep=20),
+    _small("f16_gqa4_d64", config_id=41, dtype="f16", num_heads=12, num_kv_heads=3,
+           num_text=6, grid_h=7, grid_w=10, keep=15, cells=3),
+    _small("f16_layer_path_d64", config_id=42, dtype="f16", batch=64, num_layers=4,
+           num_heads=6, num_kv_heads=6, num_text=5, grid_h=7, grid_w=9, keep=13, cells=3),
     # batch x layers >= the CU count: e2s_prune / e2s_layer_reliability take the
     # on-chip layer path (one workgroup per image and layer)
     _small("layer_path_ragged", config_id=57, batch=64, num_layers=4, num_heads=6,

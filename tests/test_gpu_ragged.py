@@ -9,7 +9,7 @@ kept sets exact or differing only inside the 1e-5 tie window).
 Cases mix grids (ragged tails, a 2x3 grid at G = 2), text lengths (1 to 150, so the
 mean-of-probabilities kernel takes one or two query chunks, 2 or 4 key tiles at a
 time), budgets (0 to N_b), one query head per key head and grouped-query heads
-(groups of 4, 7 and 16), bf16 and fp32 storage, d = 64 and 128, near-uniform and
+(groups of 4, 7 and 16), bf16, fp16 and fp32 storage, d = 64 and 128, near-uniform and
 peaked attention, packed and gapped layouts, and a batch large enough that every
 (image, layer) gets its own workgroup on the on-chip layer path.
 """
@@ -52,6 +52,9 @@ CASES = {
     "gqa8_f32_d64": (_base("gqa8_f32_d64", config_id=74, dtype="f32", num_layers=1,
                            num_heads=8, num_kv_heads=1),
                      [(5, 13, 3, 7), (8, 8, 9, 64), (2, 3, 1, 2)], 2),
+    "gqa4_f16_d128": (_base("gqa4_f16_d128", config_id=44, dtype="f16", num_heads=8,
+                            num_kv_heads=2, head_dim=128),
+                      [(9, 12, 20, 30), (5, 6, 3, 0), (14, 11, 70, 40)], 3),
     "mha_f32_d128": (_base("mha_f32_d128", config_id=75, dtype="f32", num_heads=3,
                            num_kv_heads=3, head_dim=128),
                      [(6, 7, 4, 10), (9, 9, 17, 20)], 3),

@@ -38,6 +38,8 @@ CASES = [
          head_dim=128, num_text=10, grid_h=8, grid_w=12, keep=20),
     _cfg("gqa7_d128", config_id=92, num_heads=14, num_kv_heads=2, head_dim=128, grid_h=11,
          grid_w=7, keep=20),
+    _cfg("f16_gqa2", config_id=43, dtype="f16", num_heads=6, num_kv_heads=3, head_dim=128,
+         num_text=9, keep=12),
     _cfg("gqa4_f32", config_id=93, dtype="f32", num_layers=2, num_heads=8, num_kv_heads=2,
          num_text=5, keep=9),
     # 25600 tokens: logits in the output rows, selection in segments

@@ -83,6 +83,10 @@ typedef struct {
     int32_t grid_h;        /* visual grid rows >= 1                    */
     int32_t grid_w;        /* visual grid cols >= 1; N = grid_h*grid_w <= 2^20  */
 } e2s_shape;
+/* Launch limits (E2S_ERR_UNSUPPORTED beyond them, for every entry point that takes
+ * an e2s_shape or e2s_image records): B*L*H < 2^22 and B*L*ceil(N/64) < 2^24, N
+ * being the largest image's token count; each keeps a kernel grid under 2^32
+ * work-items. */
 
 /* The full method and the ablation variants of the paper's ablation study (Sec. 5,
  * Table 2), each removing or replacing one component.  Honoured by e2s_prune and

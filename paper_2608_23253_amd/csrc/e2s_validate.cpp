@@ -14,6 +14,13 @@ e2s_status check_aligned(const void* ptr, size_t align) {
     return (reinterpret_cast<uintptr_t>(ptr) % align) == 0 ? E2S_OK : E2S_ERR_MISALIGNED;
 }
 
+// A grid may hold fewer than 2^32 work-items.  The kernels launch at most 1024
+// threads per (image, layer, head) unit and 256 per (image, layer, 64-token tile);
+// blh and bl_tiles count those units.
+static bool grids_fit(double blh, double bl_tiles) {
+    return blh * 1024.0 < 4294967296.0 && bl_tiles * 256.0 < 4294967296.0;
+}
+
 e2s_status check_shape(const e2s_shape* s, Dims* out) {
     if (s == nullptr) return E2S_ERR_NULL_POINTER;
     if (s->batch < 1 || s->num_layers < 1 || s->num_heads < 1 || s->num_kv_heads < 1 ||
@@ -34,15 +41,15 @@ e2s_status check_shape(const e2s_shape* s, Dims* out) {
     if (d.N > kMaxVisual) return E2S_ERR_UNSUPPORTED;
     if (d.H > kMaxHeads) return E2S_ERR_UNSUPPORTED;
     if (d.D != 64 && d.D != 128) return E2S_ERR_UNSUPPORTED;
-    // Every tensor of the call must be indexable with 63-bit element offsets and
-    // the grids must stay below 2^31 workgroups.
+    // Every tensor of the call must be indexable with 63-bit element offsets.
     const double big = static_cast<double>(std::numeric_limits<int64_t>::max() / 16);
     const double qel = static_cast<double>(d.B) * d.L * d.H * d.NT * d.D;
     const double kel = static_cast<double>(d.B) * d.L * d.Hkv * d.N * d.D;
     const double eel = static_cast<double>(d.B) * d.L * d.H * d.N;
     if (qel > big || kel > big || eel > big) return E2S_ERR_BAD_SHAPE;
-    if (static_cast<double>(d.B) * d.L * d.H > 2147483647.0) return E2S_ERR_BAD_SHAPE;
-    if (static_cast<double>(d.B) * d.N > 2147483647.0) return E2S_ERR_BAD_SHAPE;
+    if (!grids_fit(static_cast<double>(d.B) * d.L * d.H,
+                   static_cast<double>(d.B) * d.L * ((d.N + 63) / 64)))
+        return E2S_ERR_UNSUPPORTED;
     d.tokens = d.B * d.N;
     if (out) *out = d;
     return E2S_OK;
@@ -131,9 +138,9 @@ e2s_status check_ragged(const e2s_ragged_shape* s, const e2s_image* images, int 
         if (im.keep > 0) keeps.emplace_back(im.keep_offset, im.keep);
     }
     if (!disjoint(toks) || !disjoint(keeps)) return E2S_ERR_BAD_SHAPE;
-    if (static_cast<double>(d.B) * d.L * d.H > 2147483647.0) return E2S_ERR_BAD_SHAPE;
-    if (static_cast<double>(d.B) * d.L * ((n_max + 63) / 64) > 2147483647.0)
-        return E2S_ERR_BAD_SHAPE;
+    if (!grids_fit(static_cast<double>(d.B) * d.L * d.H,
+                   static_cast<double>(d.B) * d.L * ((n_max + 63) / 64)))
+        return E2S_ERR_UNSUPPORTED;
     d.NT = nt_max;
     d.N = n_max;
     d.tokens = span;

@@ -106,6 +106,24 @@ def test_large_grids_accepted_and_cells_capped():
     assert select(wide, good_params(cells=129, keep=5)) == L.ERR_UNSUPPORTED
 
 
+def test_grid_limits():
+    """Every kernel grid stays under 2^32 work-items: B*L*H < 2^22 and
+    B*L*ceil(N/64) < 2^24, else E2S_ERR_UNSUPPORTED before any launch."""
+    at = good_shape(batch=(1 << 22) // 128 - 1, num_layers=4, num_heads=32, num_kv_heads=32,
+                    grid_h=2, grid_w=2)                           # B*L*H = 2^22 - 128
+    assert score(at, good_params(keep=1), q=None) == L.ERR_NULL_POINTER
+    over = good_shape(batch=(1 << 22) // 128, num_layers=4, num_heads=32, num_kv_heads=32,
+                      grid_h=2, grid_w=2)                         # B*L*H = 2^22
+    assert score(over, good_params(keep=1)) == L.ERR_UNSUPPORTED
+    assert prune(over, good_params(keep=1), ws_bytes=0) == L.ERR_UNSUPPORTED
+    tokens = good_shape(batch=1 << 14, num_layers=1, num_heads=1, num_kv_heads=1,
+                        grid_h=1024, grid_w=64)                   # B*L*N/64 = 2^24
+    assert score(tokens, good_params(keep=1)) == L.ERR_UNSUPPORTED
+    fits = good_shape(batch=(1 << 14) - 1, num_layers=1, num_heads=1, num_kv_heads=1,
+                      grid_h=1024, grid_w=64)
+    assert score(fits, good_params(keep=1), q=None) == L.ERR_NULL_POINTER
+
+
 def test_fp16_dtype_accepted():
     """E2S_DTYPE_F16 = 2 passes validation (the call then stops at a missing pointer)."""
     assert L.DTYPE_F16 == 2

@@ -149,7 +149,8 @@ __device__ __forceinline__ void load_queries(float (&b)[D / 4], const float* qs,
 template <typename T, int D, int TG, bool GLOBAL>
 __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_kernel(
     const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
-    float* __restrict__ r_out, BatchGeom bg, int group, float scale, int nblocks, int qcap) {
+    float* __restrict__ r_out, BatchGeom bg, int group, float scale, int nblocks, int qcap,
+    bool cols_over_stats) {
     using C = ProbCfg<T, D>;
     constexpr int QS = C::QS, NA = C::NA;
     using AFrag = typename C::AFrag;
@@ -175,8 +176,12 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
     const T* kg = key_rows(k, bg, ig, b, l, g);
     const int64_t qld = query_ld(bg), kld = key_ld(bg);
     const int64_t row = bg.L * bg.H * ig.tok + static_cast<int64_t>(lh) * N;
-    // [N] column sums: LDS, or (GLOBAL) the head's output row, overwritten at the end
-    float* colsum = GLOBAL ? e_out + row : lstat + 3 * qbcap * kThreads;
+    // [N] column sums: LDS, or (GLOBAL) the head's output row, overwritten at the
+    // end.  cols_over_stats: every head has one query chunk and the sums fit in the
+    // per-lane statistics, which are dead once pass 1 has been merged, so the sums
+    // take their place (less LDS per workgroup, more workgroups per CU).
+    float* colsum = GLOBAL ? e_out + row
+                           : (cols_over_stats ? lstat : lstat + 3 * qbcap * kThreads);
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const int lr = lane % 16, lg = lane / 16;
     // Key tiles of 16 rows go to the waves round-robin (wave w: tiles w, w + 4,
@@ -222,9 +227,6 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
         }
     };
 
-    if constexpr (!GLOBAL)
-        for (int n = tid; n < N; n += kThreads) colsum[n] = 0.f;
-
     for (int t0 = 0; t0 < NT; t0 += qcap) {
         const int rows = min(qcap, NT - t0);
         const int QB = (rows + 15) / 16;
@@ -262,7 +264,7 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
         const ScaledSeries<5> p5(scale);
         const ScaledSeries<6> p6(scale);
         float amax = 0.f;                                         // largest |y| seen
-        stream_groups([&](const AFrag (&a)[TG][NA], int j) {
+        auto pass1_group = [&](const AFrag (&a)[TG][NA], int j, auto whole) {
             for (int qb = 0; qb < QB; ++qb) {
                 AFrag bq[NA];
                 load_queries<D>(bq, qs, qb * 16, lr, lg);
@@ -270,10 +272,19 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
                 float E = lE[qb * kThreads];
 #pragma unroll
                 for (int tt = 0; tt < TG; ++tt)
-                    prob::series_tile(tile_mma<NA>(a[tt], bq), cz, tile_of(j, tt) * 16 + 4 * lg,
-                                      N, p5, E, amax);
+                    prob::series_tile<decltype(whole)::value>(tile_mma<NA>(a[tt], bq), cz,
+                                                              tile_of(j, tt) * 16 + 4 * lg, N,
+                                                              p5, E, amax);
                 lE[qb * kThreads] = E;
             }
+        };
+        stream_groups([&](const AFrag (&a)[TG][NA], int j) {
+            // the group's last tile ends at or before N: no key of the group is masked
+            // (tile_of is the same for every lane of the wave)
+            if (__builtin_amdgcn_readfirstlane(tile_of(j, TG - 1)) * 16 + 16 <= N)
+                pass1_group(a, j, std::true_type{});
+            else
+                pass1_group(a, j, std::false_type{});
         });
         // |s y| <= 1/8 everywhere keeps the series within its range
         if (!(wave_max(amax) * scale <= kSeriesRange) && lane == 0) atomicOr(&s_far, 1);
@@ -350,10 +361,10 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
             for (int i = 0; i < TG * 4; ++i) {
                 const float sum = group_sum<16>(col[i]);
                 const int key = tile_of(j, i / 4) * 16 + 4 * lg + i % 4;
-                // a key's sums are kept by one lane through every chunk; in global
-                // memory its first chunk starts the sum, as the zeroed LDS does
+                // a key's sums are kept by one lane through every chunk, the first
+                // chunk starting them (every key below N is written then)
                 if (lr == 0 && key < N) {
-                    const float prev = (GLOBAL && t0 == 0) ? 0.f : colsum[key];
+                    const float prev = (t0 == 0) ? 0.f : colsum[key];
                     colsum[key] = prev + unit * sum;
                 }
             }
@@ -412,11 +423,14 @@ template <typename T, int D, int TG>
 hipError_t launch_mp(const Dims& d, float scale, const void* q, const void* k, float* e,
                      float* r, int qcap, hipStream_t st) {
     using C = ProbCfg<T, D>;
-    // the column sums in LDS up to kColumnsInLds keys, else in the output rows
+    // the column sums in LDS up to kColumnsInLds keys, else in the output rows; in
+    // the statistics' place when every head has one query chunk and they fit
     const bool global = d.N > kColumnsInLds;
+    const int64_t stats = 3 * (qcap / 16) * kThreads;            // floats
+    const bool over = !global && d.NT <= qcap && d.N <= stats;
     const size_t lds = static_cast<size_t>(qcap) * C::QS * sizeof(T) +
-                       (2 * qcap + kWaves * qcap * 4 + 3 * (qcap / 16) * kThreads) * sizeof(float) +
-                       (global ? 0 : static_cast<size_t>(d.N) * sizeof(float));
+                       (2 * qcap + kWaves * qcap * 4 + stats) * sizeof(float) +
+                       (global || over ? 0 : static_cast<size_t>(d.N) * sizeof(float));
     auto kern = global ? score_mean_prob_kernel<T, D, TG, true>
                        : score_mean_prob_kernel<T, D, TG, false>;
     if (lds > 64 * 1024) {
@@ -429,7 +443,7 @@ hipError_t launch_mp(const Dims& d, float scale, const void* q, const void* k, f
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), lds, st,
                        static_cast<const T*>(q), static_cast<const T*>(k), e, r,
                        batch_geom(d), static_cast<int>(d.group), scale,
-                       static_cast<int>(blocks), qcap);
+                       static_cast<int>(blocks), qcap, over);
     return hipGetLastError();
 }
 

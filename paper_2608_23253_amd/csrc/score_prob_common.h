@@ -85,10 +85,13 @@ __device__ __forceinline__ float block_reference(const f32x4v& z, int N, int lr)
 
 // Pass 1, near uniform: E += expm1(s y) = s y P5(y) (in units of s) for the
 // tile's logits with y = z - c_t / s; keys past N count as y = 0.  amax: the
-// largest |y| seen, to confirm afterwards that |s y| <= 1/8 held.
+// largest |y| seen, to confirm afterwards that |s y| <= 1/8 held.  WHOLE: the
+// caller knows that every key of the tile is below N (the same arithmetic without
+// the masking).
+template <bool WHOLE>
 __device__ __forceinline__ void series_tile(const f32x4v& z, float cz, int key0, int N,
                                             const ScaledSeries<5>& p5, float& E, float& amax) {
-    const bool full = key0 + 4 <= N;
+    const bool full = WHOLE || key0 + 4 <= N;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         float y = z[r] - cz;

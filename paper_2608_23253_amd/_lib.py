@@ -188,8 +188,22 @@ def _ptr(t) -> Optional[int]:
     return None if t is None else t.data_ptr()
 
 
-def _stream(device=None) -> int:
-    return _torch().cuda.current_stream(device).cuda_stream
+def _device_of(*tensors):
+    """The one device of the given tensors (None entries skipped)."""
+    devs = {t.device for t in tensors if t is not None}
+    if len(devs) != 1:
+        raise ValueError(f"all tensors of a call must be on one GPU (got {sorted(map(str, devs))})")
+    return devs.pop()
+
+
+def _launch(where: str, tensors, fn, *args, stream=None):
+    """fn(*args, stream) with the tensors' device current (kernels are launched on
+    that device), on its current stream unless one is given; raises on a status."""
+    torch = _torch()
+    dev = _device_of(*tensors)
+    with torch.cuda.device(dev):
+        st = torch.cuda.current_stream(dev).cuda_stream if stream is None else stream
+        _raise(fn(*args, st), where)
 
 
 def _raise(status: int, where: str):
@@ -244,8 +258,8 @@ def score_heads(q, k, grid_h: int, grid_w: int, mode="mean_logit", scale: float 
     e = torch.empty((sh.batch, sh.num_layers, sh.num_heads, n), device=q.device,
                     dtype=torch.float32)
     r = torch.empty_like(e) if want_r else None
-    _raise(_LIB.e2s_score_heads(ctypes.byref(sh), ctypes.byref(pa), q.data_ptr(), k.data_ptr(),
-                                e.data_ptr(), _ptr(r), _stream(q.device)), "e2s_score_heads")
+    _launch("e2s_score_heads", (q, k, e, r), _LIB.e2s_score_heads, ctypes.byref(sh),
+            ctypes.byref(pa), q.data_ptr(), k.data_ptr(), e.data_ptr(), _ptr(r))
     return e, r
 
 
@@ -265,9 +279,8 @@ def head_reliability(support_c, grid_h: int, grid_w: int):
     B, L, H, N = support_c.shape
     rho = torch.empty((B, L, N), device=support_c.device, dtype=torch.float32)
     pbar = torch.empty_like(rho)
-    _raise(_LIB.e2s_head_reliability(ctypes.byref(sh), support_c.data_ptr(), rho.data_ptr(),
-                                     pbar.data_ptr(), _stream(support_c.device)),
-           "e2s_head_reliability")
+    _launch("e2s_head_reliability", (support_c,), _LIB.e2s_head_reliability, ctypes.byref(sh),
+            support_c.data_ptr(), rho.data_ptr(), pbar.data_ptr())
     return rho, pbar
 
 
@@ -279,8 +292,8 @@ def head_masses(rho, pbar_c, grid_h: int, grid_w: int):
     B, L, N = rho.shape
     sh = make_shape(B, L, 1, 1, 128, 1, grid_h, grid_w)
     mass = torch.empty((B, L, N, 3), device=rho.device, dtype=torch.float32)
-    _raise(_LIB.e2s_head_masses(ctypes.byref(sh), rho.data_ptr(), pbar_c.data_ptr(),
-                                mass.data_ptr(), _stream(rho.device)), "e2s_head_masses")
+    _launch("e2s_head_masses", (rho, pbar_c), _LIB.e2s_head_masses, ctypes.byref(sh),
+            rho.data_ptr(), pbar_c.data_ptr(), mass.data_ptr())
     return mass
 
 
@@ -294,9 +307,8 @@ def ds_combine_layers(mass, grid_h: int, grid_w: int, want_fused=True, want_conf
     fused = torch.empty((B, N, 3), device=dev, dtype=torch.float32) if want_fused else None
     conflict = torch.empty((B, L, N), device=dev, dtype=torch.float32) if want_conflict else None
     prio = torch.empty((B, N), device=dev, dtype=torch.float32)
-    _raise(_LIB.e2s_ds_combine_layers(ctypes.byref(sh), mass.data_ptr(), _ptr(fused),
-                                      _ptr(conflict), prio.data_ptr(), _stream(dev)),
-           "e2s_ds_combine_layers")
+    _launch("e2s_ds_combine_layers", (mass,), _LIB.e2s_ds_combine_layers, ctypes.byref(sh),
+            mass.data_ptr(), _ptr(fused), _ptr(conflict), prio.data_ptr())
     return fused, conflict, prio
 
 
@@ -310,9 +322,8 @@ def fuse_evidence(support_c, grid_h: int, grid_w: int, want_fused=True, want_con
     fused = torch.empty((B, N, 3), device=dev, dtype=torch.float32) if want_fused else None
     conflict = torch.empty((B, L, N), device=dev, dtype=torch.float32) if want_conflict else None
     prio = torch.empty((B, N), device=dev, dtype=torch.float32)
-    _raise(_LIB.e2s_fuse_evidence(ctypes.byref(sh), support_c.data_ptr(), _ptr(fused),
-                                  _ptr(conflict), prio.data_ptr(), _stream(dev)),
-           "e2s_fuse_evidence")
+    _launch("e2s_fuse_evidence", (support_c,), _LIB.e2s_fuse_evidence, ctypes.byref(sh),
+            support_c.data_ptr(), _ptr(fused), _ptr(conflict), prio.data_ptr())
     return fused, conflict, prio
 
 
@@ -328,9 +339,9 @@ def spatial_select(prio_c, grid_h: int, grid_w: int, keep: int, cells: int = 4,
     out = torch.empty((B, keep), device=dev, dtype=torch.int32)
     adj = torch.empty((B, N), device=dev, dtype=torch.float64) if want_adj else None
     rep = torch.empty((B, N), device=dev, dtype=torch.uint8) if want_rep else None
-    _raise(_LIB.e2s_spatial_select(ctypes.byref(sh), ctypes.byref(pa), prio_c.data_ptr(),
-                                   out.data_ptr() if keep > 0 else None, _ptr(adj), _ptr(rep),
-                                   _stream(dev)), "e2s_spatial_select")
+    _launch("e2s_spatial_select", (prio_c,), _LIB.e2s_spatial_select, ctypes.byref(sh),
+            ctypes.byref(pa), prio_c.data_ptr(), out.data_ptr() if keep > 0 else None,
+            _ptr(adj), _ptr(rep))
     return out, adj, rep
 
 
@@ -348,10 +359,9 @@ def layer_reliability(q, k, grid_h: int, grid_w: int, mode="mean_logit", scale: 
     B, L, N = sh.batch, sh.num_layers, grid_h * grid_w
     rho = torch.empty((B, L, N), device=q.device, dtype=torch.float32)
     pbar = torch.empty_like(rho)
-    _raise(_LIB.e2s_layer_reliability(ctypes.byref(sh), ctypes.byref(pa), q.data_ptr(),
-                                      k.data_ptr(), workspace.data_ptr(), workspace.numel(),
-                                      rho.data_ptr(), pbar.data_ptr(), _stream(q.device)),
-           "e2s_layer_reliability")
+    _launch("e2s_layer_reliability", (q, k, workspace), _LIB.e2s_layer_reliability,
+            ctypes.byref(sh), ctypes.byref(pa), q.data_ptr(), k.data_ptr(), workspace.data_ptr(),
+            workspace.numel(), rho.data_ptr(), pbar.data_ptr())
     return rho, pbar
 
 
@@ -368,9 +378,9 @@ def fuse_select(rho, pbar_c, grid_h: int, grid_w: int, keep: int, cells: int = 4
     out = torch.empty((B, keep), device=dev, dtype=torch.int32)
     fused = torch.empty((B, N, 3), device=dev, dtype=torch.float32) if want_fused else None
     prio = torch.empty((B, N), device=dev, dtype=torch.float32) if want_prio else None
-    _raise(_LIB.e2s_fuse_select(ctypes.byref(sh), ctypes.byref(pa), rho.data_ptr(),
-                                pbar_c.data_ptr(), out.data_ptr() if keep > 0 else None,
-                                _ptr(fused), _ptr(prio), _stream(dev)), "e2s_fuse_select")
+    _launch("e2s_fuse_select", (rho, pbar_c), _LIB.e2s_fuse_select, ctypes.byref(sh),
+            ctypes.byref(pa), rho.data_ptr(), pbar_c.data_ptr(),
+            out.data_ptr() if keep > 0 else None, _ptr(fused), _ptr(prio))
     return out, fused, prio
 
 
@@ -405,11 +415,11 @@ class Pruner:
             raise ValueError("k does not match the Pruner's shape")
         if q.dtype != k.dtype or _dtype_code(q) != self.params.dtype:
             raise TypeError("q/k dtype does not match the Pruner's")
-        st = _stream(self.device) if stream is None else stream
-        _raise(_LIB.e2s_prune(ctypes.byref(self.shape), ctypes.byref(self.params), q.data_ptr(),
-                              k.data_ptr(), self.workspace.data_ptr(), self.workspace.numel(),
-                              self.keep_idx.data_ptr() if self.params.keep > 0 else None,
-                              _ptr(fused), _ptr(prio_c), st), "e2s_prune")
+        _launch("e2s_prune", (q, k, fused, prio_c, self.workspace), _LIB.e2s_prune,
+                ctypes.byref(self.shape), ctypes.byref(self.params), q.data_ptr(), k.data_ptr(),
+                self.workspace.data_ptr(), self.workspace.numel(),
+                self.keep_idx.data_ptr() if self.params.keep > 0 else None, _ptr(fused),
+                _ptr(prio_c), stream=stream)
         return self.keep_idx
 
 
@@ -467,9 +477,9 @@ def prune_views(q_layers, k_layers, grid_h: int, grid_w: int, keep: int, cells: 
     out = torch.empty((B, keep), device=q0.device, dtype=torch.int32)
     fused = torch.empty((B, N, 3), device=q0.device, dtype=torch.float32) if want_fused else None
     prio = torch.empty((B, N), device=q0.device, dtype=torch.float32) if want_prio else None
-    _raise(_LIB.e2s_prune_views(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(views),
-                                ws.data_ptr(), ws.numel(), out.data_ptr() if keep > 0 else None,
-                                _ptr(fused), _ptr(prio), _stream(q0.device)), "e2s_prune_views")
+    _launch("e2s_prune_views", (*q_layers, *k_layers), _LIB.e2s_prune_views, ctypes.byref(shape),
+            ctypes.byref(params), ctypes.byref(views), ws.data_ptr(), ws.numel(),
+            out.data_ptr() if keep > 0 else None, _ptr(fused), _ptr(prio))
     return out, fused, prio
 
 
@@ -515,15 +525,13 @@ class StagePruner:
             _check(m_prev, "m_prev", dtype=torch.float32, ndim=3)
             if tuple(m_prev.shape) != (B, N, 3):
                 raise ValueError("m_prev must be [B, num_cand, 3]")
-        st = _stream(self.device) if stream is None else stream
         K = self.params.keep
-        _raise(_LIB.e2s_prune_stage(ctypes.byref(self.shape), ctypes.byref(self.params), N,
-                                    q.data_ptr(), k.data_ptr(), _ptr(cand_pos), _ptr(m_prev),
-                                    self.workspace.data_ptr(), self.workspace.numel(),
-                                    self.keep_idx.data_ptr() if K > 0 else None,
-                                    self.keep_pos.data_ptr() if K > 0 else None,
-                                    self.m_out.data_ptr() if K > 0 else None, st),
-               "e2s_prune_stage")
+        _launch("e2s_prune_stage", (q, k, cand_pos, m_prev, self.workspace), _LIB.e2s_prune_stage,
+                ctypes.byref(self.shape), ctypes.byref(self.params), N, q.data_ptr(), k.data_ptr(),
+                _ptr(cand_pos), _ptr(m_prev), self.workspace.data_ptr(), self.workspace.numel(),
+                self.keep_idx.data_ptr() if K > 0 else None,
+                self.keep_pos.data_ptr() if K > 0 else None,
+                self.m_out.data_ptr() if K > 0 else None, stream=stream)
         return self.keep_idx, self.keep_pos, self.m_out
 
 
@@ -600,13 +608,12 @@ class RaggedPruner:
                 _check(t, name, dtype=torch.float32)
                 if t.numel() < n:
                     raise ValueError(f"{name} holds fewer than {n} values")
-        st = _stream(self.device) if stream is None else stream
-        _raise(_LIB.e2s_prune_ragged(ctypes.byref(self.shape), ctypes.byref(self.params),
-                                     ctypes.addressof(self.images), self.images_dev.data_ptr(),
-                                     q.data_ptr(), k.data_ptr(), self.workspace.data_ptr(),
-                                     self.workspace.numel(),
-                                     self.keep_idx.data_ptr() if self.kept > 0 else None,
-                                     _ptr(fused), _ptr(prio_c), st), "e2s_prune_ragged")
+        _launch("e2s_prune_ragged", (q, k, fused, prio_c, self.workspace), _LIB.e2s_prune_ragged,
+                ctypes.byref(self.shape), ctypes.byref(self.params),
+                ctypes.addressof(self.images), self.images_dev.data_ptr(), q.data_ptr(),
+                k.data_ptr(), self.workspace.data_ptr(), self.workspace.numel(),
+                self.keep_idx.data_ptr() if self.kept > 0 else None, _ptr(fused), _ptr(prio_c),
+                stream=stream)
         return self.keep_idx
 
 
@@ -653,7 +660,7 @@ def compact_tokens(src, keep_idx, out=None):
     sh = CompactShape(B, R, N, K, C, src.element_size(),
                       (ctypes.c_int64 * 3)(*src.stride()[:3]),
                       (ctypes.c_int64 * 3)(*out.stride()[:3]))
-    _raise(_LIB.e2s_compact_tokens(ctypes.byref(sh), keep_idx.data_ptr(), src.data_ptr(),
-                                   out.data_ptr(), _stream(src.device)), "e2s_compact_tokens")
+    _launch("e2s_compact_tokens", (keep_idx, src), _LIB.e2s_compact_tokens, ctypes.byref(sh),
+            keep_idx.data_ptr(), src.data_ptr(), out.data_ptr())
     return out
 

@@ -1,6 +1,7 @@
 // extern "C" entry points of libe2s.so (declared and documented in include/e2s.h).
 // Each call validates every argument on the host before it touches the HIP
 // runtime, then enqueues its kernels on the caller's stream.
+#include <atomic>
 #include <cmath>
 
 #include "e2s.h"
@@ -58,15 +59,17 @@ e2s_status run_score(const Dims& d, const e2s_params* params, const void* q, con
 
 // Compute units of the current device (cached per device).
 int device_cus() {
-    static int cached[64] = {0};
+    // calls may come from several host threads; every writer stores the same value
+    static std::atomic<int> cached[64];
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-    if (cached[dev] == 0) {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess)
-            cached[dev] = n;
+    int n = cached[dev].load(std::memory_order_relaxed);
+    if (n == 0) {
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        cached[dev].store(n, std::memory_order_relaxed);
     }
-    return cached[dev];
+    return n;
 }
 
 // Eq. 1, 8-10: per-layer rho and pbar_c, on chip when a layer fits and there are

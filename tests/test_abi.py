@@ -216,6 +216,22 @@ def test_binding_rejects_cpu_tensors():
         L.score_heads(q, q, 1, 1)
 
 
+def test_binding_requires_one_device():
+    """Every tensor of a call must live on one GPU; the call then runs with that GPU
+    current (checked on stand-in objects: no GPU is touched)."""
+    torch = pytest.importorskip("torch")
+
+    class T:
+        def __init__(self, dev):
+            self.device = torch.device(dev)
+
+    assert L._device_of(T("cuda:1"), None, T("cuda:1")) == torch.device("cuda:1")
+    with pytest.raises(ValueError):
+        L._device_of(T("cuda:0"), T("cuda:1"))
+    with pytest.raises(ValueError):
+        L._device_of(None)
+
+
 @pytest.mark.parametrize("variant", [-1, 6])
 def test_bad_variant(variant):
     assert prune(good_shape(), good_params(variant=variant)) == L.ERR_BAD_PARAM

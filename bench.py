@@ -35,8 +35,11 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "layer_evidence_llava_traffic.txt")
 # the sources of the score and reliability stage: a counter summary taken on other
 # versions of them is not used
-STAGE_SOURCES = ("layer.hip", "score.hip", "score_prob.hip", "score_common.h",
-                 "score_prob_common.h", "batch_geom.h", "fuse.hip", "e2s_device.h")
+# The sources compiled into the kernel whose counters the traffic summary holds
+# (layer_evidence_kernel: the score and reliability stage of the mean-of-logits
+# reading at the LLaVA shape); the summary is used only while they are unchanged.
+STAGE_SOURCES = ("layer.hip", "score_common.h", "batch_geom.h", "e2s_device.h", "e2s_kernels.h")
+TRAFFIC_WORKLOAD = "llava"
 
 
 def log(*a):
@@ -70,10 +73,11 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def read_traffic(mode: str):
+def read_traffic(mode: str, workload: str):
     """HBM bytes per launch of the score and reliability stage from the committed
-    counter summary, or None when it is missing or was taken on other sources."""
-    if not os.path.exists(TRAFFIC_FILE):
+    counter summary, or None when it is missing, covers another workload or reading,
+    or was taken on other sources."""
+    if workload != TRAFFIC_WORKLOAD or not os.path.exists(TRAFFIC_FILE):
         return None
     vals = {}
     with open(TRAFFIC_FILE) as f:
@@ -432,7 +436,7 @@ def main():
     algo_bytes = B * per_img_qk + 2 * 4 * B * L_ * N
     lr_ms = float(t_lr.mean())
     achieved = algo_bytes / (lr_ms * 1e-3) / 1e9
-    traffic = read_traffic(args.mode)
+    traffic = read_traffic(args.mode, args.workload)
     flops_eq1 = 2.0 * B * L_ * H_ * cfg.num_text * N * cfg.head_dim
     log(f"[bench] layer_reliability {lr_ms * 1e3:.1f} us (p10 {np.percentile(t_lr, 10) * 1e3:.1f},"
         f" p90 {np.percentile(t_lr, 90) * 1e3:.1f}) {achieved:.0f} GB/s; fuse_select "

@@ -25,7 +25,10 @@
  *    below.  q and k must be 16-byte aligned, float/int outputs 4-byte aligned,
  *    double outputs 8-byte aligned.  Outputs must not overlap inputs or each other.
  *  - The library is stateless and reentrant; calls on different streams may
- *    run concurrently.  There is no global error state.
+ *    run concurrently when they share no workspace and no output.  There is no
+ *    global error state.
+ *  - The kernels run on the current HIP device; every pointer of a call must be
+ *    memory of that device and `stream` one of its streams.
  *  - Centred quantities: the support p is exported as e = p - 1/2 and the
  *    retention priority q as c = 1 - q (Eq. 19 rewritten with Eq. 18 as
  *    c = m~(U) * (1 - K)).  Near the uniform-attention point p = 1/2 and q = 1,

@@ -116,7 +116,10 @@ e2s_status run_operation(const Dims& d, const e2s_params* params, const void* q,
     float* pbar_c =
         reinterpret_cast<float*>(ws + e2s::support_region_bytes(d) + e2s::layer_region_bytes(d));
     E2S_TRY(run_layer_reliability(d, params, q, k, workspace, rho, pbar_c, st));
-    return from_hip(e2s::launch_ds_select(d, a, rho, pbar_c, m_prev, st));
+    // the supports region is free again (the reliability stage has read it) and
+    // lends the selection room for its device-wide fusion when it is large enough
+    const bool room = e2s::support_region_bytes(d) >= static_cast<size_t>(d.tokens) * 16;
+    return from_hip(e2s::launch_ds_select(d, a, rho, pbar_c, m_prev, room ? ws : nullptr, st));
 }
 
 e2s_status check_score_inputs(const e2s_shape* shape, const e2s_params* params, const void* q,
@@ -271,7 +274,8 @@ e2s_status e2s_fuse_select(const e2s_shape* shape, const e2s_params* params, con
     E2S_TRY(aligned_opt(prio_c_opt, 4));
     if (params->variant == E2S_VARIANT_ATTENTION_TOPK) return E2S_ERR_UNSUPPORTED;
     return from_hip(e2s::launch_ds_select(d, select_args(params, keep_idx, fused_opt, prio_c_opt),
-                                          rho, pbar_c, nullptr, static_cast<hipStream_t>(stream)));
+                                          rho, pbar_c, nullptr, nullptr,
+                                          static_cast<hipStream_t>(stream)));
 }
 
 e2s_status e2s_prune(const e2s_shape* shape, const e2s_params* params, const void* q,

@@ -134,15 +134,19 @@ __device__ __forceinline__ void masses_from_reliability(float rho, float ebar, f
 }
 
 // One Dempster step (Eq. 13-16) of the running mass (aI, aU, aT) with (mI, mU, mT).
-// Returns K; on total conflict the running mass becomes vacuous and K = 1.
+// Returns K; on total conflict the running mass becomes vacuous and K = 1.  The
+// three normalisations share one correctly rounded reciprocal of 1 - K (one
+// division sequence instead of three; each mass then carries at most two
+// roundings from it).
 __device__ __forceinline__ float ds_step(float& aI, float& aU, float& aT, float mI, float mU,
                                          float mT) {
     const float k = aI * mU + aU * mI;
     const float den = 1.0f - k;
     if (den > 0.0f) {
-        const float fI = (aI * mI + aI * mT + aT * mI) / den;
-        const float fU = (aU * mU + aU * mT + aT * mU) / den;
-        const float fT = (aT * mT) / den;
+        const float inv = 1.0f / den;
+        const float fI = (aI * mI + aI * mT + aT * mI) * inv;
+        const float fU = (aU * mU + aU * mT + aT * mU) * inv;
+        const float fT = (aT * mT) * inv;
         aI = fI;
         aU = fU;
         aT = fT;

@@ -75,8 +75,12 @@ struct SelectArgs {
     float* prio_c;             // [B, N] c = 1 - q, or null
 };
 // Eq. 11-19 from rho, pbar_c (onto m_prev [B, N, 3] when given), then Eq. 20-23.
+// fuse_scratch: null, or 16-byte aligned device memory of d.tokens x 16 bytes that
+// the call may use to run the fusion device-wide before the per-image selection
+// (for images of more than 2048 tokens; the results are the same either way).
 hipError_t launch_ds_select(const Dims& d, const SelectArgs& a, const float* rho,
-                            const float* pbar_c, const float* m_prev, hipStream_t stream);
+                            const float* pbar_c, const float* m_prev, void* fuse_scratch,
+                            hipStream_t stream);
 // Attention top-K (ablation A1) from the supports [B, L, H, N].
 hipError_t launch_attention_select(const Dims& d, const SelectArgs& a, const float* support_c,
                                    hipStream_t stream);

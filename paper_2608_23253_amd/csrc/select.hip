@@ -421,125 +421,188 @@ __device__ __forceinline__ void token_positions(int (&posv)[MAXC], const int32_t
         posv[j] = cand_pos ? (j < cnt ? cand_pos[tok + n0 + j] : -1) : n0 + j;
 }
 
+// How an operation fuses its layers (Eq. 11-19); the ablation variants change one
+// step each (e2s.h).  m_prev, when given, is the candidates' fused mass from
+// earlier operations: every layer is combined onto it.
+struct FusionPlan {
+    bool unit_rho;   // rho = 1 (no head reliability)
+    bool carried;    // combine onto m_prev
+    bool protect;    // Eq. 19's conflict factor
+    int l_first, l_end;
+};
+__device__ __forceinline__ FusionPlan fusion_plan(const SelectArgs& a, const float* m_prev, int L) {
+    const bool last_only = a.variant == E2S_VARIANT_NO_LAYER_FUSION;
+    FusionPlan f;
+    f.unit_rho = a.variant == E2S_VARIANT_NO_HEAD_RELIABILITY;
+    f.carried = m_prev != nullptr && !last_only;
+    f.protect = a.variant != E2S_VARIANT_NO_CONFLICT;
+    f.l_first = last_only ? L - 1 : 0;
+    f.l_end = L;
+    return f;
+}
+
+// Eq. 11-19 for the tokens n0 .. n0 + cnt - 1 (cnt <= MAXC) of the image whose
+// tokens start at `tok`: the fused masses (aI, aU, aT) and the conflict kl of the
+// last combination (0 when nothing was combined), from the per-layer rho and
+// pbar_c.  The per-token arithmetic is that of the staged mass and Dempster
+// kernels and does not depend on MAXC.  With up to 2 tokens per call every
+// layer's inputs are requested at once; with up to 4, each layer's before the
+// previous layer is combined.
+template <int MAXC>
+__device__ __forceinline__ void fuse_tokens(const float* __restrict__ rho,
+                                            const float* __restrict__ pbar_c,
+                                            const float* __restrict__ m_prev, const FusionPlan& f,
+                                            int L, int64_t tok, int N, int n0, int cnt,
+                                            float (&aI)[MAXC], float (&aU)[MAXC],
+                                            float (&aT)[MAXC], float (&kl)[MAXC]) {
+    const int l_first = f.l_first, l_end = f.l_end;
+    auto load_layer = [&](int l, float (&rr)[MAXC], float (&ee)[MAXC]) {
+        const int64_t base = L * tok + static_cast<int64_t>(l) * N;
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= cnt) break;
+            const int64_t i = base + n0 + j;
+            rr[j] = f.unit_rho ? 1.0f : rho[i];
+            ee[j] = pbar_c[i];
+        }
+    };
+    // the first layer's masses (combined onto the carried mass, if any)
+    auto start = [&](const float (&r)[MAXC], const float (&e)[MAXC]) {
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= cnt) break;
+            kl[j] = 0.f;
+            if (f.carried) {
+                const int64_t i = 3 * (tok + n0 + j);
+                aI[j] = m_prev[i];
+                aU[j] = m_prev[i + 1];
+                aT[j] = m_prev[i + 2];
+                float mI, mU, mT;
+                masses_from_reliability(r[j], e[j], mI, mU, mT);
+                kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
+            } else {
+                masses_from_reliability(r[j], e[j], aI[j], aU[j], aT[j]);
+            }
+        }
+    };
+    // one further layer combined (Eq. 13-16)
+    auto step = [&](const float (&r)[MAXC], const float (&e)[MAXC]) {
+#pragma unroll
+        for (int j = 0; j < MAXC; ++j) {
+            if (j >= cnt) break;
+            float mI, mU, mT;
+            masses_from_reliability(r[j], e[j], mI, mU, mT);
+            kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
+        }
+    };
+    constexpr int kAhead = MAXC <= 2 ? 8 : 0;
+    if (kAhead > 0 && l_end - l_first <= kAhead) {
+        float ra[kAhead > 0 ? kAhead : 1][MAXC], ea[kAhead > 0 ? kAhead : 1][MAXC];
+#pragma unroll
+        for (int t = 0; t < kAhead; ++t)
+            if (l_first + t < l_end) load_layer(l_first + t, ra[t], ea[t]);
+        start(ra[0], ea[0]);
+#pragma unroll
+        for (int t = 1; t < kAhead; ++t)
+            if (l_first + t < l_end) step(ra[t], ea[t]);
+    } else {
+        constexpr bool kPrefetch = MAXC <= 4;
+        float r[MAXC], e[MAXC];
+        load_layer(l_first, r, e);
+        start(r, e);
+        if (kPrefetch && l_first + 1 < l_end) load_layer(l_first + 1, r, e);
+        for (int l = l_first + 1; l < l_end; ++l) {
+            float r2[MAXC], e2[MAXC];
+            if (!kPrefetch) load_layer(l, r, e);
+            else if (l + 1 < l_end) load_layer(l + 1, r2, e2);
+            step(r, e);
+            if (kPrefetch && l + 1 < l_end) {
+#pragma unroll
+                for (int j = 0; j < MAXC; ++j) {
+                    r[j] = r2[j];
+                    e[j] = e2[j];
+                }
+            }
+        }
+    }
+}
+
+// The fused masses and c of one token into the optional per-token outputs.
+__device__ __forceinline__ void write_fused(const SelectArgs& a, int64_t i, float aI, float aU,
+                                            float aT, float c) {
+    if (a.fused) {
+        a.fused[3 * i + 0] = aI;
+        a.fused[3 * i + 1] = aU;
+        a.fused[3 * i + 2] = aT;
+    }
+    if (a.prio_c) a.prio_c[i] = c;
+}
+
+// Eq. 11-19 for every token of the batch, one token per thread, ahead of the
+// selection: pre[token] = (aI, aU, aT, kl), plus the optional per-token outputs.
+// Used for images of more than 2048 tokens, where the per-image selection
+// workgroup would otherwise do this work for four or more tokens per thread on one
+// CU.  The values are those fuse_tokens gives inside the selection kernel.
+constexpr int kFuseThreads = 256;
+__global__ __launch_bounds__(kFuseThreads) void ds_fuse_kernel(
+    const float* __restrict__ rho, const float* __restrict__ pbar_c,
+    const float* __restrict__ m_prev, SelectArgs a, BatchGeom bg, f32x4* __restrict__ pre,
+    int tiles) {
+    const int64_t b = blockIdx.x / tiles;
+    const int n = static_cast<int>(blockIdx.x - b * tiles) * kFuseThreads + threadIdx.x;
+    const ImageGeom ig = image_geom(bg, b);
+    if (n >= ig.N) return;
+    const FusionPlan f = fusion_plan(a, m_prev, bg.L);
+    float aI[1], aU[1], aT[1], kl[1];
+    fuse_tokens<1>(rho, pbar_c, m_prev, f, bg.L, ig.tok, ig.N, n, 1, aI, aU, aT, kl);
+    const int64_t i = ig.tok + n;
+    f32x4 v = {aI[0], aU[0], aT[0], kl[0]};
+    pre[i] = v;
+    write_fused(a, i, aI[0], aU[0], aT[0], priority_complement(aU[0], f.protect ? kl[0] : 0.0f));
+}
+
 // Dempster fusion across the layers (Eq. 11-19) from per-layer reliability and
-// mean support, then the selection: the tail of a pruning operation after the
-// per-layer evidence.  The per-token arithmetic is that of the staged mass and
-// Dempster kernels.  With up to 2 tokens per thread every layer's inputs are
-// requested at once; with up to 4, each layer's before the previous layer is
-// combined.  m_prev, when
-// given, is the candidates' fused mass from earlier operations: every layer is
-// combined onto it.  The ablation variants change one step each (e2s.h).  For an
-// image of more than 16384 tokens the fusion is recomputed on every visit of a
-// segment (the same arithmetic, so the same values).
+// mean support (fuse_tokens), or its results from ds_fuse_kernel when `pre` is
+// given, then the selection: the tail of a pruning operation after the per-layer
+// evidence.  For an image of more than 16384 tokens the fusion is recomputed (or
+// reread) on every visit of a segment (the same arithmetic, so the same values).
 template <int MAXC>
 __global__ __launch_bounds__(kThreads) void ds_select_kernel(
     const float* __restrict__ rho, const float* __restrict__ pbar_c,
-    const float* __restrict__ m_prev, SelectArgs a, BatchGeom bg) {
+    const float* __restrict__ m_prev, const f32x4* __restrict__ pre, SelectArgs a,
+    BatchGeom bg) {
     extern __shared__ uint64_t best[];
     __shared__ SelectShared sh;
     const int64_t b = blockIdx.x;
     const ImageGeom ig = image_geom(bg, b);
     const int L = bg.L, N = ig.N, gh = ig.gh, gw = ig.gw, K = ig.K;
     const int64_t tok = ig.tok;
-    const bool unit_rho = a.variant == E2S_VARIANT_NO_HEAD_RELIABILITY;
-    const bool last_only = a.variant == E2S_VARIANT_NO_LAYER_FUSION;
-    const bool carried = m_prev != nullptr && !last_only;
-    const bool protect = a.variant != E2S_VARIANT_NO_CONFLICT;
-    const int l_first = last_only ? L - 1 : 0;          // first layer read
-    const int l_end = last_only ? l_first + 1 : L;
+    const FusionPlan f = fusion_plan(a, m_prev, L);
 
     float aI[MAXC], aU[MAXC], aT[MAXC];
     float cv[MAXC];
     int posv[MAXC];
     auto load = [&](int n0, int cnt, bool first) {
         float kl[MAXC];
-        auto load_layer = [&](int l, float (&rr)[MAXC], float (&ee)[MAXC]) {
-            const int64_t base = L * tok + static_cast<int64_t>(l) * N;
+        if (pre) {
 #pragma unroll
             for (int j = 0; j < MAXC; ++j) {
                 if (j >= cnt) break;
-                const int64_t i = base + n0 + j;
-                rr[j] = unit_rho ? 1.0f : rho[i];
-                ee[j] = pbar_c[i];
+                const f32x4 v = pre[tok + n0 + j];
+                aI[j] = v.x;
+                aU[j] = v.y;
+                aT[j] = v.z;
+                kl[j] = v.w;
             }
-        };
-        // the first layer's masses (combined onto the carried mass, if any)
-        auto start = [&](const float (&r)[MAXC], const float (&e)[MAXC]) {
-#pragma unroll
-            for (int j = 0; j < MAXC; ++j) {
-                if (j >= cnt) break;
-                kl[j] = 0.f;
-                if (carried) {
-                    const int64_t i = 3 * (tok + n0 + j);
-                    aI[j] = m_prev[i];
-                    aU[j] = m_prev[i + 1];
-                    aT[j] = m_prev[i + 2];
-                    float mI, mU, mT;
-                    masses_from_reliability(r[j], e[j], mI, mU, mT);
-                    kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
-                } else {
-                    masses_from_reliability(r[j], e[j], aI[j], aU[j], aT[j]);
-                }
-            }
-        };
-        // one further layer combined (Eq. 13-16)
-        auto step = [&](const float (&r)[MAXC], const float (&e)[MAXC]) {
-#pragma unroll
-            for (int j = 0; j < MAXC; ++j) {
-                if (j >= cnt) break;
-                float mI, mU, mT;
-                masses_from_reliability(r[j], e[j], mI, mU, mT);
-                kl[j] = ds_step(aI[j], aU[j], aT[j], mI, mU, mT);
-            }
-        };
-        // With at most two tokens per thread and kAhead layers, every layer's
-        // inputs are requested at once (one memory latency instead of one per
-        // layer); otherwise the next layer's while the current one is combined,
-        // or (many tokens per thread) none ahead.
-        constexpr int kAhead = MAXC <= 2 ? 8 : 0;
-        if (kAhead > 0 && l_end - l_first <= kAhead) {
-            float ra[kAhead > 0 ? kAhead : 1][MAXC], ea[kAhead > 0 ? kAhead : 1][MAXC];
-#pragma unroll
-            for (int t = 0; t < kAhead; ++t)
-                if (l_first + t < l_end) load_layer(l_first + t, ra[t], ea[t]);
-            start(ra[0], ea[0]);
-#pragma unroll
-            for (int t = 1; t < kAhead; ++t)
-                if (l_first + t < l_end) step(ra[t], ea[t]);
         } else {
-            constexpr bool kPrefetch = MAXC <= 4;
-            float r[MAXC], e[MAXC];
-            load_layer(l_first, r, e);
-            start(r, e);
-            if (kPrefetch && l_first + 1 < l_end) load_layer(l_first + 1, r, e);
-            for (int l = l_first + 1; l < l_end; ++l) {
-                float r2[MAXC], e2[MAXC];
-                if (!kPrefetch) load_layer(l, r, e);
-                else if (l + 1 < l_end) load_layer(l + 1, r2, e2);
-                step(r, e);
-                if (kPrefetch && l + 1 < l_end) {
-#pragma unroll
-                    for (int j = 0; j < MAXC; ++j) {
-                        r[j] = r2[j];
-                        e[j] = e2[j];
-                    }
-                }
-            }
+            fuse_tokens<MAXC>(rho, pbar_c, m_prev, f, L, tok, N, n0, cnt, aI, aU, aT, kl);
         }
         token_positions<MAXC>(posv, a.cand_pos, tok, n0, cnt);
 #pragma unroll
         for (int j = 0; j < MAXC; ++j) {
             if (j >= cnt) break;
-            cv[j] = priority_complement(aU[j], protect ? kl[j] : 0.0f);
-            if (first) {
-                const int64_t i = tok + n0 + j;
-                if (a.fused) {
-                    a.fused[3 * i + 0] = aI[j];
-                    a.fused[3 * i + 1] = aU[j];
-                    a.fused[3 * i + 2] = aT[j];
-                }
-                if (a.prio_c) a.prio_c[i] = cv[j];
-            }
+            cv[j] = priority_complement(aU[j], f.protect ? kl[j] : 0.0f);
+            if (first && !pre) write_fused(a, tok + n0 + j, aI[j], aU[j], aT[j], cv[j]);
         }
     };
     select_image<MAXC>(cv, posv, load, best, sh, tok, nullptr, nullptr, N, gh, gw, a.cells,
@@ -612,13 +675,22 @@ hipError_t allow_lds(Kern kern, size_t lds) {
 
 template <int MAXC>
 hipError_t launch_dssel(const Dims& d, const SelectArgs& a, const float* rho, const float* pbar_c,
-                        const float* m_prev, hipStream_t st) {
+                        const float* m_prev, f32x4* pre, hipStream_t st) {
     const size_t lds = static_cast<size_t>(a.cells) * a.cells * sizeof(uint64_t);
     auto kern = ds_select_kernel<MAXC>;
     hipError_t err = allow_lds(kern, lds);
     if (err != hipSuccess) return err;
+    const BatchGeom bg = batch_geom(d, a.keep);
+    if (pre) {
+        const int64_t tiles = (d.N + kFuseThreads - 1) / kFuseThreads;
+        hipLaunchKernelGGL(ds_fuse_kernel, dim3(static_cast<unsigned>(d.B * tiles)),
+                           dim3(kFuseThreads), 0, st, rho, pbar_c, m_prev, a, bg, pre,
+                           static_cast<int>(tiles));
+        err = hipGetLastError();
+        if (err != hipSuccess) return err;
+    }
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(kThreads), lds, st, rho, pbar_c,
-                       m_prev, a, batch_geom(d, a.keep));
+                       m_prev, static_cast<const f32x4*>(pre), a, bg);
     return hipGetLastError();
 }
 
@@ -656,13 +728,18 @@ int chunk_class(const Dims& d) {
 }  // namespace
 
 hipError_t launch_ds_select(const Dims& d, const SelectArgs& a, const float* rho,
-                            const float* pbar_c, const float* m_prev, hipStream_t st) {
-    switch (chunk_class(d)) {
-        case 1: return launch_dssel<1>(d, a, rho, pbar_c, m_prev, st);
-        case 2: return launch_dssel<2>(d, a, rho, pbar_c, m_prev, st);
-        case 4: return launch_dssel<4>(d, a, rho, pbar_c, m_prev, st);
-        case 8: return launch_dssel<8>(d, a, rho, pbar_c, m_prev, st);
-        default: return launch_dssel<kMaxChunk>(d, a, rho, pbar_c, m_prev, st);
+                            const float* pbar_c, const float* m_prev, void* fuse_scratch,
+                            hipStream_t st) {
+    // four or more tokens per thread: the fusion runs device-wide first when the
+    // caller lends room for it (d.tokens x 16 bytes)
+    const int cc = chunk_class(d);
+    f32x4* pre = cc >= 4 ? static_cast<f32x4*>(fuse_scratch) : nullptr;
+    switch (cc) {
+        case 1: return launch_dssel<1>(d, a, rho, pbar_c, m_prev, nullptr, st);
+        case 2: return launch_dssel<2>(d, a, rho, pbar_c, m_prev, nullptr, st);
+        case 4: return launch_dssel<4>(d, a, rho, pbar_c, m_prev, pre, st);
+        case 8: return launch_dssel<8>(d, a, rho, pbar_c, m_prev, pre, st);
+        default: return launch_dssel<kMaxChunk>(d, a, rho, pbar_c, m_prev, pre, st);
     }
 }
 

@@ -1,8 +1,8 @@
-// Spatial novelty and global top-K (Sec. 4.3 Eq. 20-23), one workgroup of 1024
-// threads per image.
+// Spatial novelty and global top-K (Sec. 4.3 Eq. 20-23), one workgroup per image:
+// one thread per token (in whole waves) up to 1024 tokens, 1024 threads above.
 //
 // Thread t owns the consecutive tokens n0 = t * chunk .. n0 + chunk - 1
-// (chunk = ceil(N / 1024), one token for N <= 1024) and keeps their values in
+// (chunk = ceil(N / 1024) above 1024 tokens, else one token) and keeps their values in
 // registers throughout.  The work per image is a few KB, so the kernel is bound
 // by latency: every step below is shaped to need few dependent LDS round trips
 // and workgroup barriers.  An image of more than 16384 tokens is taken in
@@ -128,7 +128,7 @@ struct SelectShared {
 
 // Token layout of one image's selection.  An image of at most kSegment tokens is
 // one segment: thread t owns tokens n0 = t * chunk .. n0 + chunk - 1 (chunk =
-// ceil(N / 1024)) and keeps their values in registers through every pass.  A
+// ceil(N / threads)) and keeps their values in registers through every pass.  A
 // larger image is cut into segments of kSegment tokens (chunk = kMaxChunk); each
 // pass visits the segments in order and has the caller load the segment's values
 // again.  Every decision is an exact comparison of integer keys, so the kept set
@@ -149,9 +149,12 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], L
                              double* __restrict__ adj_out, uint8_t* __restrict__ rep_out, int N,
                              int gh, int gw, int G, float lambda, int K, Keep&& keep) {
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+    // images of at most 1024 tokens run with one thread per token, rounded up to
+    // whole waves; larger ones with kThreads
+    const int nthreads = blockDim.x, nwaves = nthreads / kWave;
     const int nseg = MAXC == kMaxChunk ? (N + kSegment - 1) / kSegment : 1;
     const bool streamed = nseg > 1;
-    const int chunk = streamed ? kMaxChunk : (N + kThreads - 1) / kThreads;
+    const int chunk = streamed ? kMaxChunk : (N + nthreads - 1) / nthreads;
     auto first_of = [&](int s) { return min(N, s * kSegment + tid * chunk); };
     auto count_of = [&](int n0) { return max(0, min(N - n0, chunk)); };
     // the tokens of segment s in the registers: a single segment is loaded once,
@@ -166,8 +169,8 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], L
     };
     if (!streamed) load_segment(0, true);
 
-    for (int i = tid; i < G * G; i += kThreads) best[i] = ~0ull;
-    if (tid < 256) sh.hist[0][tid] = 0u;
+    for (int i = tid; i < G * G; i += nthreads) best[i] = ~0ull;
+    for (int i = tid; i < 256; i += nthreads) sh.hist[0][i] = 0u;
     __syncthreads();
 
     int cell[MAXC];
@@ -261,7 +264,7 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], L
     }
     __syncthreads();
     // the waves' ranges, combined across lanes of every wave at once
-    uint64_t lo = lane < kWaves ? sh.wlo[lane] : ~0ull, hi = lane < kWaves ? sh.whi[lane] : 0ull;
+    uint64_t lo = lane < nwaves ? sh.wlo[lane] : ~0ull, hi = lane < nwaves ? sh.whi[lane] : 0ull;
     wave_minmax_u64(lo, hi);
 
     // ---- radix select of the K-th smallest key (Eq. 23) -----------------------
@@ -280,7 +283,7 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], L
         for (int round = 0;; ++round) {
             uint32_t* h = sh.hist[round % 3];
             // the buffer after this one was last read before the previous barrier
-            if (tid < 256) sh.hist[(round + 1) % 3][tid] = 0u;
+            for (int i = tid; i < 256; i += nthreads) sh.hist[(round + 1) % 3][i] = 0u;
             for (int s = 0; s < nseg; ++s) {
                 revisit(s);
                 const int cnt = count_of(first_of(s));
@@ -362,7 +365,7 @@ __device__ void select_image(const float (&cv)[MAXC], const int (&posv)[MAXC], L
         if (lane == kWave - 1) sh.scan[wave] = incl;
         __syncthreads();
         uint32_t before = incl - packed, total = 0;
-        for (int w = 0; w < kWaves; ++w) {
+        for (int w = 0; w < nwaves; ++w) {
             const uint32_t v = sh.scan[w];
             if (w < wave) before += v;
             total += v;
@@ -666,6 +669,22 @@ __global__ __launch_bounds__(kThreads) void attention_select_kernel(
                        });
 }
 
+// Tokens per thread, rounded up to the kernel variant's register budget.
+int chunk_class(const Dims& d) {
+    const int64_t chunk = (d.N + kThreads - 1) / kThreads;
+    return chunk <= 1 ? 1 : chunk <= 2 ? 2 : chunk <= 4 ? 4 : chunk <= 8 ? 8 : kMaxChunk;
+}
+
+// Workgroup size of the selection kernels: one thread per token, in whole waves,
+// for images of at most kThreads tokens (fewer waves to synchronise, and each
+// wave's scan of the histogram is not repeated by idle waves); kThreads above.
+// Every decision is an exact comparison of integer keys, so the kept set does not
+// depend on it.
+unsigned select_threads(const Dims& d) {
+    if (d.N > kThreads) return kThreads;
+    return static_cast<unsigned>((d.N + kWave - 1) / kWave * kWave);
+}
+
 template <typename Kern>
 hipError_t allow_lds(Kern kern, size_t lds) {
     if (lds <= 64 * 1024) return hipSuccess;
@@ -689,7 +708,7 @@ hipError_t launch_dssel(const Dims& d, const SelectArgs& a, const float* rho, co
         err = hipGetLastError();
         if (err != hipSuccess) return err;
     }
-    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(kThreads), lds, st, rho, pbar_c,
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(select_threads(d)), lds, st, rho, pbar_c,
                        m_prev, static_cast<const f32x4*>(pre), a, bg);
     return hipGetLastError();
 }
@@ -701,7 +720,7 @@ hipError_t launch_attsel(const Dims& d, const SelectArgs& a, const float* suppor
     auto kern = attention_select_kernel<MAXC>;
     hipError_t err = allow_lds(kern, lds);
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(kThreads), lds, st, support_c,
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(select_threads(d)), lds, st, support_c,
                        a, batch_geom(d, a.keep));
     return hipGetLastError();
 }
@@ -713,16 +732,10 @@ hipError_t launch_sel(const Dims& d, int cells, float lambda, int keep, const fl
     auto kern = spatial_select_kernel<MAXC>;
     hipError_t err = allow_lds(kern, lds);
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(kThreads), lds, st, prio_c,
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(d.B)), dim3(select_threads(d)), lds, st, prio_c,
                        keep_idx, adj_c, is_rep, static_cast<int>(d.N), static_cast<int>(d.gh),
                        static_cast<int>(d.gw), cells, lambda, keep);
     return hipGetLastError();
-}
-
-// Tokens per thread, rounded up to the kernel variant's register budget.
-int chunk_class(const Dims& d) {
-    const int64_t chunk = (d.N + kThreads - 1) / kThreads;
-    return chunk <= 1 ? 1 : chunk <= 2 ? 2 : chunk <= 4 ? 4 : chunk <= 8 ? 8 : kMaxChunk;
 }
 
 }  // namespace

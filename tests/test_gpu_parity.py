@@ -251,6 +251,28 @@ def test_selection_edges(keep, cells, lam):
         np.testing.assert_array_equal(rep[b].cpu().numpy(), bb)
 
 
+@pytest.mark.parametrize("grid", [(1, 1), (7, 9), (8, 8), (5, 13), (31, 33), (32, 32), (25, 41)])
+def test_selection_workgroup_sizes(grid):
+    """1, 63, 64, 65, 1023, 1024 and 1025 tokens: the selection kernels run with one
+    thread per token in whole waves up to 1024 tokens and with 1024 threads (two
+    tokens per thread) above; kept sets and representatives equal the oracle's,
+    with exact ties in c."""
+    gh, gw = grid
+    n = gh * gw
+    rng = np.random.default_rng(n)
+    c = (rng.integers(0, 9, size=(2, n)) / 16.0).astype(np.float32)
+    cd = torch.from_numpy(c).cuda()
+    cells = min(4, gh, gw)
+    for keep in sorted({0, 1, n // 3, n}):
+        idx, _, rep = E.spatial_select(cd, gh, gw, keep, cells, 0.25, want_rep=True)
+        torch.cuda.synchronize()
+        for b in range(2):
+            ok, _, bb = O.spatial_select(1.0 - c[b].astype(np.float64), gh, gw, cells,
+                                         F32(0.25), keep)
+            assert idx[b].cpu().tolist() == ok.tolist(), (grid, keep, b)
+            np.testing.assert_array_equal(rep[b].cpu().numpy(), bb)
+
+
 def test_determinism_and_stream():
     """Two runs give identical bits; a call on a side stream matches the default stream."""
     cfg = synth.config_by_name("llava").replace(batch=3)

@@ -93,6 +93,18 @@ def read_traffic(mode: str, workload: str):
         return None
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def copy_calibrate(mib: int):
     import torch
     n = mib * (1 << 20) // 4
@@ -451,8 +463,10 @@ def main():
 
     # ---- CPU oracle baseline ----------------------------------------------------
     import oracle as O
-    from threadpoolctl import threadpool_info
-    cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    from threadpoolctl import threadpool_info, threadpool_limits
+    cores = len(os.sched_getaffinity(0))
+    threadpool_limits(cores)
+    used = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     t_c = time.perf_counter()
     done = 0
     passes = 0
@@ -468,7 +482,8 @@ def main():
             break
     cpu_s = time.perf_counter() - t_c
     cpu_value = done / cpu_s
-    log(f"[bench] oracle: {done} images in {cpu_s:.1f}s on {cores} threads")
+    log(f"[bench] oracle: {done} images in {cpu_s:.1f}s on {used} threads ({cores} cores, "
+        f"{cpu_model()})")
 
     out = {
         "metric": METRIC,
@@ -481,7 +496,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": cfg.dtype,
         "data": "synthetic",
         "config": {
             "workload": (f"{cfg.name}: {SHAPES.get(cfg.name, 'synthetic')}, batch {B} images, "
@@ -516,7 +531,8 @@ def main():
         "cpu_baseline": {
             "value": round(cpu_value, 2),
             "unit": "images/s",
-            "cores": cores,
+            "cores": used,
+            "cpu_model": cpu_model(),
             "kind": "oracle",
             "sample": (f"{done} images of the same {cfg.name} batch ({passes} pass(es) over "
                        f"images 0..{B - 1}), NumPy float64 oracle, mode {args.mode}"),

@@ -5,7 +5,7 @@ include/e2s.h); this package only builds and binds it.  Importing it without a
 built library raises ImportError: there is no CPU fallback.
 """
 from ._lib import (VARIANTS, CompactShape, E2SError, Image, Params, Pruner, QKViews,
-                   RaggedPruner, RaggedShape, Shape, StagePruner, compact_tokens, default_scale,
+                   RaggedPruner, RaggedShape, Shape, StagePruner, compact_tokens,
                    ds_combine_layers, fuse_evidence, fuse_select, head_masses, head_reliability,
                    layer_reliability, lib, make_params, make_shape, packed_images, prune,
                    prune_ragged, prune_stage, prune_views, qk_views, score_heads, spatial_select,
@@ -13,7 +13,7 @@ from ._lib import (VARIANTS, CompactShape, E2SError, Image, Params, Pruner, QKVi
 
 __all__ = ["VARIANTS", "CompactShape", "E2SError", "Image", "Params", "Pruner", "QKViews",
            "RaggedPruner", "RaggedShape", "Shape", "StagePruner", "compact_tokens",
-           "default_scale", "ds_combine_layers", "fuse_evidence", "fuse_select", "head_masses",
+           "ds_combine_layers", "fuse_evidence", "fuse_select", "head_masses",
            "head_reliability", "layer_reliability", "lib", "make_params", "make_shape",
            "packed_images", "prune", "prune_ragged", "prune_stage", "prune_views", "qk_views",
            "score_heads", "spatial_select", "workspace_size"]

@@ -19,7 +19,6 @@ from __future__ import annotations
 
 import ctypes
 import dataclasses
-import math
 import os
 import re
 from typing import Optional
@@ -544,10 +543,6 @@ def prune_stage(q, k, grid_h: int, grid_w: int, keep: int, cand_pos=None, m_prev
     sp = StagePruner(q, k, grid_h, grid_w, keep, cells, lam, mode, scale, variant)
     idx, pos, m = sp(q, k, cand_pos, m_prev)
     return idx, pos, m
-
-
-def default_scale(head_dim: int) -> float:
-    return 1.0 / math.sqrt(head_dim)
 
 
 # ---------------------------------------------------------------------------

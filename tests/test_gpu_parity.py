@@ -9,11 +9,13 @@ batches with at least one (image, layer) per compute unit, where the whole path
 keeps each layer's supports on chip.  Each stage is checked twice: fed the GPU's own
 upstream output (isolates that stage's arithmetic) and end to end from Q and K.
 
-Tolerances (absolute + relative to the oracle value), all float32 arithmetic on
-exact inputs:
+Tolerances, all float32 arithmetic on exact inputs (err <= atol + rtol |ref|
+unless stated otherwise):
   r (Eq. 8), e = p - 1/2 (Eq. 9)      atol 1e-6 / rtol 2e-4 of the logit-scale error
   evidence stages on equal inputs      atol 1e-7 / rtol 2e-5
-  fused masses end to end              atol 1e-4 (the stated bar) and rtol 2e-3
+  fused masses end to end              two gates, both enforced: max |d| <= 1e-4 (the
+                                       stated bar), and |d| <= 1e-7 + 2e-3 |ref| per
+                                       element
   kept sets                            exact, or differing only by tokens whose
                                        oracle score is within 1e-5 of the K-th
   selection on equal inputs            bit-exact sets and representatives
@@ -23,7 +25,8 @@ import pytest
 
 import oracle as O
 import synth
-from _helpers import TIE_GAP, check_keep_wellformed, compare_sets, log, oracle_images, to_device
+from _helpers import (TIE_GAP, SelectGeom, assert_mass_bar, check_keep_wellformed,
+                      compare_sets, log, oracle_images, to_device)
 
 pytestmark = pytest.mark.gpu
 
@@ -176,9 +179,10 @@ def _run_case(cfg, mode):
         assert keep[b].tolist() == sel_keep.tolist()
         _errs("adj_c", adj[b], 1.0 - sel_qt, 1e-15, 1e-12)
         # end to end
-        _errs("fused e2e", fused[b], ref.fused, 1e-4, 2e-3)
+        err = assert_mass_bar(fused[b], ref.fused, "fused e2e")
+        log(f"    fused e2e  max|d|={err:.3e}")
         _errs("c e2e", prio[b], 1.0 - ref.q, 1e-7, 2e-3)
-        cmp = compare_sets(keep[b], ref)
+        cmp = compare_sets(keep[b], ref, geom=SelectGeom(gh, gw, G, lam))
         log(f"    set: {cmp.verdict} swaps={cmp.swaps} near-boundary={cmp.near_boundary}")
         assert cmp.verdict != "fail"
 

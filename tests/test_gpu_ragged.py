@@ -3,8 +3,9 @@
 A ragged batch gives every image its own grid, text length and budget.  The path
 never mixes images (Eq. 1-23 are per image), so each image's result must be the
 one e2s_prune returns for that image alone, bit for bit, and must match the CPU
-oracle under the same rule as the uniform path (fused masses within 1e-4 absolute,
-kept sets exact or differing only inside the 1e-5 tie window).
+oracle under the same rule as the uniform path (fused masses within 1e-4 absolute
+and within 1e-7 + 2e-3 |ref| per element, kept sets exact or differing only inside
+the 1e-5 tie window).
 
 Cases mix grids (ragged tails, a 2x3 grid at G = 2), text lengths (1 to 150, so the
 mean-of-probabilities kernel takes one or two query chunks, 2 or 4 key tiles at a
@@ -20,7 +21,7 @@ import pytest
 
 import oracle as O
 import synth
-from _helpers import check_keep_wellformed, compare_sets, log, to_device
+from _helpers import assert_mass_bar, check_keep_wellformed, compare_sets, log, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -153,7 +154,7 @@ def test_ragged_matches_each_image_alone_and_the_oracle(name, mode):
         check_keep_wellformed(kb_keep[None], n, K)
         ref = O.prune_image(qb, kb, gh, gw, K, cells, 0.1, mode)
         err = np.abs(kb_fused.astype(np.float64) - ref.fused)
-        assert (err <= 1e-4 + 2e-3 * np.abs(ref.fused)).all(), f"image {b}: fused masses"
+        assert_mass_bar(kb_fused, ref.fused, f"image {b}: fused masses")
         cmp = compare_sets(kb_keep, ref)
         log(f"  image {b} {gh}x{gw} N_T={nt} K={K}: set {cmp.verdict} swaps={cmp.swaps} "
             f"max|d fused|={err.max():.2e}")
@@ -218,8 +219,8 @@ def test_ragged_variants(variant):
             keep_all[im.keep_offset:im.keep_offset + K].tolist()
 
 
-def test_ragged_workload_sampled_images():
-    """The Qwen2-VL dynamic-resolution workload at full size: sampled images against
+def test_ragged_workload_every_image():
+    """The Qwen2-VL dynamic-resolution workload at full size: every image against
     the oracle (the launch configuration the benchmark times)."""
     rc = synth.ragged_by_name("qwen2vl_dynamic")
     qs, ks, _, dims = synth.gen_ragged(rc)
@@ -232,15 +233,19 @@ def test_ragged_workload_sampled_images():
                                         want_fused=True)
         torch.cuda.synchronize()
         keep_all, fused_all = keep.cpu().numpy(), fused.cpu().numpy()
-        for b in (0, 13, 31):
+        counts = {}
+        for b in range(len(dims)):
             gh, gw, nt, K = dims[b]
             im = arr[b]
             ref = O.prune_image(qs[b], ks[b], gh, gw, K, 4, 0.1, mode)
             got_f = fused_all[im.token_offset:im.token_offset + gh * gw]
-            assert np.abs(got_f - ref.fused).max() <= 1e-4
+            err = assert_mass_bar(got_f, ref.fused, f"image {b}: fused masses")
             cmp = compare_sets(keep_all[im.keep_offset:im.keep_offset + K], ref)
-            log(f"  {mode} image {b} {gh}x{gw} N_T={nt} K={K}: {cmp.verdict} swaps={cmp.swaps}")
+            log(f"  {mode} image {b} {gh}x{gw} N_T={nt} K={K}: {cmp.verdict} swaps={cmp.swaps} "
+                f"max|d fused|={err:.2e}")
+            counts[cmp.verdict] = counts.get(cmp.verdict, 0) + 1
             assert cmp.verdict != "fail"
+        log(f"  {mode}: {len(dims)} images, sets {counts}")
 
 
 def test_ragged_validation_on_device_pointers():
@@ -298,7 +303,7 @@ def test_mean_prob_group_size_does_not_change_bits(heavy):
         ref = O.prune_image(qb, kb, gh, gw, K, 2, 0.1, "mean_prob")
         got = fused_a[a.token_offset:a.token_offset + gh * gw].astype(np.float64)
         err = np.abs(got - ref.fused)
-        assert (err <= 1e-4 + 2e-3 * np.abs(ref.fused)).all(), f"image {b}: fused masses"
+        assert_mass_bar(got, ref.fused, f"image {b}: fused masses")
         cmp = compare_sets(keep_a[a.keep_offset:a.keep_offset + K], ref)
         log(f"  image {b} {gh}x{gw} N_T={nt} K={K}: set {cmp.verdict} "
             f"max|d fused|={err.max():.2e}")

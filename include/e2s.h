@@ -26,7 +26,8 @@
  *    double outputs 8-byte aligned.  Outputs must not overlap inputs or each other.
  *  - The library is stateless and reentrant; calls on different streams may
  *    run concurrently when they share no workspace and no output.  There is no
- *    global error state.
+ *    global error state.  The one exception is e2s_prune_noalloc, whose workspace
+ *    is a static device array of the library (one per GPU, shared by its calls).
  *  - The kernels run on the current HIP device; every pointer of a call must be
  *    memory of that device and `stream` one of its streams.
  *  - Centred quantities: the support p is exported as e = p - 1/2 and the
@@ -50,7 +51,7 @@
 extern "C" {
 #endif
 
-#define E2S_ABI_VERSION 7
+#define E2S_ABI_VERSION 8
 
 #if defined(__GNUC__) || defined(__clang__)
 #define E2S_API __attribute__((visibility("default")))
@@ -66,7 +67,10 @@ typedef enum {
     E2S_ERR_UNSUPPORTED = 4,          /* valid per the paper, not implemented here     */
     E2S_ERR_MISALIGNED = 5,           /* a pointer violates the alignment rule         */
     E2S_ERR_WORKSPACE_TOO_SMALL = 6,  /* e2s_prune workspace below the required size   */
-    E2S_ERR_LAUNCH = 7                /* the HIP runtime refused a kernel launch       */
+    E2S_ERR_LAUNCH = 7,               /* the HIP runtime refused a kernel launch       */
+    E2S_ERR_SCRATCH_TOO_SMALL = 8     /* e2s_prune_noalloc: the call needs more than
+                                         E2S_NOALLOC_SCRATCH_BYTES of scratch, or the
+                                         scratch's device address was not available     */
 } e2s_status;
 
 typedef enum { E2S_DTYPE_F32 = 0, E2S_DTYPE_BF16 = 1, E2S_DTYPE_F16 = 2 } e2s_dtype;
@@ -365,6 +369,34 @@ E2S_API e2s_status e2s_prune_views(const e2s_shape* shape, const e2s_params* par
                                    const e2s_qk_views* views, void* workspace,
                                    size_t workspace_bytes, int32_t* keep_idx, float* fused_opt,
                                    float* prio_c_opt, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): e2s_prune without the
+ * caller's workspace.
+ * ------------------------------------------------------------------------- */
+
+/* Size of the library's static device scratch: one array per GPU, held from the
+ * first e2s_prune_noalloc call on that GPU until the process ends. */
+#define E2S_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+/* e2s_prune with its workspace taken from the library's static scratch instead of
+ * an argument.  Everything else (arguments, validation, kernels, results) is
+ * e2s_prune's: the results equal e2s_prune's bit for bit.  The call allocates
+ * nothing: no hipMalloc or hipFree, no allocating library routine.  Its first call
+ * on a device, with that device current, looks up that device's copy of the
+ * scratch (hipGetSymbolAddress) and keeps the address for later calls.
+ *   A shape whose e2s_prune_workspace_size exceeds E2S_NOALLOC_SCRATCH_BYTES (e.g.
+ *   more than 64 LLaVA-shaped images per call) returns E2S_ERR_SCRATCH_TOO_SMALL
+ *   and enqueues nothing; so does a failed address lookup.
+ *   Every call on one GPU shares that GPU's scratch, which keeps the last call's
+ *   contents (the kernels write every scratch byte before they read it, so no
+ *   call needs it cleared).  Calls that overlap in time on one GPU (other streams,
+ *   other host threads) race on it: order them on one stream, or use e2s_prune
+ *   with a workspace each. */
+E2S_API e2s_status e2s_prune_noalloc(const e2s_shape* shape, const e2s_params* params,
+                                     const void* q, const void* k, int32_t* keep_idx,
+                                     float* fused_opt, float* prio_c_opt, void* stream);
 
 /* Static description of a status code (never NULL). */
 E2S_API const char* e2s_status_string(e2s_status status);

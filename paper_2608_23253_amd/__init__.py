@@ -8,12 +8,12 @@ from ._lib import (VARIANTS, CompactShape, E2SError, Image, Params, Pruner, QKVi
                    RaggedPruner, RaggedShape, Shape, StagePruner, compact_tokens,
                    ds_combine_layers, fuse_evidence, fuse_select, head_masses, head_reliability,
                    layer_reliability, lib, make_params, make_shape, packed_images, prune,
-                   prune_ragged, prune_stage, prune_views, qk_views, score_heads, spatial_select,
+                   prune_noalloc, prune_ragged, prune_stage, prune_views, qk_views, score_heads, spatial_select,
                    workspace_size)
 
 __all__ = ["VARIANTS", "CompactShape", "E2SError", "Image", "Params", "Pruner", "QKViews",
            "RaggedPruner", "RaggedShape", "Shape", "StagePruner", "compact_tokens",
            "ds_combine_layers", "fuse_evidence", "fuse_select", "head_masses",
            "head_reliability", "layer_reliability", "lib", "make_params", "make_shape",
-           "packed_images", "prune", "prune_ragged", "prune_stage", "prune_views", "qk_views",
+           "packed_images", "prune", "prune_noalloc", "prune_ragged", "prune_stage", "prune_views", "qk_views",
            "score_heads", "spatial_select", "workspace_size"]

@@ -29,7 +29,9 @@ HEADER = os.path.join(os.path.dirname(PKG), "include", "e2s.h")
 
 # status codes (e2s_status)
 OK, ERR_NULL_POINTER, ERR_BAD_SHAPE, ERR_BAD_PARAM, ERR_UNSUPPORTED, ERR_MISALIGNED, \
-    ERR_WORKSPACE_TOO_SMALL, ERR_LAUNCH = range(8)
+    ERR_WORKSPACE_TOO_SMALL, ERR_LAUNCH, ERR_SCRATCH_TOO_SMALL = range(9)
+# E2S_NOALLOC_SCRATCH_BYTES: the static scratch of e2s_prune_noalloc
+NOALLOC_SCRATCH_BYTES = 64 << 20
 DTYPE_F32, DTYPE_BF16, DTYPE_F16 = 0, 1, 2
 MEAN_LOGIT, MEAN_PROB = 0, 1
 MODES = {"mean_logit": MEAN_LOGIT, "mean_prob": MEAN_PROB}
@@ -112,6 +114,7 @@ _SIGNATURES = {
                          _P, _P, _P, _P],
     "e2s_compact_tokens": [ctypes.POINTER(CompactShape), _P, _P, _P, _P],
     "e2s_prune_views": [_SH, _PA, ctypes.POINTER(QKViews), _P, ctypes.c_size_t, _P, _P, _P, _P],
+    "e2s_prune_noalloc": [_SH, _PA, _P, _P, _P, _P, _P, _P],
     "e2s_status_string": [ctypes.c_int],
     "e2s_abi_version": [],
 }
@@ -433,6 +436,25 @@ def prune(q, k, grid_h: int, grid_w: int, keep: int, cells: int = 4, lam: float 
     prio = torch.empty((B, N), device=q.device, dtype=torch.float32) if want_prio else None
     idx = p(q, k, fused, prio)
     return idx, fused, prio
+
+
+def prune_noalloc(q, k, grid_h: int, grid_w: int, keep: int, cells: int = 4, lam: float = 0.1,
+                  mode="mean_logit", scale: float = 0.0, keep_idx=None, fused=None, prio_c=None,
+                  variant="full"):
+    """e2s_prune with the library's static scratch as its workspace (e2s_prune_noalloc):
+    (keep_idx [B,K], fused [B,N,3] or None, prio_c [B,N] or None).  Output tensors may
+    be passed in; only those not given are allocated here, by torch."""
+    torch = _torch()
+    _check(q, "q", ndim=5)
+    _check(k, "k", dtype=q.dtype, ndim=5)
+    sh = shape_from(q, k, grid_h, grid_w)
+    pa = make_params(_dtype_code(q), mode, scale, cells, lam, keep, variant)
+    if keep_idx is None:
+        keep_idx = torch.empty((sh.batch, keep), device=q.device, dtype=torch.int32)
+    _launch("e2s_prune_noalloc", (q, k, keep_idx, fused, prio_c), _LIB.e2s_prune_noalloc,
+            ctypes.byref(sh), ctypes.byref(pa), q.data_ptr(), k.data_ptr(),
+            keep_idx.data_ptr() if keep > 0 else None, _ptr(fused), _ptr(prio_c))
+    return keep_idx, fused, prio_c
 
 
 def qk_views(q_layers, k_layers) -> QKViews:

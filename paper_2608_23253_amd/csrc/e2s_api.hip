@@ -3,10 +3,16 @@
 // runtime, then enqueues its kernels on the caller's stream.
 #include <atomic>
 #include <cmath>
+#include <mutex>
 
 #include "e2s.h"
 #include "e2s_kernels.h"
 #include "e2s_validate.h"
+
+// Workspace of e2s_prune_noalloc (callers that cannot allocate).  In host code
+// `scratch` names a host-side stand-in, not device memory: kernels and copies get
+// the device address that scratch_address() looks up once per device.
+static __device__ __align__(256) unsigned char scratch[E2S_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -136,6 +142,27 @@ e2s_status check_score_inputs(const e2s_shape* shape, const e2s_params* params, 
     return E2S_OK;
 }
 
+constexpr int kMaxDevices = 64;
+
+// The current device's address of `scratch`: looked up with that device current on
+// the first call, then reused (each device holds its own copy of the array).
+e2s_status scratch_address(void** out) {
+    static std::mutex mu;
+    static void* addr[kMaxDevices] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return E2S_ERR_SCRATCH_TOO_SMALL;
+    std::lock_guard<std::mutex> lock(mu);
+    if (addr[dev] == nullptr) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+            return E2S_ERR_SCRATCH_TOO_SMALL;
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return E2S_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -152,6 +179,7 @@ const char* e2s_status_string(e2s_status status) {
         case E2S_ERR_MISALIGNED: return "E2S_ERR_MISALIGNED: a pointer violates the alignment rule";
         case E2S_ERR_WORKSPACE_TOO_SMALL: return "E2S_ERR_WORKSPACE_TOO_SMALL: workspace below e2s_prune_workspace_size";
         case E2S_ERR_LAUNCH: return "E2S_ERR_LAUNCH: the HIP runtime refused a kernel launch";
+        case E2S_ERR_SCRATCH_TOO_SMALL: return "E2S_ERR_SCRATCH_TOO_SMALL: the call needs more than the library's static scratch (E2S_NOALLOC_SCRATCH_BYTES), or its device address was unavailable";
     }
     return "unknown e2s_status";
 }
@@ -290,6 +318,29 @@ e2s_status e2s_prune(const e2s_shape* shape, const e2s_params* params, const voi
     E2S_TRY(aligned_opt(prio_c_opt, 4));
 
     return run_operation(d, params, q, k, workspace,
+                         select_args(params, keep_idx, fused_opt, prio_c_opt), nullptr,
+                         static_cast<hipStream_t>(stream));
+}
+
+e2s_status e2s_prune_noalloc(const e2s_shape* shape, const e2s_params* params, const void* q,
+                             const void* k, int32_t* keep_idx, float* fused_opt,
+                             float* prio_c_opt, void* stream) {
+    Dims d;
+    E2S_TRY(e2s::check_shape(shape, &d));
+    E2S_TRY(e2s::check_score_params(params));
+    E2S_TRY(need(q));
+    E2S_TRY(need(k));
+    E2S_TRY(e2s::check_aligned(q, 16));
+    E2S_TRY(e2s::check_aligned(k, 16));
+    E2S_TRY(e2s::check_select_params(params, d));
+    if (params->keep > 0) E2S_TRY(need(keep_idx));
+    E2S_TRY(aligned_opt(keep_idx, 4));
+    E2S_TRY(aligned_opt(fused_opt, 4));
+    E2S_TRY(aligned_opt(prio_c_opt, 4));
+    if (e2s::prune_workspace_bytes(d) > E2S_NOALLOC_SCRATCH_BYTES) return E2S_ERR_SCRATCH_TOO_SMALL;
+    void* ws = nullptr;
+    E2S_TRY(scratch_address(&ws));
+    return run_operation(d, params, q, k, ws,
                          select_args(params, keep_idx, fused_opt, prio_c_opt), nullptr,
                          static_cast<hipStream_t>(stream));
 }

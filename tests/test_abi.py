@@ -67,14 +67,14 @@ def stage(shape, params, ncand, q=A, k=A, pos=A, mprev=None, ws=A, ws_bytes=None
 
 def test_exports_every_declared_entry_point():
     names = L.header_entry_points()
-    assert len(names) == 17
+    assert len(names) == 18
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.e2s_abi_version() == 7
+    assert lib.e2s_abi_version() == 8
 
 
 def test_status_strings():
-    for code in range(8):
+    for code in range(9):
         s = lib.e2s_status_string(code).decode()
         assert s.startswith("E2S_")
     assert b"unknown" in lib.e2s_status_string(99)
@@ -409,3 +409,30 @@ def test_views_validation():
     # the packed strides of f32 rows (d = 64: 256 bytes) are accepted by validation
     v = good_views()
     assert views(sh, good_params(dtype=L.DTYPE_F32), v, out=None) == L.ERR_NULL_POINTER
+
+
+def noalloc(shape, params, q=A, k=A, out=A):
+    return lib.e2s_prune_noalloc(ctypes.byref(shape), ctypes.byref(params), q, k, out, None,
+                                 None, None)
+
+
+def test_noalloc_validation():
+    """e2s_prune_noalloc validates like e2s_prune and refuses a shape whose workspace
+    exceeds the static scratch before it looks the scratch up."""
+    pa = good_params()
+    assert noalloc(good_shape(), pa, q=None) == L.ERR_NULL_POINTER
+    assert noalloc(good_shape(), pa, k=A + 2) == L.ERR_MISALIGNED
+    assert noalloc(good_shape(head_dim=96), pa) == L.ERR_UNSUPPORTED
+    assert noalloc(good_shape(), good_params(keep=43)) == L.ERR_BAD_PARAM
+    assert noalloc(good_shape(), pa, out=None) == L.ERR_NULL_POINTER
+    # 256 LLaVA-shaped images: 80 MB of workspace against 64 MiB of scratch
+    big = good_shape(batch=256, num_layers=4, num_heads=32, num_kv_heads=32, head_dim=128,
+                     num_text=64, grid_h=24, grid_w=24)
+    assert L.workspace_size(big, pa) > L.NOALLOC_SCRATCH_BYTES
+    assert noalloc(big, pa) == L.ERR_SCRATCH_TOO_SMALL
+    with open(L.HEADER) as f:
+        assert "#define E2S_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)" in f.read()
+    # 64 of them fit
+    fits = good_shape(batch=64, num_layers=4, num_heads=32, num_kv_heads=32, head_dim=128,
+                      num_text=64, grid_h=24, grid_w=24)
+    assert L.workspace_size(fits, pa) <= L.NOALLOC_SCRATCH_BYTES

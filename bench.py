@@ -11,7 +11,15 @@ reliability stage, timed alone with HIP events on the launch stream), per-stage
 times of the staged entry points, the ablation variants, the progressive
 schedule, a ragged batch (e2s_prune_ragged on seeded dynamic-resolution images),
 token compaction of the kept tokens (e2s_compact_tokens) and the CPU oracle's
-throughput on a bounded sample.
+throughput on a bounded sample, with a parity summary of the step's results on
+the images the oracle processed.
+
+`configs` repeats the measurement for the other workloads and readings at their
+full batches (the aggressive LLaVA workload for each lambda of its sweep): step
+time and images/s, the two kernels of e2s_prune timed alone, the fraction of the
+binding roofline (bf16 MFMA for the mean-of-probabilities reading where the
+contraction outweighs the bytes), the selection tail's bytes and HBM fraction, and
+the oracle on a few images of each, timed, with the parity summary of those images.
 
 Other modes (used by the profiling commands kept with the results):
     --kernel-only   run only the timed e2s_prune steps (no CPU baseline)
@@ -58,6 +66,8 @@ def parse():
     ap.add_argument("--kernel-only", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the ablation-variant and progressive-schedule timings")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other workloads and readings (the configs object)")
     ap.add_argument("--copy-calibrate", type=int, default=0, metavar="N_MIB")
     ap.add_argument("--hbm-probe", type=int, default=0, metavar="N_MIB",
                     help="time a streaming read (torch sum) of N MiB: a practical read ceiling")
@@ -317,6 +327,208 @@ def bench_compaction(args, timed, kd, keep_idx):
     return out
 
 
+# The workloads and readings reported beside the headline one, each at its full
+# batch, and how many images of each are compared with the oracle.
+CONFIG_RUNS = (("llava", ("mean_prob",)),
+               ("llava_aggressive", ("mean_logit", "mean_prob")),
+               ("qwen2vl_gqa", ("mean_logit", "mean_prob")),
+               ("hires", ("mean_logit", "mean_prob")))
+PARITY_SAMPLE = {"llava": 8, "llava_aggressive": 8, "qwen2vl_gqa": 8, "hires": 2}
+
+
+def roofline_floor_us(cfg, mode, batch):
+    """Roofline time of one step: max(Q + K bytes / 8 TB/s, Eq. 1 flops / bf16 MFMA
+    peak), the flops only for the mean-of-probabilities reading (the mean-of-logits
+    reading hoists the query mean and streams the keys against one vector)."""
+    hbm_us = batch * cfg.bytes_per_image() / (HBM_PEAK_GBS * 1e9) * 1e6
+    if mode != "mean_prob":
+        return hbm_us, "hbm", None
+    flops = 2.0 * batch * cfg.num_layers * cfg.num_heads * cfg.num_text * cfg.num_visual \
+        * cfg.head_dim
+    mfma_us = flops / (MFMA_BF16_PEAK_TFLOPS * 1e12) * 1e6
+    return max(hbm_us, mfma_us), ("mfma" if mfma_us > hbm_us else "hbm"), flops
+
+
+def cpu_baseline_leg(cfg, mode, q_np, k_np, sample):
+    """The CPU oracle on the sampled images: (images/s, threads used, its results)."""
+    import oracle as O
+    from threadpoolctl import threadpool_info, threadpool_limits
+    threadpool_limits(len(os.sched_getaffinity(0)))
+    used = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    t0 = time.perf_counter()
+    refs = [O.prune_image(q_np[j], k_np[j], cfg.grid_h, cfg.grid_w, cfg.keep, cfg.cells,
+                          cfg.lam, mode) for j in range(len(sample))]
+    dt = time.perf_counter() - t0
+    return len(sample) / dt, used, refs
+
+
+def parity_summary(cfg, refs, sample, kept_by_lam, fused):
+    """GPU results of the sampled images against the oracle's results `refs` (from the
+    CPU-baseline leg): max |d m~| (first lambda's fused masses) and the exact / tie /
+    rep_flip / fail counts of every lambda's kept sets, by the test suite's rule
+    (tests/_helpers.compare_sets)."""
+    import dataclasses
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    from _helpers import SelectGeom, compare_sets, mass_errors
+    import oracle as O
+
+    out = {"images": [int(b) for b in sample], "max_abs_dfused": 0.0, "by_lambda": {}}
+    gh, gw, G, K = cfg.grid_h, cfg.grid_w, cfg.cells, cfg.keep
+    for j, b in enumerate(sample):
+        a, _ = mass_errors(fused[b], refs[j].fused)
+        out["max_abs_dfused"] = max(out["max_abs_dfused"], a)
+    for lam, kept in kept_by_lam.items():
+        counts = {"exact": 0, "tie": 0, "rep_flip": 0, "fail": 0, "swaps": 0}
+        for j, b in enumerate(sample):
+            ref = refs[j]
+            if lam != cfg.lam:
+                o_keep, o_qt, o_b = O.spatial_select(ref.q, gh, gw, G, lam, K)
+                ref = dataclasses.replace(ref, keep=o_keep, qt=o_qt, is_rep=o_b)
+            cmp = compare_sets(kept[b], ref, geom=SelectGeom(gh, gw, G, lam))
+            counts[cmp.verdict] += 1
+            counts["swaps"] += cmp.swaps
+        out["by_lambda"][str(lam)] = counts
+    out["max_abs_dfused"] = float(f"{out['max_abs_dfused']:.3e}")
+    return out
+
+
+def make_timed(args):
+    """timed(calls, n) on a given stream: per-call durations (ms) of each function in
+    `calls`, run in order n times, from HIP events recorded on the launch stream
+    between the calls (after args.warmup untimed rounds)."""
+    import numpy as np
+    import torch
+
+    def on_stream(stream):
+        def timed(calls, n):
+            for _ in range(args.warmup):
+                for c in calls:
+                    c()
+            torch.cuda.synchronize()
+            ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
+                  for _ in range(n)]
+            for i in range(n):
+                ev[i][0].record(stream)
+                for j, c in enumerate(calls):
+                    rc = c()
+                    if rc:
+                        raise RuntimeError(f"{c.__name__} failed with status {rc}")
+                    ev[i][j + 1].record(stream)
+            torch.cuda.synchronize()
+            return [np.array([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(n)])
+                    for j in range(len(calls))]
+        return timed
+    return on_stream
+
+
+def bench_configs(args, make_timed):
+    """Every other workload at its full batch, both readings: wall-clock step time
+    and images/s per lambda, the two kernels of e2s_prune timed alone with HIP events,
+    the fraction of the binding roofline, the selection tail's bytes and HBM fraction,
+    and a sampled parity summary against the oracle."""
+    import numpy as np
+    import torch
+    import synth
+    import paper_2608_23253_amd as E
+    from paper_2608_23253_amd import _lib as L
+
+    lib = L.lib()
+    out = {}
+    n_rep = max(20, args.steps // 4)
+    for name, modes in CONFIG_RUNS:
+        cfg = synth.config_by_name(name)
+        B, N, L_, gh, gw = cfg.batch, cfg.num_visual, cfg.num_layers, cfg.grid_h, cfg.grid_w
+        t0 = time.time()
+        q_np, k_np, _ = synth.gen_batch(cfg)
+        qd = torch.from_numpy(synth.to_bf16_bits(q_np).view(np.int16)).cuda().view(torch.bfloat16)
+        kd = torch.from_numpy(synth.to_bf16_bits(k_np).view(np.int16)).cuda().view(torch.bfloat16)
+        sample = sorted(set(np.linspace(0, B - 1, PARITY_SAMPLE[name]).round().astype(int)))
+        q_s, k_s = q_np[sample].copy(), k_np[sample].copy()
+        del q_np, k_np
+        sets = Cycle(cache_sets(qd, kd))
+        log(f"[bench] {name}: batch {B} generated and uploaded in {time.time() - t0:.1f}s, "
+            f"{len(sets.sets)} input set(s) in rotation")
+        stream = torch.cuda.current_stream()
+        timed = make_timed(stream)
+        for mode in modes:
+            rec = {"batch": B, "lambdas": {}}
+            kept_by_lam = {}
+            for lam in cfg.lambdas:
+                pr = E.Pruner(qd, kd, gh, gw, cfg.keep, cfg.cells, lam, mode)
+                for _ in range(args.warmup):
+                    pr(*sets.next())
+                torch.cuda.synchronize()
+                t_a = time.perf_counter()
+                for _ in range(n_rep):
+                    pr(*sets.next())
+                torch.cuda.synchronize()
+                us = (time.perf_counter() - t_a) * 1e6 / n_rep
+                rec["lambdas"][str(lam)] = {"us_per_step": round(us, 2),
+                                            "images_per_s": round(B / (us * 1e-6), 1)}
+                kept_by_lam[lam] = pr(qd, kd).cpu().numpy()
+            # the two kernels of e2s_prune at the first lambda, each timed alone
+            pr = E.Pruner(qd, kd, gh, gw, cfg.keep, cfg.cells, cfg.lam, mode)
+            fused = torch.empty((B, N, 3), device="cuda")
+            pr(qd, kd, fused)
+            fused_h = fused.cpu().numpy()
+            del fused
+            sh, pa = pr.shape, pr.params
+            rho = torch.empty((B, L_, N), device="cuda")
+            pbar = torch.empty_like(rho)
+            keep_buf = torch.empty((B, cfg.keep), device="cuda", dtype=torch.int32)
+            st = stream.cuda_stream
+            ws, ws_n = pr.workspace.data_ptr(), pr.workspace.numel()
+
+            def layer_rel():
+                qx, kx = sets.next()
+                return lib.e2s_layer_reliability(ctypes.byref(sh), ctypes.byref(pa),
+                                                 qx.data_ptr(), kx.data_ptr(), ws, ws_n,
+                                                 rho.data_ptr(), pbar.data_ptr(), st)
+
+            def fuse_sel():
+                return lib.e2s_fuse_select(ctypes.byref(sh), ctypes.byref(pa), rho.data_ptr(),
+                                           pbar.data_ptr(), keep_buf.data_ptr(), None, None, st)
+
+            t_lr, t_fs = timed([layer_rel, fuse_sel], n_rep)
+            stage_us, tail_us = float(t_lr.mean()) * 1e3, float(t_fs.mean()) * 1e3
+            step_us = rec["lambdas"][str(cfg.lam)]["us_per_step"]
+            floor_us, bound, flops = roofline_floor_us(cfg, mode, B)
+            tail_bytes = B * (2 * 4 * L_ * N + 4 * cfg.keep)
+            rec.update({
+                "us_per_step": step_us,
+                "images_per_s": round(B / (step_us * 1e-6), 1),
+                "stage_us": round(stage_us, 2),
+                "tail_us": round(tail_us, 2),
+                "roofline": {"bound": bound, "floor_us": round(floor_us, 2),
+                             "path_frac": round(floor_us / step_us, 4),
+                             "stage_frac": round(floor_us / stage_us, 4),
+                             "stage_hbm_GBps": round(B * cfg.bytes_per_image()
+                                                     / (stage_us * 1e-6) / 1e9, 1)},
+                "tail": {"algorithmic_bytes": int(tail_bytes),
+                         "hbm_frac": round(tail_bytes / (tail_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 5),
+                         "share_of_step": round(tail_us / step_us, 4)},
+            })
+            if flops is not None:
+                rec["roofline"]["stage_mfma_frac"] = round(
+                    flops / (stage_us * 1e-6) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
+            t_p = time.time()
+            ips, used, refs = cpu_baseline_leg(cfg, mode, q_s, k_s, sample)
+            rec["cpu_baseline"] = {"value": round(ips, 2), "unit": "images/s", "cores": used,
+                                   "kind": "oracle",
+                                   "sample": f"images {sample} of the batch, mode {mode}"}
+            rec["parity"] = parity_summary(cfg, refs, sample, kept_by_lam, fused_h)
+            log(f"[bench] {name}/{mode}: {step_us:.1f} us/step ({rec['images_per_s']:.0f} "
+                f"images/s), stage {stage_us:.1f} us, tail {tail_us:.1f} us, "
+                f"{rec['roofline']['path_frac']:.1%} of the {bound} roofline; parity "
+                f"max|d m~| {rec['parity']['max_abs_dfused']:.1e} "
+                f"{rec['parity']['by_lambda']} ({time.time() - t_p:.1f}s)")
+            out[f"{name}/{mode}"] = rec
+            del pr, rho, pbar, keep_buf
+        del qd, kd, sets
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -400,25 +612,7 @@ def main():
         return lib.e2s_fuse_select(shp, pap, rho.data_ptr(), pbar.data_ptr(), keep_buf.data_ptr(),
                                    None, None, st)
 
-    def timed(calls, n):
-        """Per-call durations (ms) of each function in `calls`, run in order n times,
-        from HIP events recorded on the launch stream between the calls."""
-        for _ in range(args.warmup):
-            for c in calls:
-                c()
-        torch.cuda.synchronize()
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
-              for _ in range(n)]
-        for i in range(n):
-            ev[i][0].record(stream)
-            for j, c in enumerate(calls):
-                rc = c()
-                if rc:
-                    raise RuntimeError(f"{c.__name__} failed with status {rc}")
-                ev[i][j + 1].record(stream)
-        torch.cuda.synchronize()
-        return [np.array([ev[i][j].elapsed_time(ev[i][j + 1]) for i in range(n)])
-                for j in range(len(calls))]
+    timed = make_timed(args)(stream)
 
     t_lr, t_fs = timed([layer_rel, fuse_sel], n_ev)
     assert torch.equal(keep_buf, pr.keep_idx), "two-call and e2s_prune results differ"
@@ -470,10 +664,13 @@ def main():
     t_c = time.perf_counter()
     done = 0
     passes = 0
+    first_pass = []
     while True:
         for b in range(B):
-            O.prune_image(q_np[b], k_np[b], cfg.grid_h, cfg.grid_w, cfg.keep, cfg.cells, cfg.lam,
-                          args.mode)
+            ref = O.prune_image(q_np[b], k_np[b], cfg.grid_h, cfg.grid_w, cfg.keep, cfg.cells,
+                                cfg.lam, args.mode)
+            if passes == 0:
+                first_pass.append(ref)
             done += 1
             if time.perf_counter() - t_c >= args.cpu_seconds and done >= 8:
                 break
@@ -484,6 +681,16 @@ def main():
     cpu_value = done / cpu_s
     log(f"[bench] oracle: {done} images in {cpu_s:.1f}s on {used} threads ({cores} cores, "
         f"{cpu_model()})")
+    # the step's results on the images the oracle processed, against its results
+    fused_full = torch.empty((B, N, 3), device="cuda")
+    kept_full = pr(qd, kd, fused_full).cpu().numpy()
+    head_sample = list(range(len(first_pass)))
+    parity = parity_summary(cfg, first_pass, head_sample, {cfg.lam: kept_full},
+                            fused_full.cpu().numpy())
+    parity["images"] = f"0..{len(first_pass) - 1}"
+    log(f"[bench] parity on {len(first_pass)} images: {parity}")
+    if not args.no_configs:
+        extras["configs"] = bench_configs(args, make_timed(args))
 
     out = {
         "metric": METRIC,
@@ -528,6 +735,7 @@ def main():
                       "staged_fuse": round(float(t_fuse.mean()) * 1e3, 2),
                       "staged_select": round(float(t_sel.mean()) * 1e3, 2)},
         "path_hbm_frac": round(B * per_img_qk / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "parity": parity,
         "cpu_baseline": {
             "value": round(cpu_value, 2),
             "unit": "images/s",

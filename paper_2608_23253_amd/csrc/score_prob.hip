@@ -22,12 +22,15 @@
 // so u_n = N r_n - 1 = (1/N_T) sum_t expm1(z[t,n] s - c_t - L_t) is accumulated in
 // centred form; e_n = u_n / (2 (2 + u_n)), r_n = (1 + u_n) / N.
 //
-// Near uniform attention (every |z s - c_t| <= 1/8, the regime of Gaussian keys
-// at the 1/sqrt(d) scale) expm1 is a short Taylor series: degree 5 in pass 1
-// (|x| <= 1/8) and degree 6 in pass 2 (|x - L_t| <= 1/4, since L_t lies between
-// the smallest and largest x), each truncated below one float32 ulp.  That costs
-// about seven vector operations per logit and pass: the products run on the
-// matrix cores and the kernel is bound by this elementwise work.  When some
+// Near uniform attention expm1 is a short Taylor series.  In the tight range
+// (every |z s - c_t| <= 1/16, the regime of Gaussian keys at the 1/sqrt(d)
+// scale) both passes take it to degree 4 (degree 5 in pass 2 when some |L_t|
+// widens its range past 1/16), each product started from minus its query's shift
+// in the matrix core's accumulator, so the series reads the product directly:
+// about four vector operations per logit and pass.  Up to 1/8 pass 1 is redone
+// with the degree-5 series and pass 2 takes degree 6 (|x - L_t| <= 1/4, since
+// L_t lies between the smallest and largest x); every truncation stays below one
+// float32 ulp of the term at the range's edge.  When some
 // logit of a query chunk lies further out (peaked attention), the chunk's
 // statistics are recomputed online with the running maximum as reference
 // (m_t = max_n z s, rescaled as it grows; S_t and E_t relative to it) and pass 2
@@ -164,6 +167,8 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
     float* wpart = st_c + qcap;                                  // [kWaves][qcap][4]
     float* lstat = wpart + kWaves * qcap * 4;                    // [3][qbcap][kThreads]
     __shared__ int s_far;                                        // some |z s - c_t| > 1/8
+    __shared__ unsigned s_amax;                                  // max |z - c_t| (float bits)
+    __shared__ unsigned s_lmax;                                  // max |L_t| (float bits)
 
     const int64_t bid = xcd_remap(blockIdx.x, nblocks);          // (b*L + l)*H + h
     const int64_t b = bid / (bg.L * bg.H);
@@ -242,7 +247,11 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
             *reinterpret_cast<f32x4v*>(qs + row * QS + c * EPV) = v;
         }
         for (int qb = 0; qb < QB; ++qb) lE[qb * kThreads] = 0.f;
-        if (tid == 0) s_far = 0;
+        if (tid == 0) {
+            s_far = 0;
+            s_amax = 0u;
+            s_lmax = 0u;
+        }
         __syncthreads();
 
         // ---- reference of each query (block_reference); zero query rows past
@@ -259,37 +268,62 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
         }
         __syncthreads();
 
-        // ---- pass 1: E_t = sum_n expm1(s y) with y = z - c_t / s, by the degree-5
-        // series; groups of keys double-buffered
+        // ---- pass 1: E_t = sum_n expm1(s y) with y = z - c_t / s; groups of keys
+        // double-buffered.  First by the degree-4 series with each product started
+        // from -c_t (the tight range, |s y| <= 1/16, checked afterwards), else again
+        // by the degree-5 series (|s y| <= 1/8), else online (below).
         const ScaledSeries<5> p5(scale);
         const ScaledSeries<6> p6(scale);
+        const ScaledSeries<4> p4(scale);
         float amax = 0.f;                                         // largest |y| seen
-        auto pass1_group = [&](const AFrag (&a)[TG][NA], int j, auto whole) {
+        auto pass1_group = [&](const AFrag (&a)[TG][NA], int j, auto whole, auto tight) {
             for (int qb = 0; qb < QB; ++qb) {
                 AFrag bq[NA];
                 load_queries<D>(bq, qs, qb * 16, lr, lg);
                 const float cz = st_c[qb * 16 + lr];
                 float E = lE[qb * kThreads];
+                if constexpr (decltype(tight)::value) {
+                    const f32x4v init = {-cz, -cz, -cz, -cz};
 #pragma unroll
-                for (int tt = 0; tt < TG; ++tt)
-                    prob::series_tile<decltype(whole)::value>(tile_mma<NA>(a[tt], bq), cz,
-                                                              tile_of(j, tt) * 16 + 4 * lg, N,
-                                                              p5, E, amax);
+                    for (int tt = 0; tt < TG; ++tt)
+                        prob::tight_series_tile<decltype(whole)::value>(
+                            tile_mma<NA>(a[tt], bq, init), tile_of(j, tt) * 16 + 4 * lg, N, p4, E,
+                            amax);
+                } else {
+#pragma unroll
+                    for (int tt = 0; tt < TG; ++tt)
+                        prob::series_tile<decltype(whole)::value>(tile_mma<NA>(a[tt], bq), cz,
+                                                                  tile_of(j, tt) * 16 + 4 * lg, N,
+                                                                  p5, E, amax);
+                }
                 lE[qb * kThreads] = E;
             }
         };
-        stream_groups([&](const AFrag (&a)[TG][NA], int j) {
-            // the group's last tile ends at or before N: no key of the group is masked
-            // (tile_of is the same for every lane of the wave)
-            if (__builtin_amdgcn_readfirstlane(tile_of(j, TG - 1)) * 16 + 16 <= N)
-                pass1_group(a, j, std::true_type{});
-            else
-                pass1_group(a, j, std::false_type{});
-        });
-        // |s y| <= 1/8 everywhere keeps the series within its range
-        if (!(wave_max(amax) * scale <= kSeriesRange) && lane == 0) atomicOr(&s_far, 1);
+        auto pass1 = [&](auto tight) {
+            stream_groups([&](const AFrag (&a)[TG][NA], int j) {
+                // the group's last tile ends at or before N: no key of the group is
+                // masked (tile_of is the same for every lane of the wave)
+                if (__builtin_amdgcn_readfirstlane(tile_of(j, TG - 1)) * 16 + 16 <= N)
+                    pass1_group(a, j, std::true_type{}, tight);
+                else
+                    pass1_group(a, j, std::false_type{}, tight);
+            });
+        };
+        pass1(std::true_type{});
+        {
+            // (non-negative floats order as their bits)
+            const float wmax = wave_max(amax);
+            if (lane == 0) atomicMax(&s_amax, __float_as_uint(wmax));
+        }
         __syncthreads();
-        const bool far = s_far != 0;
+        const float amax_s = __uint_as_float(s_amax) * scale;
+        const bool tight = amax_s <= prob::kTightRange;
+        // |s y| <= 1/8 everywhere keeps the degree-5 series within its range
+        const bool far = !(amax_s <= kSeriesRange);
+        if (!tight && !far) {
+            for (int qb = 0; qb < QB; ++qb) lE[qb * kThreads] = 0.f;
+            pass1(std::false_type{});
+        }
 
         if (!far) {
             // ---- merge the series sums: the 4 lane groups, then the waves ----
@@ -303,7 +337,14 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
             if (tid < QB * 16) {
                 float e = 0.f;
                 for (int w = 0; w < kWaves; ++w) e += wpart[(w * qcap + tid) * 4];
-                st_m[tid] = (tid < rows) ? prob::near_shift(st_c[tid], e, scale, fN) : 0.f;
+                // the shift of pass 2 in logit units: c_t + L_t / s
+                float L = 0.f, sh = 0.f;
+                if (tid < rows) {
+                    L = log1pf((scale * e) / fN);
+                    sh = st_c[tid] + L / scale;
+                }
+                st_m[tid] = sh;
+                atomicMax(&s_lmax, __float_as_uint(fabsf(L)));
             }
         } else {
             // ---- pass 1 again, online, tile by tile: running maximum as the
@@ -369,7 +410,33 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
                 }
             }
         };
-        if (!far) {
+        // tight: |s (z - shift)| <= amax_s + max |L_t| <= 1/8 (|L_t| <= amax_s), the
+        // products started from -shift: the degree-4 series up to 1/16, else degree 5
+        auto pass2_tight = [&](const auto& series) {
+            stream_groups([&](const AFrag (&a)[TG][NA], int j) {
+                float col[TG][4];
+#pragma unroll
+                for (int tt = 0; tt < TG; ++tt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) col[tt][r] = 0.f;
+                for (int qb = 0; qb < QB; ++qb) {
+                    AFrag bq[NA];
+                    load_queries<D>(bq, qs, qb * 16, lr, lg);
+                    const float sz = st_m[qb * 16 + lr];
+                    const f32x4v init = {-sz, -sz, -sz, -sz};
+#pragma unroll
+                    for (int tt = 0; tt < TG; ++tt)
+                        prob::column_tight_tile(tile_mma<NA>(a[tt], bq, init), series, col[tt]);
+                }
+                add_columns(reinterpret_cast<const float(&)[TG * 4]>(col), j, scale);
+            });
+        };
+        if (tight) {
+            if (amax_s + __uint_as_float(s_lmax) <= prob::kTightRange)
+                pass2_tight(p4);
+            else
+                pass2_tight(p5);
+        } else if (!far) {
             // y = z - shift; |s y| <= 1/4: the degree-6 series; the column sums are
             // in units of s
             stream_groups([&](const AFrag (&a)[TG][NA], int j) {

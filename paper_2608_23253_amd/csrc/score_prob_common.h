@@ -71,6 +71,36 @@ __device__ __forceinline__ f32x4v tile_mma(const float (&a)[NA], const float (&b
     return acc;
 }
 
+// The same product started from the accumulator `acc` instead of zero: with acc
+// holding minus a per-query shift, the tile comes out already centred.
+template <int NA>
+__device__ __forceinline__ f32x4v tile_mma(const bf16x8 (&a)[NA], const bf16x8 (&b)[NA],
+                                           f32x4v acc) {
+#pragma unroll
+    for (int s = 0; s < NA; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s], b[s], acc, 0, 0, 0);
+    return acc;
+}
+template <int NA>
+__device__ __forceinline__ f32x4v tile_mma(const f16x8 (&a)[NA], const f16x8 (&b)[NA],
+                                           f32x4v acc) {
+#pragma unroll
+    for (int s = 0; s < NA; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[s], b[s], acc, 0, 0, 0);
+    return acc;
+}
+template <int NA>
+__device__ __forceinline__ f32x4v tile_mma(const float (&a)[NA], const float (&b)[NA],
+                                           f32x4v acc) {
+#pragma unroll
+    for (int s = 0; s < NA; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s], acc, 0, 0, 0);
+    return acc;
+}
+
+// Range of the tight path: every centred logit |s (z - c_t)| of a query chunk
+// within 1/16.  There expm1 to degree 4 (terms up to x^4 / 24) truncates below
+// x^5 / 120, i.e. 1.3e-7 of the term at the edge and far less for the bulk of the
+// logits (about 1/100 at the workloads' scale).
+constexpr float kTightRange = 0.0625f;
+
 // Reference of a query (in logit units, before the scale): the mean logit
 // Q_t.K_n over keys 0..15, summed pairwise so that equal logits give exactly
 // their value, or key 0's logit when N < 16.  z: the product of key tile 0 with
@@ -98,6 +128,22 @@ __device__ __forceinline__ void series_tile(const f32x4v& z, float cz, int key0,
         if (!full) y = (key0 + r < N) ? y : 0.f;
         amax = fmaxf(amax, fabsf(y));
         E = fmaf(p5(y), y, E);
+    }
+}
+
+// Pass 1, tight range: the same sum by the degree-4 series on the product z
+// started from -c_t (so z is already y); amax tracks |y| to confirm |s y| <= 1/16.
+template <bool WHOLE>
+__device__ __forceinline__ void tight_series_tile(const f32x4v& z, int key0, int N,
+                                                  const ScaledSeries<4>& p4, float& E,
+                                                  float& amax) {
+    const bool full = WHOLE || key0 + 4 <= N;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        float y = z[r];
+        if (!full) y = (key0 + r < N) ? y : 0.f;
+        amax = fmaxf(amax, fabsf(y));
+        E = fmaf(p4(y), y, E);
     }
 }
 
@@ -211,6 +257,15 @@ __device__ __forceinline__ void column_series_tile(const f32x4v& z, float sz,
         const float y = z[r] - sz;
         col[r] = fmaf(p6(y), y, col[r]);
     }
+}
+
+// Pass 2, tight range: col += expm1(s y) / s = y P(y) on the product started from
+// -shift (z is already y), by the given series.
+template <typename Series>
+__device__ __forceinline__ void column_tight_tile(const f32x4v& z, const Series& p,
+                                                  float (&col)[4]) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) col[r] = fmaf(p(z[r]), z[r], col[r]);
 }
 
 // Pass 2, peaked attention: col += expm1(x) with x = z s - shift, by the series

@@ -185,6 +185,10 @@ e2s_status check_compact(const e2s_compact_shape* s) {
     double src_end = s->channels, dst_end = s->channels;
     for (int i = 0; i < 3; ++i) {
         if (s->src_stride[i] < 0 || s->dst_stride[i] < 0) return E2S_ERR_BAD_SHAPE;
+        // (the products below stay in range: elem_bytes <= 4)
+        if (s->src_stride[i] > std::numeric_limits<int64_t>::max() / 16 ||
+            s->dst_stride[i] > std::numeric_limits<int64_t>::max() / 16)
+            return E2S_ERR_BAD_SHAPE;
         if ((s->src_stride[i] * s->elem_bytes) % 16 != 0 ||
             (s->dst_stride[i] * s->elem_bytes) % 16 != 0)
             return E2S_ERR_MISALIGNED;

@@ -25,9 +25,11 @@
 // Near uniform attention expm1 is a short Taylor series.  In the tight range
 // (every |z s - c_t| <= 1/16, the regime of Gaussian keys at the 1/sqrt(d)
 // scale) both passes take it to degree 4 (degree 5 in pass 2 when some |L_t|
-// widens its range past 1/16), each product started from minus its query's shift
-// in the matrix core's accumulator, so the series reads the product directly:
-// about four vector operations per logit and pass.  Up to 1/8 pass 1 is redone
+// widens its range past 1/16), about five vector operations per logit and pass.
+// The reference is subtracted from the product after the matrix core, not
+// started in its accumulator: a product started from -c_t rounds differently from
+// the product minus c_t, and exactly uniform attention (identical keys) would then
+// give supports of ~1e-11 instead of exactly 0.  Up to 1/8 pass 1 is redone
 // with the degree-5 series and pass 2 takes degree 6 (|x - L_t| <= 1/4, since
 // L_t lies between the smallest and largest x); every truncation stays below one
 // float32 ulp of the term at the range's edge.  When some
@@ -269,9 +271,9 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
         __syncthreads();
 
         // ---- pass 1: E_t = sum_n expm1(s y) with y = z - c_t / s; groups of keys
-        // double-buffered.  First by the degree-4 series with each product started
-        // from -c_t (the tight range, |s y| <= 1/16, checked afterwards), else again
-        // by the degree-5 series (|s y| <= 1/8), else online (below).
+        // double-buffered.  First by the degree-4 series (the tight range,
+        // |s y| <= 1/16, checked afterwards), else again by the degree-5 series
+        // (|s y| <= 1/8), else online (below).
         const ScaledSeries<5> p5(scale);
         const ScaledSeries<6> p6(scale);
         const ScaledSeries<4> p4(scale);
@@ -283,12 +285,11 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
                 const float cz = st_c[qb * 16 + lr];
                 float E = lE[qb * kThreads];
                 if constexpr (decltype(tight)::value) {
-                    const f32x4v init = {-cz, -cz, -cz, -cz};
 #pragma unroll
                     for (int tt = 0; tt < TG; ++tt)
-                        prob::tight_series_tile<decltype(whole)::value>(
-                            tile_mma<NA>(a[tt], bq, init), tile_of(j, tt) * 16 + 4 * lg, N, p4, E,
-                            amax);
+                        prob::series_tile<decltype(whole)::value>(tile_mma<NA>(a[tt], bq), cz,
+                                                                  tile_of(j, tt) * 16 + 4 * lg, N,
+                                                                  p4, E, amax);
                 } else {
 #pragma unroll
                     for (int tt = 0; tt < TG; ++tt)
@@ -410,8 +411,8 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
                 }
             }
         };
-        // tight: |s (z - shift)| <= amax_s + max |L_t| <= 1/8 (|L_t| <= amax_s), the
-        // products started from -shift: the degree-4 series up to 1/16, else degree 5
+        // tight: |s (z - shift)| <= amax_s + max |L_t| <= 1/8 (|L_t| <= amax_s): the
+        // degree-4 series up to 1/16, else degree 5
         auto pass2_tight = [&](const auto& series) {
             stream_groups([&](const AFrag (&a)[TG][NA], int j) {
                 float col[TG][4];
@@ -423,10 +424,9 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
                     AFrag bq[NA];
                     load_queries<D>(bq, qs, qb * 16, lr, lg);
                     const float sz = st_m[qb * 16 + lr];
-                    const f32x4v init = {-sz, -sz, -sz, -sz};
 #pragma unroll
                     for (int tt = 0; tt < TG; ++tt)
-                        prob::column_tight_tile(tile_mma<NA>(a[tt], bq, init), series, col[tt]);
+                        prob::column_series_tile(tile_mma<NA>(a[tt], bq), sz, series, col[tt]);
                 }
                 add_columns(reinterpret_cast<const float(&)[TG * 4]>(col), j, scale);
             });

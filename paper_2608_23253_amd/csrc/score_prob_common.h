@@ -71,30 +71,6 @@ __device__ __forceinline__ f32x4v tile_mma(const float (&a)[NA], const float (&b
     return acc;
 }
 
-// The same product started from the accumulator `acc` instead of zero: with acc
-// holding minus a per-query shift, the tile comes out already centred.
-template <int NA>
-__device__ __forceinline__ f32x4v tile_mma(const bf16x8 (&a)[NA], const bf16x8 (&b)[NA],
-                                           f32x4v acc) {
-#pragma unroll
-    for (int s = 0; s < NA; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[s], b[s], acc, 0, 0, 0);
-    return acc;
-}
-template <int NA>
-__device__ __forceinline__ f32x4v tile_mma(const f16x8 (&a)[NA], const f16x8 (&b)[NA],
-                                           f32x4v acc) {
-#pragma unroll
-    for (int s = 0; s < NA; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a[s], b[s], acc, 0, 0, 0);
-    return acc;
-}
-template <int NA>
-__device__ __forceinline__ f32x4v tile_mma(const float (&a)[NA], const float (&b)[NA],
-                                           f32x4v acc) {
-#pragma unroll
-    for (int s = 0; s < NA; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s], acc, 0, 0, 0);
-    return acc;
-}
-
 // Range of the tight path: every centred logit |s (z - c_t)| of a query chunk
 // within 1/16.  There expm1 to degree 4 (terms up to x^4 / 24) truncates below
 // x^5 / 120, i.e. 1.3e-7 of the term at the edge and far less for the bulk of the
@@ -113,37 +89,22 @@ __device__ __forceinline__ float block_reference(const f32x4v& z, int N, int lr)
     return (N >= 16) ? sum * (1.0f / 16.0f) : z0;
 }
 
-// Pass 1, near uniform: E += expm1(s y) = s y P5(y) (in units of s) for the
-// tile's logits with y = z - c_t / s; keys past N count as y = 0.  amax: the
-// largest |y| seen, to confirm afterwards that |s y| <= 1/8 held.  WHOLE: the
-// caller knows that every key of the tile is below N (the same arithmetic without
-// the masking).
-template <bool WHOLE>
+// Pass 1, near uniform: E += expm1(s y) = s y P(y) (in units of s) for the
+// tile's logits with y = z - c_t / s; keys past N count as y = 0.  P: the
+// degree-4 series in the tight range (|s y| <= 1/16), else degree 5 (<= 1/8).
+// amax: the largest |y| seen, to confirm afterwards that the range held.  WHOLE:
+// the caller knows that every key of the tile is below N (the same arithmetic
+// without the masking).
+template <bool WHOLE, typename Series>
 __device__ __forceinline__ void series_tile(const f32x4v& z, float cz, int key0, int N,
-                                            const ScaledSeries<5>& p5, float& E, float& amax) {
+                                            const Series& p, float& E, float& amax) {
     const bool full = WHOLE || key0 + 4 <= N;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         float y = z[r] - cz;
         if (!full) y = (key0 + r < N) ? y : 0.f;
         amax = fmaxf(amax, fabsf(y));
-        E = fmaf(p5(y), y, E);
-    }
-}
-
-// Pass 1, tight range: the same sum by the degree-4 series on the product z
-// started from -c_t (so z is already y); amax tracks |y| to confirm |s y| <= 1/16.
-template <bool WHOLE>
-__device__ __forceinline__ void tight_series_tile(const f32x4v& z, int key0, int N,
-                                                  const ScaledSeries<4>& p4, float& E,
-                                                  float& amax) {
-    const bool full = WHOLE || key0 + 4 <= N;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        float y = z[r];
-        if (!full) y = (key0 + r < N) ? y : 0.f;
-        amax = fmaxf(amax, fabsf(y));
-        E = fmaf(p4(y), y, E);
+        E = fmaf(p(y), y, E);
     }
 }
 
@@ -248,24 +209,17 @@ __device__ __forceinline__ float online_shift(const float* p, int stride, float 
     return M + log_mean_exp(e, s, fN);
 }
 
-// Pass 2, near uniform: col += expm1(s y) / s = y P6(y) with y = z - shift
-// (|s y| <= 1/4), per key of the tile, over the query blocks in order.
-__device__ __forceinline__ void column_series_tile(const f32x4v& z, float sz,
-                                                   const ScaledSeries<6>& p6, float (&col)[4]) {
+// Pass 2, near uniform: col += expm1(s y) / s = y P(y) with y = z - shift, per key
+// of the tile, over the query blocks in order; P: the degree-6 series (|s y| <=
+// 1/4), or in the tight range degree 4 (|s y| <= 1/16) or 5 (<= 1/8).
+template <typename Series>
+__device__ __forceinline__ void column_series_tile(const f32x4v& z, float sz, const Series& p,
+                                                   float (&col)[4]) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const float y = z[r] - sz;
-        col[r] = fmaf(p6(y), y, col[r]);
+        col[r] = fmaf(p(y), y, col[r]);
     }
-}
-
-// Pass 2, tight range: col += expm1(s y) / s = y P(y) on the product started from
-// -shift (z is already y), by the given series.
-template <typename Series>
-__device__ __forceinline__ void column_tight_tile(const f32x4v& z, const Series& p,
-                                                  float (&col)[4]) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) col[r] = fmaf(p(z[r]), z[r], col[r]);
 }
 
 // Pass 2, peaked attention: col += expm1(x) with x = z s - shift, by the series

@@ -515,7 +515,8 @@ def bench_configs(args, make_timed):
             ips, used, refs = cpu_baseline_leg(cfg, mode, q_s, k_s, sample)
             rec["cpu_baseline"] = {"value": round(ips, 2), "unit": "images/s", "cores": used,
                                    "kind": "oracle",
-                                   "sample": f"images {sample} of the batch, mode {mode}"}
+                                   "sample": f"images {[int(i) for i in sample]} of the batch, "
+                                             f"mode {mode}"}
             rec["parity"] = parity_summary(cfg, refs, sample, kept_by_lam, fused_h)
             log(f"[bench] {name}/{mode}: {step_us:.1f} us/step ({rec['images_per_s']:.0f} "
                 f"images/s), stage {stage_us:.1f} us, tail {tail_us:.1f} us, "

@@ -66,6 +66,7 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
 }
 
 constexpr int64_t kColumnsInLds = 16384;
+constexpr size_t kLdsPerCu = 160 * 1024;
 
 template <typename T, int D> struct ProbCfg;
 template <int D> struct ProbCfg<uint16_t, D> {
@@ -150,9 +151,14 @@ __device__ __forceinline__ void load_queries(float (&b)[D / 4], const float* qs,
 }
 
 // TG key tiles per group, two groups in flight per wave: 4 tiles (2 workgroups per
-// CU by registers) when a chunk has 8 query blocks, else 2 (3 per CU).
+// CU by registers) when a chunk has 8 query blocks, else 2 (3 per CU) or 1 (4 per
+// CU with 16-bit keys, where the LDS allows it; fp32 keys always take 1, 3 per CU).
+template <typename T, int D, int TG>
+constexpr int mp_workgroups_per_cu() {
+    return TG >= 4 ? 2 : (TG == 1 && !std::is_same<T, float>::value ? 4 : 3);
+}
 template <typename T, int D, int TG, bool GLOBAL>
-__global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_kernel(
+__global__ __launch_bounds__(kThreads, (mp_workgroups_per_cu<T, D, TG>())) void score_mean_prob_kernel(
     const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
     float* __restrict__ r_out, BatchGeom bg, int group, float scale, int nblocks, int qcap,
     bool cols_over_stats) {
@@ -168,7 +174,6 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
     float* st_c = st_m + qcap;                                   // [qcap] reference c_t
     float* wpart = st_c + qcap;                                  // [kWaves][qcap][4]
     float* lstat = wpart + kWaves * qcap * 4;                    // [3][qbcap][kThreads]
-    __shared__ int s_far;                                        // some |z s - c_t| > 1/8
     __shared__ unsigned s_amax;                                  // max |z - c_t| (float bits)
     __shared__ unsigned s_lmax;                                  // max |L_t| (float bits)
 
@@ -250,7 +255,6 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
         }
         for (int qb = 0; qb < QB; ++qb) lE[qb * kThreads] = 0.f;
         if (tid == 0) {
-            s_far = 0;
             s_amax = 0u;
             s_lmax = 0u;
         }
@@ -486,18 +490,25 @@ __global__ __launch_bounds__(kThreads, TG >= 4 ? 2 : 3) void score_mean_prob_ker
     }
 }
 
+// LDS of one workgroup: the column sums in LDS up to kColumnsInLds keys, else in
+// the output rows; in the statistics' place when every head has one query chunk
+// and they fit (over).
+template <typename T, int D>
+size_t mp_lds(const Dims& d, int qcap, bool& global, bool& over) {
+    using C = ProbCfg<T, D>;
+    global = d.N > kColumnsInLds;
+    const int64_t stats = 3 * (qcap / 16) * kThreads;            // floats
+    over = !global && d.NT <= qcap && d.N <= stats;
+    return static_cast<size_t>(qcap) * C::QS * sizeof(T) +
+           (2 * qcap + kWaves * qcap * 4 + stats) * sizeof(float) +
+           (global || over ? 0 : static_cast<size_t>(d.N) * sizeof(float));
+}
+
 template <typename T, int D, int TG>
 hipError_t launch_mp(const Dims& d, float scale, const void* q, const void* k, float* e,
                      float* r, int qcap, hipStream_t st) {
-    using C = ProbCfg<T, D>;
-    // the column sums in LDS up to kColumnsInLds keys, else in the output rows; in
-    // the statistics' place when every head has one query chunk and they fit
-    const bool global = d.N > kColumnsInLds;
-    const int64_t stats = 3 * (qcap / 16) * kThreads;            // floats
-    const bool over = !global && d.NT <= qcap && d.N <= stats;
-    const size_t lds = static_cast<size_t>(qcap) * C::QS * sizeof(T) +
-                       (2 * qcap + kWaves * qcap * 4 + stats) * sizeof(float) +
-                       (global || over ? 0 : static_cast<size_t>(d.N) * sizeof(float));
+    bool global = false, over = false;
+    const size_t lds = mp_lds<T, D>(d, qcap, global, over);
     auto kern = global ? score_mean_prob_kernel<T, D, TG, true>
                        : score_mean_prob_kernel<T, D, TG, false>;
     if (lds > 64 * 1024) {
@@ -523,8 +534,14 @@ hipError_t dispatch_mp(const Dims& d, float scale, const void* q, const void* k,
     if constexpr (std::is_same<T, float>::value) {
         return launch_mp<T, D, 1>(d, scale, q, k, e, r, qcap, st);
     } else {
-        // measured: 4 tiles per group pays when a chunk has 8 query blocks
+        // measured: 4 tiles per group pays when a chunk has 8 query blocks; one tile
+        // per group (114 VGPRs: 4 workgroups per CU) when the LDS also leaves room
+        // for 4 (the LLaVA shape: 34 KiB, stage 413 -> 397 us), else 2 (Qwen2-VL:
+        // 50 KiB, 3 per CU, where one tile measured 284 -> 293 us)
         if (qcap >= 128) return launch_mp<T, D, 4>(d, scale, q, k, e, r, qcap, st);
+        bool global = false, over = false;
+        if (4 * mp_lds<T, D>(d, qcap, global, over) <= kLdsPerCu)
+            return launch_mp<T, D, 1>(d, scale, q, k, e, r, qcap, st);
         return launch_mp<T, D, 2>(d, scale, q, k, e, r, qcap, st);
     }
 }

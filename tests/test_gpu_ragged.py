@@ -270,10 +270,11 @@ def test_ragged_validation_on_device_pointers():
 
 @pytest.mark.parametrize("heavy", [False, True], ids=["near_uniform", "peaked"])
 def test_mean_prob_group_size_does_not_change_bits(heavy):
-    """The mean-of-probabilities kernel takes 2 key tiles at a time when a query chunk
-    holds at most 112 queries and 4 when it holds 128; an image's bits must not
-    depend on which.  40 images with N_T <= 64 alone run with 2; one more image with
-    N_T = 130 (two query chunks) makes the same images run with 4."""
+    """The mean-of-probabilities kernel takes 4 key tiles at a time when a query chunk
+    holds 128 queries, else 1 when four workgroups' LDS fits a CU and 2 when it does
+    not; an image's bits must not depend on which.  40 images with N_T <= 64 alone
+    run with 1 (34 KiB per workgroup); one more image with N_T = 96 (51 KiB) makes
+    the same images run with 2, one with N_T = 130 (two query chunks) with 4."""
     extra = dict(value_std=2.0, shift_sigmas=4.0) if heavy else {}
     cfg = _base("mp_group_size", config_id=79 + int(heavy), num_layers=2, num_heads=8,
                 num_kv_heads=2, head_dim=128, salient_count=5, **extra)
@@ -284,18 +285,21 @@ def test_mean_prob_group_size_does_not_change_bits(heavy):
     dims[0] = (24, 24, 64, 100)
     log(f"[case] mean_prob group size heavy={heavy}")
     imgs, arr_a, keep_a, fused_a, prio_a = _run(cfg, dims, 2, "mean_prob")
-    _, arr_b, keep_b, fused_b, prio_b = _run(cfg, dims + [(6, 6, 130, 5)], 2, "mean_prob")
     keep_a, fused_a, prio_a = keep_a.cpu().numpy(), fused_a.cpu().numpy(), prio_a.cpu().numpy()
-    keep_b, fused_b, prio_b = keep_b.cpu().numpy(), fused_b.cpu().numpy(), prio_b.cpu().numpy()
-    for b, (gh, gw, nt, K) in enumerate(dims):
-        a, c = arr_a[b], arr_b[b]
-        n = gh * gw
-        np.testing.assert_array_equal(fused_a[a.token_offset:a.token_offset + n],
-                                      fused_b[c.token_offset:c.token_offset + n])
-        np.testing.assert_array_equal(prio_a[a.token_offset:a.token_offset + n],
-                                      prio_b[c.token_offset:c.token_offset + n])
-        assert keep_a[a.keep_offset:a.keep_offset + K].tolist() == \
-            keep_b[c.keep_offset:c.keep_offset + K].tolist()
+    for extra_nt in (96, 130):
+        _, arr_b, keep_b, fused_b, prio_b = _run(cfg, dims + [(6, 6, extra_nt, 5)], 2,
+                                                 "mean_prob")
+        keep_b, fused_b = keep_b.cpu().numpy(), fused_b.cpu().numpy()
+        prio_b = prio_b.cpu().numpy()
+        for b, (gh, gw, nt, K) in enumerate(dims):
+            a, c = arr_a[b], arr_b[b]
+            n = gh * gw
+            np.testing.assert_array_equal(fused_a[a.token_offset:a.token_offset + n],
+                                          fused_b[c.token_offset:c.token_offset + n])
+            np.testing.assert_array_equal(prio_a[a.token_offset:a.token_offset + n],
+                                          prio_b[c.token_offset:c.token_offset + n])
+            assert keep_a[a.keep_offset:a.keep_offset + K].tolist() == \
+                keep_b[c.keep_offset:c.keep_offset + K].tolist()
     for b in (0, 17, 33):
         gh, gw, nt, K = dims[b]
         qb, kb = imgs[b]

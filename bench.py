@@ -10,9 +10,10 @@ with images/s, a roofline object for the dominant kernel (the score and
 reliability stage, timed alone with HIP events on the launch stream), per-stage
 times of the staged entry points, the ablation variants, the progressive
 schedule, a ragged batch (e2s_prune_ragged on seeded dynamic-resolution images),
-token compaction of the kept tokens (e2s_compact_tokens) and the CPU oracle's
-throughput on a bounded sample, with a parity summary of the step's results on
-the images the oracle processed.
+token compaction of the kept tokens (e2s_compact_tokens), the step rate with two
+batches in flight on two streams (`pipelined`: a serving loop's rate; `value`
+stays the one-stream rate) and the CPU oracle's throughput on a bounded sample,
+with a parity summary of the step's results on the images the oracle processed.
 
 `configs` repeats the measurement for the other workloads and readings at their
 full batches (the aggressive LLaVA workload for each lambda of its sweep): step
@@ -530,6 +531,44 @@ def bench_configs(args, make_timed):
     return out
 
 
+def bench_pipelined(args, cfg, qd, kd, sets, ref_keep):
+    """Two batches in flight: the steps alternate between two streams (default
+    priority), each with its own Pruner (workspace and outputs), so that a step's
+    selection tail can run beside the next step's score stage, as in a serving loop
+    that prunes batch after batch.  Wall clock over as many steps as the metric;
+    every step's kept indices are those of the one-stream step (same inputs)."""
+    import torch
+    import paper_2608_23253_amd as E
+    prs = [E.Pruner(qd, kd, cfg.grid_h, cfg.grid_w, cfg.keep, cfg.cells, cfg.lam, args.mode)
+           for _ in range(2)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    cur = torch.cuda.current_stream()
+    for s in streams:
+        s.wait_stream(cur)
+
+    def run(n):
+        for i in range(n):
+            qx, kx = sets.next()
+            prs[i % 2](qx, kx, stream=streams[i % 2].cuda_stream)
+
+    run(max(args.warmup, 2))
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    run(args.steps)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t
+    for p in prs:
+        assert torch.equal(p.keep_idx, ref_keep), "pipelined steps changed the kept sets"
+    us = wall * 1e6 / args.steps
+    B = cfg.batch
+    log(f"[bench] two batches in flight (2 streams): {us:.1f} us/step, "
+        f"{B / (us * 1e-6):.0f} images/s")
+    return {"streams": 2, "steps": args.steps, "us_per_step": round(us, 2),
+            "images_per_s": round(B / (us * 1e-6), 1),
+            "path_hbm_frac": round(B * cfg.bytes_per_image() / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                                   4)}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -655,6 +694,7 @@ def main():
         extras = bench_variants_and_schedule(args, cfg, qd, kd, stream, timed)
         extras["ragged"] = bench_ragged(args, timed)
         extras["compaction"] = bench_compaction(args, timed, kd, pr.keep_idx)
+        extras["pipelined"] = bench_pipelined(args, cfg, qd, kd, sets, pr.keep_idx)
 
     # ---- CPU oracle baseline ----------------------------------------------------
     import oracle as O

@@ -424,7 +424,8 @@ def make_timed(args):
 
 def bench_configs(args, make_timed):
     """Every other workload at its full batch, both readings: wall-clock step time
-    and images/s per lambda, the two kernels of e2s_prune timed alone with HIP events,
+    and images/s per lambda, the rate with two batches in flight (bench_pipelined,
+    first lambda), the two kernels of e2s_prune timed alone with HIP events,
     the fraction of the binding roofline, the selection tail's bytes and HBM fraction,
     and a sampled parity summary against the oracle."""
     import numpy as np
@@ -467,6 +468,9 @@ def bench_configs(args, make_timed):
                 rec["lambdas"][str(lam)] = {"us_per_step": round(us, 2),
                                             "images_per_s": round(B / (us * 1e-6), 1)}
                 kept_by_lam[lam] = pr(qd, kd).cpu().numpy()
+            rec["pipelined"] = bench_pipelined(
+                cfg, mode, cfg.lam, qd, kd, sets, n_rep, args.warmup,
+                torch.from_numpy(kept_by_lam[cfg.lam]).cuda())
             # the two kernels of e2s_prune at the first lambda, each timed alone
             pr = E.Pruner(qd, kd, gh, gw, cfg.keep, cfg.cells, cfg.lam, mode)
             fused = torch.empty((B, N, 3), device="cuda")
@@ -520,7 +524,8 @@ def bench_configs(args, make_timed):
                                              f"mode {mode}"}
             rec["parity"] = parity_summary(cfg, refs, sample, kept_by_lam, fused_h)
             log(f"[bench] {name}/{mode}: {step_us:.1f} us/step ({rec['images_per_s']:.0f} "
-                f"images/s), stage {stage_us:.1f} us, tail {tail_us:.1f} us, "
+                f"images/s; 2 streams {rec['pipelined']['us_per_step']:.1f} us/step), "
+                f"stage {stage_us:.1f} us, tail {tail_us:.1f} us, "
                 f"{rec['roofline']['path_frac']:.1%} of the {bound} roofline; parity "
                 f"max|d m~| {rec['parity']['max_abs_dfused']:.1e} "
                 f"{rec['parity']['by_lambda']} ({time.time() - t_p:.1f}s)")
@@ -531,7 +536,7 @@ def bench_configs(args, make_timed):
     return out
 
 
-def bench_pipelined(args, cfg, qd, kd, sets, ref_keep):
+def bench_pipelined(cfg, mode, lam, qd, kd, sets, steps, warmup, ref_keep):
     """Two batches in flight: the steps alternate between two streams (default
     priority), each with its own Pruner (workspace and outputs), so that a step's
     selection tail can run beside the next step's score stage, as in a serving loop
@@ -539,7 +544,7 @@ def bench_pipelined(args, cfg, qd, kd, sets, ref_keep):
     every step's kept indices are those of the one-stream step (same inputs)."""
     import torch
     import paper_2608_23253_amd as E
-    prs = [E.Pruner(qd, kd, cfg.grid_h, cfg.grid_w, cfg.keep, cfg.cells, cfg.lam, args.mode)
+    prs = [E.Pruner(qd, kd, cfg.grid_h, cfg.grid_w, cfg.keep, cfg.cells, lam, mode)
            for _ in range(2)]
     streams = [torch.cuda.Stream(), torch.cuda.Stream()]
     cur = torch.cuda.current_stream()
@@ -551,19 +556,17 @@ def bench_pipelined(args, cfg, qd, kd, sets, ref_keep):
             qx, kx = sets.next()
             prs[i % 2](qx, kx, stream=streams[i % 2].cuda_stream)
 
-    run(max(args.warmup, 2))
+    run(max(warmup, 2))
     torch.cuda.synchronize()
     t = time.perf_counter()
-    run(args.steps)
+    run(steps)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t
     for p in prs:
         assert torch.equal(p.keep_idx, ref_keep), "pipelined steps changed the kept sets"
-    us = wall * 1e6 / args.steps
+    us = wall * 1e6 / steps
     B = cfg.batch
-    log(f"[bench] two batches in flight (2 streams): {us:.1f} us/step, "
-        f"{B / (us * 1e-6):.0f} images/s")
-    return {"streams": 2, "steps": args.steps, "us_per_step": round(us, 2),
+    return {"streams": 2, "steps": steps, "us_per_step": round(us, 2),
             "images_per_s": round(B / (us * 1e-6), 1),
             "path_hbm_frac": round(B * cfg.bytes_per_image() / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
                                    4)}
@@ -694,7 +697,11 @@ def main():
         extras = bench_variants_and_schedule(args, cfg, qd, kd, stream, timed)
         extras["ragged"] = bench_ragged(args, timed)
         extras["compaction"] = bench_compaction(args, timed, kd, pr.keep_idx)
-        extras["pipelined"] = bench_pipelined(args, cfg, qd, kd, sets, pr.keep_idx)
+        extras["pipelined"] = bench_pipelined(cfg, args.mode, cfg.lam, qd, kd, sets,
+                                              args.steps, args.warmup, pr.keep_idx)
+        log(f"[bench] two batches in flight (2 streams): "
+            f"{extras['pipelined']['us_per_step']:.1f} us/step, "
+            f"{extras['pipelined']['images_per_s']:.0f} images/s")
 
     # ---- CPU oracle baseline ----------------------------------------------------
     import oracle as O

@@ -33,7 +33,7 @@
 // with the degree-5 series and pass 2 takes degree 6 (|x - L_t| <= 1/4, since
 // L_t lies between the smallest and largest x); every truncation stays within about
 // one float32 ulp of the term at the range's edge (degree 4 at 1/16: x^5 / 120,
-// 1.05 ulp of x) and far below it for the bulk.  When some
+// 1.07 ulp of x) and far below it for the bulk.  When some
 // logit of a query chunk lies further out (peaked attention), the chunk's
 // statistics are recomputed online with the running maximum as reference
 // (m_t = max_n z s, rescaled as it grows; S_t and E_t relative to it) and pass 2

@@ -14,6 +14,9 @@ token compaction of the kept tokens (e2s_compact_tokens), the step rate with two
 batches in flight on two streams (`pipelined`: a serving loop's rate; `value`
 stays the one-stream rate) and the CPU oracle's throughput on a bounded sample,
 with a parity summary of the step's results on the images the oracle processed.
+`device` records the GPU and its achievable streaming-read bandwidth (e2s_read_probe
+over the batch's keys), and `roofline.frac_of_measured_read` the dominant kernel's
+rate against it as well as against the nominal 8 TB/s.
 
 `configs` repeats the measurement for the other workloads and readings at their
 full batches (the aggressive LLaVA workload for each lambda of its sweep): step
@@ -536,6 +539,33 @@ def bench_configs(args, make_timed):
     return out
 
 
+def read_probe_GBps(buf):
+    """Achievable streaming-read bandwidth of the device: e2s_read_probe over `buf`
+    (the batch's keys, larger than the Infinity Cache), timed with events on the
+    current stream; the best of two launch widths, median of 10 launches each."""
+    import torch
+    from paper_2608_23253_amd import _lib as L
+    sink = torch.zeros(1, device=buf.device, dtype=torch.int32)
+    nbytes = buf.numel() * buf.element_size()
+    best = None
+    for wgs in (512, 1024):
+        for _ in range(3):
+            L.read_probe(buf, wgs, sink)
+        ts = []
+        for _ in range(10):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            L.read_probe(buf, wgs, sink)
+            b.record()
+            b.synchronize()
+            ts.append(a.elapsed_time(b) * 1e-3)
+        gbps = nbytes / sorted(ts)[len(ts) // 2] / 1e9
+        if best is None or gbps > best[0]:
+            best = (gbps, wgs)
+    return {"GBps": round(best[0], 1), "bytes": int(nbytes), "workgroups": best[1],
+            "frac_of_nominal": round(best[0] / HBM_PEAK_GBS, 4)}
+
+
 def bench_pipelined(cfg, mode, lam, qd, kd, sets, steps, warmup, ref_keep):
     """Two batches in flight: the steps alternate between two streams (default
     priority), each with its own Pruner (workspace and outputs), so that a step's
@@ -692,6 +722,13 @@ def main():
         f"{t_fs.mean() * 1e3:.1f} us | staged: score {t_score.mean() * 1e3:.1f} us, fuse "
         f"{t_fuse.mean() * 1e3:.1f} us, select {t_sel.mean() * 1e3:.1f} us")
 
+    probe = read_probe_GBps(kd)
+    log(f"[bench] streaming read of the keys ({probe['bytes'] / 1e9:.2f} GB): "
+        f"{probe['GBps']:.0f} GB/s ({probe['frac_of_nominal']:.1%} of 8 TB/s)")
+    props = torch.cuda.get_device_properties(qd.device)
+    device = {"name": props.name, "gcn_arch": getattr(props, "gcnArchName", ""),
+              "compute_units": props.multi_processor_count, "read_probe": probe}
+
     extras = {}
     if not args.no_extras:
         extras = bench_variants_and_schedule(args, cfg, qd, kd, stream, timed)
@@ -776,7 +813,9 @@ def main():
             "launch_us": round(lr_ms * 1e3, 2),
             "mfma_frac_if_eq1_flops": round(flops_eq1 / (lr_ms * 1e-3) / 1e12
                                             / MFMA_BF16_PEAK_TFLOPS, 4),
+            "frac_of_measured_read": round(achieved / probe["GBps"], 4),
         },
+        "device": device,
         "stages_us": {"layer_reliability": round(lr_ms * 1e3, 2),
                       "fuse_select": round(float(t_fs.mean()) * 1e3, 2),
                       "staged_score": round(float(t_score.mean()) * 1e3, 2),

@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define E2S_ABI_VERSION 8
+#define E2S_ABI_VERSION 9
 
 #if defined(__GNUC__) || defined(__clang__)
 #define E2S_API __attribute__((visibility("default")))
@@ -397,6 +397,17 @@ E2S_API e2s_status e2s_prune_views(const e2s_shape* shape, const e2s_params* par
 E2S_API e2s_status e2s_prune_noalloc(const e2s_shape* shape, const e2s_params* params,
                                      const void* q, const void* k, int32_t* keep_idx,
                                      float* fused_opt, float* prio_c_opt, void* stream);
+
+/* Measurement helper, not a step of the method: a streaming read of device memory,
+ * which the benchmark times to report the achievable read bandwidth beside the
+ * nominal HBM peak.  `workgroups` workgroups of 256 threads each read one
+ * contiguous share of buf[0 .. bytes) (16-byte aligned, bytes > 0 and a multiple
+ * of 16) with 16-byte non-temporal loads and combine the words with XOR; the
+ * 4-byte `sink` (device memory) is written only when that XOR equals a fixed
+ * value, so the loads cannot be dropped and nothing else is written.
+ * workgroups: 1 .. 65535.  Enqueued on `stream`. */
+E2S_API e2s_status e2s_read_probe(const void* buf, size_t bytes, int32_t workgroups,
+                                  uint32_t* sink, void* stream);
 
 /* Static description of a status code (never NULL). */
 E2S_API const char* e2s_status_string(e2s_status status);

@@ -115,6 +115,7 @@ _SIGNATURES = {
     "e2s_compact_tokens": [ctypes.POINTER(CompactShape), _P, _P, _P, _P],
     "e2s_prune_views": [_SH, _PA, ctypes.POINTER(QKViews), _P, ctypes.c_size_t, _P, _P, _P, _P],
     "e2s_prune_noalloc": [_SH, _PA, _P, _P, _P, _P, _P, _P],
+    "e2s_read_probe": [_P, ctypes.c_size_t, ctypes.c_int32, _P, _P],
     "e2s_status_string": [ctypes.c_int],
     "e2s_abi_version": [],
 }
@@ -455,6 +456,16 @@ def prune_noalloc(q, k, grid_h: int, grid_w: int, keep: int, cells: int = 4, lam
             ctypes.byref(sh), ctypes.byref(pa), q.data_ptr(), k.data_ptr(),
             keep_idx.data_ptr() if keep > 0 else None, _ptr(fused), _ptr(prio_c))
     return keep_idx, fused, prio_c
+
+
+def read_probe(buf, workgroups: int, sink, stream: Optional[int] = None):
+    """e2s_read_probe over the bytes of the contiguous tensor `buf` (a measurement
+    helper: a streaming read, timed by the caller); sink: a 4-byte device tensor."""
+    _check(buf, "buf")
+    _check(sink, "sink")
+    nbytes = buf.numel() * buf.element_size()
+    _launch("e2s_read_probe", (buf, sink), _LIB.e2s_read_probe, buf.data_ptr(), nbytes,
+            int(workgroups), sink.data_ptr(), stream=stream)
 
 
 def qk_views(q_layers, k_layers) -> QKViews:

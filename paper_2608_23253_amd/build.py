@@ -22,7 +22,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libe2s.so")
 
 SOURCES = ["e2s_validate.cpp", "e2s_api.hip", "score.hip", "score_prob.hip", "layer.hip",
-           "fuse.hip", "select.hip", "compact.hip"]
+           "fuse.hip", "select.hip", "compact.hip", "read_probe.hip"]
 
 ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-Wno-unused-parameter",

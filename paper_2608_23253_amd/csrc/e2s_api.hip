@@ -169,6 +169,18 @@ extern "C" {
 
 int32_t e2s_abi_version(void) { return E2S_ABI_VERSION; }
 
+e2s_status e2s_read_probe(const void* buf, size_t bytes, int32_t workgroups, uint32_t* sink,
+                          void* stream) {
+    E2S_TRY(need(buf));
+    E2S_TRY(need(sink));
+    E2S_TRY(e2s::check_aligned(buf, 16));
+    E2S_TRY(e2s::check_aligned(sink, 4));
+    if (bytes == 0 || bytes % 16 != 0) return E2S_ERR_BAD_SHAPE;
+    if (workgroups < 1 || workgroups > 65535) return E2S_ERR_BAD_PARAM;
+    return from_hip(e2s::launch_read_probe(buf, bytes, workgroups, sink,
+                                           static_cast<hipStream_t>(stream)));
+}
+
 const char* e2s_status_string(e2s_status status) {
     switch (status) {
         case E2S_OK: return "E2S_OK";

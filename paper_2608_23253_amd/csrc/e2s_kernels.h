@@ -85,6 +85,10 @@ hipError_t launch_ds_select(const Dims& d, const SelectArgs& a, const float* rho
 hipError_t launch_attention_select(const Dims& d, const SelectArgs& a, const float* support_c,
                                    hipStream_t stream);
 
+// Streaming read of bytes / 16 packets (e2s_read_probe), arguments validated.
+hipError_t launch_read_probe(const void* buf, size_t bytes, int workgroups, uint32_t* sink,
+                             hipStream_t stream);
+
 // Token compaction (e2s_compact_tokens), arguments validated.
 hipError_t launch_compact(const e2s_compact_shape& s, const int32_t* keep, const void* src,
                           void* dst, hipStream_t stream);

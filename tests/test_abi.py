@@ -67,10 +67,10 @@ def stage(shape, params, ncand, q=A, k=A, pos=A, mprev=None, ws=A, ws_bytes=None
 
 def test_exports_every_declared_entry_point():
     names = L.header_entry_points()
-    assert len(names) == 18
+    assert len(names) == 19
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.e2s_abi_version() == 8
+    assert lib.e2s_abi_version() == 9
 
 
 def test_status_strings():
@@ -436,3 +436,16 @@ def test_noalloc_validation():
     fits = good_shape(batch=64, num_layers=4, num_heads=32, num_kv_heads=32, head_dim=128,
                       num_text=64, grid_h=24, grid_w=24)
     assert L.workspace_size(fits, pa) <= L.NOALLOC_SCRATCH_BYTES
+
+
+def test_read_probe_validation():
+    """The measurement helper rejects bad arguments before any launch."""
+    f = lib.e2s_read_probe
+    assert f(None, 1024, 8, A, None) == L.ERR_NULL_POINTER
+    assert f(A, 1024, 8, None, None) == L.ERR_NULL_POINTER
+    assert f(A + 4, 1024, 8, A, None) == L.ERR_MISALIGNED
+    assert f(A, 1024, 8, A + 2, None) == L.ERR_MISALIGNED
+    assert f(A, 0, 8, A, None) == L.ERR_BAD_SHAPE
+    assert f(A, 1000, 8, A, None) == L.ERR_BAD_SHAPE
+    assert f(A, 1024, 0, A, None) == L.ERR_BAD_PARAM
+    assert f(A, 1024, 65536, A, None) == L.ERR_BAD_PARAM

@@ -811,6 +811,8 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": algo_bytes,
             "launch_us": round(lr_ms * 1e3, 2),
+            "launch_us_p10_p50_p90": [round(float(np.percentile(t_lr, x)) * 1e3, 2)
+                                      for x in (10, 50, 90)],
             "mfma_frac_if_eq1_flops": round(flops_eq1 / (lr_ms * 1e-3) / 1e12
                                             / MFMA_BF16_PEAK_TFLOPS, 4),
             "frac_of_measured_read": round(achieved / probe["GBps"], 4),

@@ -25,7 +25,7 @@
 // Near uniform attention expm1 is a short Taylor series.  In the tight range
 // (every |z s - c_t| <= 1/16, the regime of Gaussian keys at the 1/sqrt(d)
 // scale) both passes take it to degree 4 (degree 5 in pass 2 when some |L_t|
-// widens its range past 1/16), about five vector operations per logit and pass.
+// widens its range past 1/16), five to seven vector operations per logit and pass.
 // The reference is subtracted from the product after the matrix core, not
 // started in its accumulator: a product started from -c_t rounds differently from
 // the product minus c_t, and exactly uniform attention (identical keys) would then

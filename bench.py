@@ -519,6 +519,32 @@ def bench_configs(args, make_timed):
             if flops is not None:
                 rec["roofline"]["stage_mfma_frac"] = round(
                     flops / (stage_us * 1e-6) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
+            if mode == "mean_logit":
+                # the staged fusion kernel (Eq. 10-19, e2s_fuse_evidence) alone on the
+                # batch's supports: it reads e and writes the fused masses, every
+                # layer's conflict and c
+                H_ = cfg.num_heads
+                e_buf = torch.empty((B, L_, H_, N), device="cuda")
+                assert lib.e2s_score_heads(ctypes.byref(sh), ctypes.byref(pa), qd.data_ptr(),
+                                           kd.data_ptr(), e_buf.data_ptr(), None, st) == 0
+                f_buf = torch.empty((B, N, 3), device="cuda")
+                k_buf = torch.empty((B, L_, N), device="cuda")
+                c_buf = torch.empty((B, N), device="cuda")
+
+                def fuse():
+                    return lib.e2s_fuse_evidence(ctypes.byref(sh), e_buf.data_ptr(),
+                                                 f_buf.data_ptr(), k_buf.data_ptr(),
+                                                 c_buf.data_ptr(), st)
+
+                (t_fu,) = timed([fuse], n_rep)
+                fu_us = float(t_fu.mean()) * 1e3
+                fu_bytes = B * (4 * L_ * H_ * N + (16 + 4 * L_) * N)
+                rec["staged_fuse"] = {
+                    "us": round(fu_us, 2), "algorithmic_bytes": int(fu_bytes),
+                    "hbm_frac": round(fu_bytes / (fu_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+                log(f"[bench] {name}: staged fusion kernel {fu_us:.1f} us, "
+                    f"{fu_bytes / 1e6:.1f} MB, {rec['staged_fuse']['hbm_frac']:.1%} of 8 TB/s")
+                del e_buf, f_buf, k_buf, c_buf
             t_p = time.time()
             ips, used, refs = cpu_baseline_leg(cfg, mode, q_s, k_s, sample)
             rec["cpu_baseline"] = {"value": round(ips, 2), "unit": "images/s", "cores": used,

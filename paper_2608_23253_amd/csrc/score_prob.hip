@@ -43,6 +43,16 @@
 // The query-block loops are not unrolled (the per-lane statistics live in LDS),
 // which keeps the kernel's code within the instruction cache.
 //
+// Heads of at most 64 text queries and 576 tokens take pass 2 in a second form in
+// the tight range.  With x = expm1(s z - c_t) and S_t = N + E_t the softmax is
+// (1 + x) / S_t, so N P - 1 = w_t x - E_t / S_t with w_t = N / S_t: the column
+// sums weight the pass-1 terms instead of re-centring them.  For bf16 keys and
+// 385 to 576 tokens (the LLaVA shape) a register-resident kernel keeps every x of
+// a wave's 9 key tiles in registers, so pass 2 is one multiply-add per logit, with
+// no second product and no second series; the two-pass kernel recomputes x for
+// such heads with the same arithmetic, in the same order, so a head's bits do not
+// depend on which of the two kernels its batch runs.
+//
 // Query heads that share a key head (grouped-query attention) run in workgroups
 // with consecutive logical ids; the ids are remapped so that those workgroups land
 // on the same XCD (blocks are dispatched round-robin over the 8 XCDs) and re-read
@@ -68,6 +78,18 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
 
 constexpr int64_t kColumnsInLds = 16384;
 constexpr size_t kLdsPerCu = 160 * 1024;
+
+// Heads of at most 16 kResMaxQueryBlocks text queries whose key tiles give each
+// wave at most kResTiles of them can run register-resident (below).  The two-pass
+// body computes such a head's column sums with the same arithmetic, so a head's
+// bits do not depend on which kernel a batch runs.
+constexpr int kResTiles = 9, kResMinTiles = 7, kResMaxQueryBlocks = 4;
+__host__ __device__ constexpr int tiles_per_wave(int64_t N) {
+    return static_cast<int>(((N + 15) / 16 + kWaves - 1) / kWaves);
+}
+__host__ __device__ constexpr bool resident_head(int64_t NT, int64_t N) {
+    return NT <= 16 * kResMaxQueryBlocks && tiles_per_wave(N) <= kResTiles;
+}
 
 template <typename T, int D> struct ProbCfg;
 template <int D> struct ProbCfg<uint16_t, D> {
@@ -158,11 +180,15 @@ template <typename T, int D, int TG>
 constexpr int mp_workgroups_per_cu() {
     return TG >= 4 ? 2 : (TG == 1 && !std::is_same<T, float>::value ? 4 : 3);
 }
+// The two-pass stage of one (image, layer, query head): the body of
+// score_mean_prob_kernel, and the fallback of the register-resident kernel below.
 template <typename T, int D, int TG, bool GLOBAL>
-__global__ __launch_bounds__(kThreads, (mp_workgroups_per_cu<T, D, TG>())) void score_mean_prob_kernel(
-    const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
-    float* __restrict__ r_out, BatchGeom bg, int group, float scale, int nblocks, int qcap,
-    bool cols_over_stats) {
+__device__ __forceinline__ void mean_prob_two_pass(const T* __restrict__ q,
+                                                   const T* __restrict__ k,
+                                                   float* __restrict__ e_out,
+                                                   float* __restrict__ r_out, const BatchGeom& bg,
+                                                   int group, float scale, int nblocks, int qcap,
+                                                   bool cols_over_stats) {
     using C = ProbCfg<T, D>;
     constexpr int QS = C::QS, NA = C::NA;
     using AFrag = typename C::AFrag;
@@ -171,9 +197,11 @@ __global__ __launch_bounds__(kThreads, (mp_workgroups_per_cu<T, D, TG>())) void 
     // qcap = min(QC, N_T rounded up to 16) query rows per chunk
     const int qbcap = qcap / 16;
     T* qs = reinterpret_cast<T*>(smem);                          // [qcap][QS]
-    float* st_m = reinterpret_cast<float*>(qs + qcap * QS);      // [qcap] shift of each query
+    float* st_m = reinterpret_cast<float*>(qs + qcap * QS);      // [qcap] shift of each query,
+                                                                 // or w_t (tight range)
     float* st_c = st_m + qcap;                                   // [qcap] reference c_t
-    float* wpart = st_c + qcap;                                  // [kWaves][qcap][4]
+    float* st_f = st_c + qcap;                                   // [qcap] E_t / S_t (tight)
+    float* wpart = st_f + qcap;                                  // [kWaves][qcap][4]
     float* lstat = wpart + kWaves * qcap * 4;                    // [3][qbcap][kThreads]
     __shared__ unsigned s_amax;                                  // max |z - c_t| (float bits)
     __shared__ unsigned s_lmax;                                  // max |L_t| (float bits)
@@ -283,7 +311,8 @@ __global__ __launch_bounds__(kThreads, (mp_workgroups_per_cu<T, D, TG>())) void 
         const ScaledSeries<6> p6(scale);
         const ScaledSeries<4> p4(scale);
         float amax = 0.f;                                         // largest |y| seen
-        auto pass1_group = [&](const AFrag (&a)[TG][NA], int j, auto whole, auto tight) {
+        auto pass1_group = [&](const AFrag (&a)[TG][NA], int j, auto whole, auto tight,
+                               auto split) {
             for (int qb = 0; qb < QB; ++qb) {
                 AFrag bq[NA];
                 load_queries<D>(bq, qs, qb * 16, lr, lg);
@@ -292,30 +321,36 @@ __global__ __launch_bounds__(kThreads, (mp_workgroups_per_cu<T, D, TG>())) void 
                 if constexpr (decltype(tight)::value) {
 #pragma unroll
                     for (int tt = 0; tt < TG; ++tt)
-                        prob::series_tile<decltype(whole)::value>(tile_mma<NA>(a[tt], bq), cz,
-                                                                  tile_of(j, tt) * 16 + 4 * lg, N,
-                                                                  p4, E, amax);
+                        prob::series_tile<decltype(whole)::value, decltype(split)::value>(
+                            tile_mma<NA>(a[tt], bq), cz, tile_of(j, tt) * 16 + 4 * lg, N, p4, E,
+                            amax);
                 } else {
 #pragma unroll
                     for (int tt = 0; tt < TG; ++tt)
-                        prob::series_tile<decltype(whole)::value>(tile_mma<NA>(a[tt], bq), cz,
-                                                                  tile_of(j, tt) * 16 + 4 * lg, N,
-                                                                  p5, E, amax);
+                        prob::series_tile<decltype(whole)::value, false>(
+                            tile_mma<NA>(a[tt], bq), cz, tile_of(j, tt) * 16 + 4 * lg, N, p5, E,
+                            amax);
                 }
                 lE[qb * kThreads] = E;
             }
         };
-        auto pass1 = [&](auto tight) {
+        auto pass1 = [&](auto tight, auto split) {
             stream_groups([&](const AFrag (&a)[TG][NA], int j) {
                 // the group's last tile ends at or before N: no key of the group is
                 // masked (tile_of is the same for every lane of the wave)
                 if (__builtin_amdgcn_readfirstlane(tile_of(j, TG - 1)) * 16 + 16 <= N)
-                    pass1_group(a, j, std::true_type{}, tight);
+                    pass1_group(a, j, std::true_type{}, tight, split);
                 else
-                    pass1_group(a, j, std::false_type{}, tight);
+                    pass1_group(a, j, std::false_type{}, tight, split);
             });
         };
-        pass1(std::true_type{});
+        // a head the register-resident kernel could take rounds x = expm1(s y) / s
+        // before summing it, as that kernel keeps it
+        const bool weighted = resident_head(NT, N);
+        if (weighted)
+            pass1(std::true_type{}, std::true_type{});
+        else
+            pass1(std::true_type{}, std::false_type{});
         {
             // (non-negative floats order as their bits)
             const float wmax = wave_max(amax);
@@ -328,7 +363,7 @@ __global__ __launch_bounds__(kThreads, (mp_workgroups_per_cu<T, D, TG>())) void 
         const bool far = !(amax_s <= kSeriesRange);
         if (!tight && !far) {
             for (int qb = 0; qb < QB; ++qb) lE[qb * kThreads] = 0.f;
-            pass1(std::false_type{});
+            pass1(std::false_type{}, std::false_type{});
         }
 
         if (!far) {
@@ -343,14 +378,27 @@ __global__ __launch_bounds__(kThreads, (mp_workgroups_per_cu<T, D, TG>())) void 
             if (tid < QB * 16) {
                 float e = 0.f;
                 for (int w = 0; w < kWaves; ++w) e += wpart[(w * qcap + tid) * 4];
-                // the shift of pass 2 in logit units: c_t + L_t / s
-                float L = 0.f, sh = 0.f;
-                if (tid < rows) {
-                    L = log1pf((scale * e) / fN);
-                    sh = st_c[tid] + L / scale;
+                if (tight && weighted) {
+                    // S_t = N + E_t: w_t = N / S_t and E_t / S_t (zero rows: 1 and 0)
+                    float wt = 1.f, ft = 0.f;
+                    if (tid < rows) {
+                        const float Et = scale * e;
+                        const float S = fN + Et;
+                        wt = fN / S;
+                        ft = Et / S;
+                    }
+                    st_m[tid] = wt;
+                    st_f[tid] = ft;
+                } else {
+                    // the shift of pass 2 in logit units: c_t + L_t / s
+                    float L = 0.f, sh = 0.f;
+                    if (tid < rows) {
+                        L = log1pf((scale * e) / fN);
+                        sh = st_c[tid] + L / scale;
+                    }
+                    st_m[tid] = sh;
+                    atomicMax(&s_lmax, __float_as_uint(fabsf(L)));
                 }
-                st_m[tid] = sh;
-                atomicMax(&s_lmax, __float_as_uint(fabsf(L)));
             }
         } else {
             // ---- pass 1 again, online, tile by tile: running maximum as the
@@ -436,11 +484,41 @@ __global__ __launch_bounds__(kThreads, (mp_workgroups_per_cu<T, D, TG>())) void 
                 add_columns(reinterpret_cast<const float(&)[TG * 4]>(col), j, scale);
             });
         };
-        if (tight) {
+        if (tight && !weighted) {
             if (amax_s + __uint_as_float(s_lmax) <= prob::kTightRange)
                 pass2_tight(p4);
             else
                 pass2_tight(p5);
+        } else if (tight) {
+            // N P - 1 = w_t x - E_t / S_t with x = expm1(s (z - c_t)) recomputed
+            // exactly as in pass 1 (the register-resident kernel's arithmetic, in
+            // the same order, so both give the same bits)
+            float fsum = 0.f;
+            for (int t = 0; t < rows; ++t) fsum += st_f[t];
+            stream_groups([&](const AFrag (&a)[TG][NA], int j) {
+                float col[TG][4];
+#pragma unroll
+                for (int tt = 0; tt < TG; ++tt)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) col[tt][r] = 0.f;
+                for (int qb = 0; qb < QB; ++qb) {
+                    AFrag bq[NA];
+                    load_queries<D>(bq, qs, qb * 16, lr, lg);
+                    const float cz = st_c[qb * 16 + lr], wq = st_m[qb * 16 + lr];
+#pragma unroll
+                    for (int tt = 0; tt < TG; ++tt)
+                        prob::column_weighted_tile(tile_mma<NA>(a[tt], bq), cz, p4, wq, col[tt]);
+                }
+#pragma unroll
+                for (int i = 0; i < TG * 4; ++i) {
+                    const float sum = group_sum<16>(col[i / 4][i % 4]);
+                    const int key = tile_of(j, i / 4) * 16 + 4 * lg + i % 4;
+                    if (lr == 0 && key < N) {
+                        const float prev = (t0 == 0) ? 0.f : colsum[key];
+                        colsum[key] = prev + (scale * sum - fsum);
+                    }
+                }
+            });
         } else if (!far) {
             // y = z - shift; |s y| <= 1/4: the degree-6 series; the column sums are
             // in units of s
@@ -491,6 +569,194 @@ __global__ __launch_bounds__(kThreads, (mp_workgroups_per_cu<T, D, TG>())) void 
     }
 }
 
+template <typename T, int D, int TG, bool GLOBAL>
+__global__ __launch_bounds__(kThreads, (mp_workgroups_per_cu<T, D, TG>())) void score_mean_prob_kernel(
+    const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
+    float* __restrict__ r_out, BatchGeom bg, int group, float scale, int nblocks, int qcap,
+    bool cols_over_stats) {
+    mean_prob_two_pass<T, D, TG, GLOBAL>(q, k, e_out, r_out, bg, group, scale, nblocks, qcap,
+                                         cols_over_stats);
+}
+
+// Register-resident variant for heads of 16 (QBN - 1) + 1 .. 16 QBN text queries
+// whose key tiles give every wave at most MAXT of them (the LLaVA shape: 64
+// queries, 576 tokens, 9 tiles per wave).  Pass 1 keeps each x = expm1(s (z - c_t)) of the
+// wave's tiles in registers; with S_t = N + E_t (E_t = sum_n x) the softmax is
+// P = (1 + x) / S_t, so
+//   N P - 1 = (N x - E_t) / S_t = w_t x - E_t / S_t,   w_t = N / S_t,
+// and the column sums take one multiply-add per logit: no second product on the
+// matrix cores and no second series.  Only the tight range (every |s (z - c_t)|
+// <= 1/16, where the degree-4 series is within an ulp) takes this path; any other
+// head runs the two-pass body from the start.  u = N r - 1 is then
+// (s sum_t w_t x' - sum_t E_t / S_t) / N_T with x = s x' (the series in units of s).
+template <typename T, int D, int MAXT, int QBN>
+__global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
+    const T* __restrict__ q, const T* __restrict__ k, float* __restrict__ e_out,
+    float* __restrict__ r_out, BatchGeom bg, int group, float scale, int nblocks, int qcap,
+    bool cols_over_stats) {
+    using C = ProbCfg<T, D>;
+    constexpr int QS = C::QS, NA = C::NA, QR = 16 * QBN;
+    constexpr int KB = 3;                                        // key tiles in registers
+    using AFrag = typename C::AFrag;
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    T* qs = reinterpret_cast<T*>(smem);                          // [QR][QS]
+    float* st_c = reinterpret_cast<float*>(qs + QR * QS);        // [QR] reference c_t
+    float* st_w = st_c + QR;                                     // [QR] w_t
+    float* st_f = st_w + QR;                                     // [QR] E_t / S_t
+    float* wpart = st_f + QR;                                    // [kWaves][QR]
+    __shared__ unsigned s_amax;                                  // max |z - c_t| (float bits)
+
+    const int64_t bid = xcd_remap(blockIdx.x, nblocks);          // (b*L + l)*H + h
+    const int64_t b = bid / (bg.L * bg.H);
+    const int lh = static_cast<int>(bid - b * bg.L * bg.H);
+    const int l = lh / bg.H, h = lh - l * bg.H;
+    const ImageGeom ig = image_geom(bg, b);
+    const int NT = ig.NT, N = ig.N;
+    const T* qh = query_rows(q, bg, ig, b, l, h);
+    const T* kg = key_rows(k, bg, ig, b, l, h / group);
+    const int64_t qld = query_ld(bg), kld = key_ld(bg);
+    const int64_t row = bg.L * bg.H * ig.tok + static_cast<int64_t>(lh) * N;
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int lr = lane % 16, lg = lane / 16;
+    const int ntiles = (N + 15) / 16;
+    // this wave's tiles (<= MAXT); the loops run MAXT of them, a tile past the
+    // wave's last one repeating that tile with every logit masked, so that no
+    // branch separates the loads from their uses
+    const int ntw = wave < ntiles ? (ntiles - wave + kWaves - 1) / kWaves : 0;
+    constexpr int QB = QBN;                                      // 16 (QBN - 1) < N_T
+    const float fN = static_cast<float>(N);
+    const int koff = std::is_same<T, float>::value ? 4 * lg : 8 * lg;
+    auto key_of = [&](int j) { return (wave + kWaves * j) * 16; };
+    auto load_tile = [&](AFrag (&a)[NA], int j) {
+        const int jj = min(j, max(ntw - 1, 0));
+        load_keys<NA>(a, kg + static_cast<int64_t>(min(key_of(jj) + lr, N - 1)) * kld + koff);
+    };
+
+    // the wave's first key tiles are requested before the queries are staged
+    AFrag a[KB][NA];
+#pragma unroll
+    for (int j = 0; j < KB - 1; ++j) load_tile(a[j], j);
+
+    // ---- stage the queries (rows past N_T are zero) and their references ----
+    {
+        constexpr int EPV = 16 / sizeof(T);
+        for (int idx = tid; idx < QB * 16 * (D / EPV); idx += kThreads) {
+            const int r = idx / (D / EPV), c = idx % (D / EPV);
+            f32x4v v = {0.f, 0.f, 0.f, 0.f};
+            if (r < NT) v = *reinterpret_cast<const f32x4v*>(qh + static_cast<int64_t>(r) * qld + c * EPV);
+            *reinterpret_cast<f32x4v*>(qs + r * QS + c * EPV) = v;
+        }
+        if (tid == 0) s_amax = 0u;
+        __syncthreads();
+        AFrag a0[NA];
+        load_keys<NA>(a0, kg + static_cast<int64_t>(min(lr, N - 1)) * kld + koff);
+        for (int qb = wave; qb < QB; qb += kWaves) {
+            AFrag bq[NA];
+            load_queries<D>(bq, qs, qb * 16, lr, lg);
+            const float c = prob::block_reference(tile_mma<NA>(a0, bq), N, lr);
+            if (lg == 0) st_c[qb * 16 + lr] = c;
+        }
+        __syncthreads();
+    }
+
+    // ---- pass 1: x = expm1(s y) / s = y P(y), y = z - c_t, kept per logit ------
+    const ScaledSeries<4> p4(scale);
+    float cz[QBN];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) cz[qb] = st_c[qb * 16 + lr];
+    float x[MAXT][QBN][4];
+    float E[QBN];
+#pragma unroll
+    for (int qb = 0; qb < QBN; ++qb) E[qb] = 0.f;
+    float amax = 0.f;
+#pragma unroll
+    for (int j = 0; j < MAXT; ++j) {
+        if (j + KB - 1 < MAXT) load_tile(a[(j + KB - 1) % KB], j + KB - 1);
+        const int key0 = key_of(j) + 4 * lg;
+        const bool own = j < ntw;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) {
+            AFrag bq[NA];
+            load_queries<D>(bq, qs, qb * 16, lr, lg);
+            const f32x4v z = tile_mma<NA>(a[j % KB], bq);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                float y = z[r] - cz[qb];
+                y = (own && key0 + r < N) ? y : 0.f;
+                amax = fmaxf(amax, fabsf(y));
+                const float xv = p4(y) * y;
+                x[j][qb][r] = xv;
+                E[qb] += xv;
+            }
+        }
+        // keep the tiles in program order: the compiler would otherwise sink each
+        // tile's loads down to its first use, which leaves none in flight
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    {
+        const float wmax = wave_max(amax);
+        if (lane == 0) atomicMax(&s_amax, __float_as_uint(wmax));
+    }
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        float e = E[qb];
+        e += __shfl_xor(e, 16);
+        e += __shfl_xor(e, 32);
+        if (lg == 0) wpart[wave * QR + qb * 16 + lr] = e;
+    }
+    __syncthreads();
+    if (!(__uint_as_float(s_amax) * scale <= prob::kTightRange)) {
+        // outside the tight range: the two-pass stage from the start (its LDS is
+        // at least this kernel's; every thread has passed the barrier above)
+        __syncthreads();
+        mean_prob_two_pass<T, D, 1, false>(q, k, e_out, r_out, bg, group, scale, nblocks, qcap,
+                                           cols_over_stats);
+        return;
+    }
+    if (tid < QB * 16) {
+        float e = 0.f;
+        for (int w = 0; w < kWaves; ++w) e += wpart[w * QR + tid];
+        float wt = 1.f, ft = 0.f;                                // rows past N_T: x = 0
+        if (tid < NT) {
+            const float Et = scale * e;
+            const float S = fN + Et;
+            wt = fN / S;
+            ft = Et / S;
+        }
+        st_w[tid] = wt;
+        st_f[tid] = ft;
+    }
+    __syncthreads();
+    float wq[QBN];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) wq[qb] = st_w[qb * 16 + lr];
+    float fsum = 0.f;                                            // sum_t E_t / S_t, in order
+    for (int t = 0; t < NT; ++t) fsum += st_f[t];
+
+    // ---- column sums: per key, sum over the queries of w_t x' -----------------
+    const float inv_nt = 1.0f / static_cast<float>(NT);
+#pragma unroll
+    for (int j = 0; j < MAXT; ++j) {
+        float col[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) col[r] = fmaf(wq[qb], x[j][qb][r], col[r]);
+        const bool own = j < ntw;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float sum = group_sum<16>(col[r]);
+            const int key = key_of(j) + 4 * lg + r;
+            if (own && lr == 0 && key < N) {
+                const float u = (scale * sum - fsum) * inv_nt;
+                __builtin_nontemporal_store(u / (2.0f * (2.0f + u)), e_out + row + key);
+                if (r_out) r_out[row + key] = (1.0f + u) / fN;
+            }
+        }
+    }
+}
+
 // LDS of one workgroup: the column sums in LDS up to kColumnsInLds keys, else in
 // the output rows; in the statistics' place when every head has one query chunk
 // and they fit (over).
@@ -501,7 +767,7 @@ size_t mp_lds(const Dims& d, int qcap, bool& global, bool& over) {
     const int64_t stats = 3 * (qcap / 16) * kThreads;            // floats
     over = !global && d.NT <= qcap && d.N <= stats;
     return static_cast<size_t>(qcap) * C::QS * sizeof(T) +
-           (2 * qcap + kWaves * qcap * 4 + stats) * sizeof(float) +
+           (3 * qcap + kWaves * qcap * 4 + stats) * sizeof(float) +
            (global || over ? 0 : static_cast<size_t>(d.N) * sizeof(float));
 }
 
@@ -526,12 +792,54 @@ hipError_t launch_mp(const Dims& d, float scale, const void* q, const void* k, f
     return hipGetLastError();
 }
 
+// The register-resident kernel takes a batch whose largest head qualifies with 7
+// to kResTiles key tiles per wave (385 to 576 tokens; every wave runs kResTiles, so
+// fewer tiles would waste more of them); every head of such a batch qualifies.
+bool resident_fits(const Dims& d) {
+    return resident_head(d.NT, d.N) && tiles_per_wave(d.N) >= kResMinTiles;
+}
+
+template <typename T, int D, int QBN>
+hipError_t launch_mp_resident(const Dims& d, float scale, const void* q, const void* k, float* e,
+                              float* r, int qcap, hipStream_t st) {
+    using C = ProbCfg<T, D>;
+    constexpr int QR = 16 * QBN;
+    bool global = false, over = false;
+    // room for the two-pass fallback (one tile per group) as well
+    const size_t lds = std::max(static_cast<size_t>(QR) * C::QS * sizeof(T) +
+                                    static_cast<size_t>(4 * QR + kWaves * QR) * sizeof(float),
+                                mp_lds<T, D>(d, qcap, global, over));
+    auto kern = score_mean_prob_resident_kernel<T, D, kResTiles, QBN>;
+    if (lds > 64 * 1024) {
+        hipError_t err = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             static_cast<int>(lds));
+        if (err != hipSuccess) return err;
+    }
+    const int64_t blocks = d.B * d.L * d.H;
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), lds, st,
+                       static_cast<const T*>(q), static_cast<const T*>(k), e, r,
+                       batch_geom(d), static_cast<int>(d.group), scale,
+                       static_cast<int>(blocks), qcap, over);
+    return hipGetLastError();
+}
+
 template <typename T, int D>
 hipError_t dispatch_mp(const Dims& d, float scale, const void* q, const void* k, float* e,
                        float* r, hipStream_t st) {
     using C = ProbCfg<T, D>;
     // qcap = min(QC, N_T rounded up to 16) query rows per chunk
     const int qcap = static_cast<int>(std::min<int64_t>(C::QC, (d.NT + 15) / 16 * 16));
+    if constexpr (std::is_same<T, uint16_t>::value) {
+        if (resident_fits(d)) {
+            switch ((d.NT + 15) / 16) {
+                case 1: return launch_mp_resident<T, D, 1>(d, scale, q, k, e, r, qcap, st);
+                case 2: return launch_mp_resident<T, D, 2>(d, scale, q, k, e, r, qcap, st);
+                case 3: return launch_mp_resident<T, D, 3>(d, scale, q, k, e, r, qcap, st);
+                default: return launch_mp_resident<T, D, 4>(d, scale, q, k, e, r, qcap, st);
+            }
+        }
+    }
     if constexpr (std::is_same<T, float>::value) {
         return launch_mp<T, D, 1>(d, scale, q, k, e, r, qcap, st);
     } else {

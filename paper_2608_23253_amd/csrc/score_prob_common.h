@@ -95,7 +95,9 @@ __device__ __forceinline__ float block_reference(const f32x4v& z, int N, int lr)
 // amax: the largest |y| seen, to confirm afterwards that the range held.  WHOLE:
 // the caller knows that every key of the tile is below N (the same arithmetic
 // without the masking).
-template <bool WHOLE, typename Series>
+// SPLIT: x = y P(y) is rounded before it is added (as the register-resident
+// kernel, which keeps x, adds it), else added in one fused step.
+template <bool WHOLE, bool SPLIT, typename Series>
 __device__ __forceinline__ void series_tile(const f32x4v& z, float cz, int key0, int N,
                                             const Series& p, float& E, float& amax) {
     const bool full = WHOLE || key0 + 4 <= N;
@@ -104,7 +106,10 @@ __device__ __forceinline__ void series_tile(const f32x4v& z, float cz, int key0,
         float y = z[r] - cz;
         if (!full) y = (key0 + r < N) ? y : 0.f;
         amax = fmaxf(amax, fabsf(y));
-        E = fmaf(p(y), y, E);
+        if constexpr (SPLIT)
+            E += p(y) * y;
+        else
+            E = fmaf(p(y), y, E);
     }
 }
 
@@ -219,6 +224,19 @@ __device__ __forceinline__ void column_series_tile(const f32x4v& z, float sz, co
     for (int r = 0; r < 4; ++r) {
         const float y = z[r] - sz;
         col[r] = fmaf(p(y), y, col[r]);
+    }
+}
+
+// Pass 2 in the tight range: col += w_t x with x = expm1(s y) / s = y P(y),
+// y = z - c_t, evaluated exactly as pass 1 evaluates it (series_tile), over the
+// query blocks in order.  Keys past N are not masked: their sums are never kept.
+template <typename Series>
+__device__ __forceinline__ void column_weighted_tile(const f32x4v& z, float cz, const Series& p,
+                                                     float w, float (&col)[4]) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const float y = z[r] - cz;
+        col[r] = fmaf(w, p(y) * y, col[r]);
     }
 }
 

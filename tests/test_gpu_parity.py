@@ -76,6 +76,18 @@ CASES = [
     synth.heavy_tailed(_small("heavy_text100_d128", config_id=63, num_layers=2, num_heads=4,
                               num_kv_heads=4, head_dim=128, num_text=100, grid_h=12,
                               grid_w=12, keep=24, salient_count=8), name="heavy_text100"),
+    # the register-resident mean-of-probabilities kernel (bf16, at most 64 text
+    # queries, 385 to 576 tokens): 1 to 4 query blocks, d = 64 and 128, waves with
+    # unequal tile counts, grouped-query heads, and peaked attention, which leaves the
+    # tight range and takes the two-pass fallback
+    _small("resident_q37_d128", config_id=70, num_heads=4, num_kv_heads=2, head_dim=128,
+           num_text=37, grid_h=23, grid_w=19, keep=60, salient_count=10, clusters=2),
+    _small("resident_q20_d64", config_id=71, num_text=20, grid_h=24, grid_w=24, keep=100,
+           salient_count=12, clusters=3),
+    _small("resident_q5", config_id=72, num_text=5, grid_h=20, grid_w=25, keep=50),
+    synth.heavy_tailed(_small("resident_heavy_q48", config_id=73, head_dim=128, num_text=48,
+                              grid_h=22, grid_w=22, keep=40, salient_count=12, clusters=2),
+                       name="resident_heavy_q48"),
     _small("max_grid_16384", config_id=56, batch=1, num_layers=1, num_heads=2, num_kv_heads=1,
            num_text=2, grid_h=128, grid_w=128, keep=1000, salient_count=40, clusters=4),
     # more than 16384 visual tokens: the selection streams the image in segments;

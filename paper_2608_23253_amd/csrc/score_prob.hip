@@ -200,11 +200,11 @@ __device__ __forceinline__ void mean_prob_two_pass(const T* __restrict__ q,
     float* st_m = reinterpret_cast<float*>(qs + qcap * QS);      // [qcap] shift of each query,
                                                                  // or w_t (tight range)
     float* st_c = st_m + qcap;                                   // [qcap] reference c_t
-    float* st_f = st_c + qcap;                                   // [qcap] E_t / S_t (tight)
-    float* wpart = st_f + qcap;                                  // [kWaves][qcap][4]
+    float* wpart = st_c + qcap;                                  // [kWaves][qcap][4]
     float* lstat = wpart + kWaves * qcap * 4;                    // [3][qbcap][kThreads]
     __shared__ unsigned s_amax;                                  // max |z - c_t| (float bits)
     __shared__ unsigned s_lmax;                                  // max |L_t| (float bits)
+    __shared__ float s_fsum;                                     // sum_t E_t / S_t (tight)
 
     const int64_t bid = xcd_remap(blockIdx.x, nblocks);          // (b*L + l)*H + h
     const int64_t b = bid / (bg.L * bg.H);
@@ -375,12 +375,13 @@ __device__ __forceinline__ void mean_prob_two_pass(const T* __restrict__ q,
                 if (lg == 0) wpart[(wave * qcap + qb * 16 + lr) * 4] = e;
             }
             __syncthreads();
+            float ft = 0.f;
             if (tid < QB * 16) {
                 float e = 0.f;
                 for (int w = 0; w < kWaves; ++w) e += wpart[(w * qcap + tid) * 4];
                 if (tight && weighted) {
                     // S_t = N + E_t: w_t = N / S_t and E_t / S_t (zero rows: 1 and 0)
-                    float wt = 1.f, ft = 0.f;
+                    float wt = 1.f;
                     if (tid < rows) {
                         const float Et = scale * e;
                         const float S = fN + Et;
@@ -388,7 +389,6 @@ __device__ __forceinline__ void mean_prob_two_pass(const T* __restrict__ q,
                         ft = Et / S;
                     }
                     st_m[tid] = wt;
-                    st_f[tid] = ft;
                 } else {
                     // the shift of pass 2 in logit units: c_t + L_t / s
                     float L = 0.f, sh = 0.f;
@@ -399,6 +399,11 @@ __device__ __forceinline__ void mean_prob_two_pass(const T* __restrict__ q,
                     st_m[tid] = sh;
                     atomicMax(&s_lmax, __float_as_uint(fabsf(L)));
                 }
+            }
+            // (a weighted head has at most 64 queries: all in wave 0)
+            if (tight && weighted && wave == 0) {
+                const float fs = prob::query_sum(ft);
+                if (lane == 0) s_fsum = fs;
             }
         } else {
             // ---- pass 1 again, online, tile by tile: running maximum as the
@@ -493,8 +498,7 @@ __device__ __forceinline__ void mean_prob_two_pass(const T* __restrict__ q,
             // N P - 1 = w_t x - E_t / S_t with x = expm1(s (z - c_t)) recomputed
             // exactly as in pass 1 (the register-resident kernel's arithmetic, in
             // the same order, so both give the same bits)
-            float fsum = 0.f;
-            for (int t = 0; t < rows; ++t) fsum += st_f[t];
+            const float fsum = s_fsum;
             stream_groups([&](const AFrag (&a)[TG][NA], int j) {
                 float col[TG][4];
 #pragma unroll
@@ -603,9 +607,9 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
     T* qs = reinterpret_cast<T*>(smem);                          // [QR][QS]
     float* st_c = reinterpret_cast<float*>(qs + QR * QS);        // [QR] reference c_t
     float* st_w = st_c + QR;                                     // [QR] w_t
-    float* st_f = st_w + QR;                                     // [QR] E_t / S_t
-    float* wpart = st_f + QR;                                    // [kWaves][QR]
+    float* wpart = st_w + QR;                                    // [kWaves][QR]
     __shared__ unsigned s_amax;                                  // max |z - c_t| (float bits)
+    __shared__ float s_fsum;                                     // sum_t E_t / S_t
 
     const int64_t bid = xcd_remap(blockIdx.x, nblocks);          // (b*L + l)*H + h
     const int64_t b = bid / (bg.L * bg.H);
@@ -633,10 +637,13 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
         load_keys<NA>(a, kg + static_cast<int64_t>(min(key_of(jj) + lr, N - 1)) * kld + koff);
     };
 
-    // the wave's first key tiles are requested before the queries are staged
+    // the wave's first key tiles, and keys 0..15 for the references, are requested
+    // before the queries are staged
     AFrag a[KB][NA];
 #pragma unroll
     for (int j = 0; j < KB - 1; ++j) load_tile(a[j], j);
+    AFrag a0[NA];
+    load_keys<NA>(a0, kg + static_cast<int64_t>(min(lr, N - 1)) * kld + koff);
 
     // ---- stage the queries (rows past N_T are zero) and their references ----
     {
@@ -649,8 +656,6 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
         }
         if (tid == 0) s_amax = 0u;
         __syncthreads();
-        AFrag a0[NA];
-        load_keys<NA>(a0, kg + static_cast<int64_t>(min(lr, N - 1)) * kld + koff);
         for (int qb = wave; qb < QB; qb += kWaves) {
             AFrag bq[NA];
             load_queries<D>(bq, qs, qb * 16, lr, lg);
@@ -714,10 +719,11 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
                                            cols_over_stats);
         return;
     }
+    float ft = 0.f;
     if (tid < QB * 16) {
         float e = 0.f;
         for (int w = 0; w < kWaves; ++w) e += wpart[w * QR + tid];
-        float wt = 1.f, ft = 0.f;                                // rows past N_T: x = 0
+        float wt = 1.f;                                          // rows past N_T: x = 0
         if (tid < NT) {
             const float Et = scale * e;
             const float S = fN + Et;
@@ -725,14 +731,16 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
             ft = Et / S;
         }
         st_w[tid] = wt;
-        st_f[tid] = ft;
+    }
+    if (wave == 0) {
+        const float fs = prob::query_sum(ft);
+        if (lane == 0) s_fsum = fs;
     }
     __syncthreads();
     float wq[QBN];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) wq[qb] = st_w[qb * 16 + lr];
-    float fsum = 0.f;                                            // sum_t E_t / S_t, in order
-    for (int t = 0; t < NT; ++t) fsum += st_f[t];
+    const float fsum = s_fsum;
 
     // ---- column sums: per key, sum over the queries of w_t x' -----------------
     const float inv_nt = 1.0f / static_cast<float>(NT);
@@ -743,15 +751,33 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
         for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
             for (int r = 0; r < 4; ++r) col[r] = fmaf(wq[qb], x[j][qb][r], col[r]);
-        const bool own = j < ntw;
+        // lane (0, lg) holds the sums of keys key0 .. key0 + 3: one 16-byte store
+        // when they are whole and aligned
+        float ev[4], rv[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-            const float sum = group_sum<16>(col[r]);
-            const int key = key_of(j) + 4 * lg + r;
-            if (own && lr == 0 && key < N) {
-                const float u = (scale * sum - fsum) * inv_nt;
-                __builtin_nontemporal_store(u / (2.0f * (2.0f + u)), e_out + row + key);
-                if (r_out) r_out[row + key] = (1.0f + u) / fN;
+            const float u = (scale * group_sum<16>(col[r]) - fsum) * inv_nt;
+            ev[r] = u / (2.0f * (2.0f + u));
+            rv[r] = (1.0f + u) / fN;
+        }
+        const int key0 = key_of(j) + 4 * lg;
+        if (j < ntw && lr == 0 && key0 < N) {
+            float* eo = e_out + row + key0;
+            float* ro = r_out ? r_out + row + key0 : nullptr;
+            const bool vec = key0 + 4 <= N && (reinterpret_cast<uintptr_t>(eo) & 15) == 0 &&
+                             (reinterpret_cast<uintptr_t>(ro) & 15) == 0;
+            if (vec) {
+                __builtin_nontemporal_store(f32x4v{ev[0], ev[1], ev[2], ev[3]},
+                                            reinterpret_cast<f32x4v*>(eo));
+                if (ro) *reinterpret_cast<f32x4v*>(ro) = f32x4v{rv[0], rv[1], rv[2], rv[3]};
+            } else {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    if (key0 + r < N) {
+                        __builtin_nontemporal_store(ev[r], eo + r);
+                        if (ro) ro[r] = rv[r];
+                    }
+                }
             }
         }
     }
@@ -767,7 +793,7 @@ size_t mp_lds(const Dims& d, int qcap, bool& global, bool& over) {
     const int64_t stats = 3 * (qcap / 16) * kThreads;            // floats
     over = !global && d.NT <= qcap && d.N <= stats;
     return static_cast<size_t>(qcap) * C::QS * sizeof(T) +
-           (3 * qcap + kWaves * qcap * 4 + stats) * sizeof(float) +
+           (2 * qcap + kWaves * qcap * 4 + stats) * sizeof(float) +
            (global || over ? 0 : static_cast<size_t>(d.N) * sizeof(float));
 }
 
@@ -807,7 +833,7 @@ hipError_t launch_mp_resident(const Dims& d, float scale, const void* q, const v
     bool global = false, over = false;
     // room for the two-pass fallback (one tile per group) as well
     const size_t lds = std::max(static_cast<size_t>(QR) * C::QS * sizeof(T) +
-                                    static_cast<size_t>(4 * QR + kWaves * QR) * sizeof(float),
+                                    static_cast<size_t>(2 * QR + kWaves * QR) * sizeof(float),
                                 mp_lds<T, D>(d, qcap, global, over));
     auto kern = score_mean_prob_resident_kernel<T, D, kResTiles, QBN>;
     if (lds > 64 * 1024) {

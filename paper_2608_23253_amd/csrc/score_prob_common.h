@@ -227,6 +227,11 @@ __device__ __forceinline__ void column_series_tile(const f32x4v& z, float sz, co
     }
 }
 
+// Sum over a head's queries of a per-query value held by lane t of one wave (0 in
+// lanes past N_T; at most 64 queries): the butterfly of wave_sum, whose order
+// depends only on the lanes, so every kernel that takes it gets the same bits.
+__device__ __forceinline__ float query_sum(float v) { return wave_sum(v); }
+
 // Pass 2 in the tight range: col += w_t x with x = expm1(s y) / s = y P(y),
 // y = z - c_t, evaluated exactly as pass 1 evaluates it (series_tile), over the
 // query blocks in order.  Keys past N are not masked: their sums are never kept.

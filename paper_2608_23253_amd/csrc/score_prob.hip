@@ -751,34 +751,17 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
         for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
             for (int r = 0; r < 4; ++r) col[r] = fmaf(wq[qb], x[j][qb][r], col[r]);
-        // lane (0, lg) holds the sums of keys key0 .. key0 + 3: one 16-byte store
-        // when they are whole and aligned
-        float ev[4], rv[4];
+        // every lane of a 16-lane row ends with the row's four key sums; lane r of
+        // the row finishes key key0 + r, so each division runs once per key
+        float sr[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const float u = (scale * group_sum<16>(col[r]) - fsum) * inv_nt;
-            ev[r] = u / (2.0f * (2.0f + u));
-            rv[r] = (1.0f + u) / fN;
-        }
-        const int key0 = key_of(j) + 4 * lg;
-        if (j < ntw && lr == 0 && key0 < N) {
-            float* eo = e_out + row + key0;
-            float* ro = r_out ? r_out + row + key0 : nullptr;
-            const bool vec = key0 + 4 <= N && (reinterpret_cast<uintptr_t>(eo) & 15) == 0 &&
-                             (reinterpret_cast<uintptr_t>(ro) & 15) == 0;
-            if (vec) {
-                __builtin_nontemporal_store(f32x4v{ev[0], ev[1], ev[2], ev[3]},
-                                            reinterpret_cast<f32x4v*>(eo));
-                if (ro) *reinterpret_cast<f32x4v*>(ro) = f32x4v{rv[0], rv[1], rv[2], rv[3]};
-            } else {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    if (key0 + r < N) {
-                        __builtin_nontemporal_store(ev[r], eo + r);
-                        if (ro) ro[r] = rv[r];
-                    }
-                }
-            }
+        for (int r = 0; r < 4; ++r) sr[r] = group_sum<16>(col[r]);
+        const float sum = lr == 0 ? sr[0] : lr == 1 ? sr[1] : lr == 2 ? sr[2] : sr[3];
+        const int key = key_of(j) + 4 * lg + lr;
+        if (j < ntw && lr < 4 && key < N) {
+            const float u = (scale * sum - fsum) * inv_nt;
+            __builtin_nontemporal_store(u / (2.0f * (2.0f + u)), e_out + row + key);
+            if (r_out) r_out[row + key] = (1.0f + u) / fN;
         }
     }
 }

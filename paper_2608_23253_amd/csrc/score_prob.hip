@@ -605,11 +605,8 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
 
     extern __shared__ __align__(16) unsigned char smem[];
     T* qs = reinterpret_cast<T*>(smem);                          // [QR][QS]
-    float* st_c = reinterpret_cast<float*>(qs + QR * QS);        // [QR] reference c_t
-    float* st_w = st_c + QR;                                     // [QR] w_t
-    float* wpart = st_w + QR;                                    // [kWaves][QR]
+    float* wpart = reinterpret_cast<float*>(qs + QR * QS);       // [kWaves][QR]
     __shared__ unsigned s_amax;                                  // max |z - c_t| (float bits)
-    __shared__ float s_fsum;                                     // sum_t E_t / S_t
 
     const int64_t bid = xcd_remap(blockIdx.x, nblocks);          // (b*L + l)*H + h
     const int64_t b = bid / (bg.L * bg.H);
@@ -656,20 +653,18 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
         }
         if (tid == 0) s_amax = 0u;
         __syncthreads();
-        for (int qb = wave; qb < QB; qb += kWaves) {
-            AFrag bq[NA];
-            load_queries<D>(bq, qs, qb * 16, lr, lg);
-            const float c = prob::block_reference(tile_mma<NA>(a0, bq), N, lr);
-            if (lg == 0) st_c[qb * 16 + lr] = c;
-        }
-        __syncthreads();
+    }
+    // every wave takes all the references itself (a few products; no barrier)
+    float cz[QBN];
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        AFrag bq[NA];
+        load_queries<D>(bq, qs, qb * 16, lr, lg);
+        cz[qb] = prob::block_reference(tile_mma<NA>(a0, bq), N, lr);
     }
 
     // ---- pass 1: x = expm1(s y) / s = y P(y), y = z - c_t, kept per logit ------
     const ScaledSeries<4> p4(scale);
-    float cz[QBN];
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) cz[qb] = st_c[qb * 16 + lr];
     float x[MAXT][QBN][4];
     float E[QBN];
 #pragma unroll
@@ -719,28 +714,22 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
                                            cols_over_stats);
         return;
     }
-    float ft = 0.f;
-    if (tid < QB * 16) {
+    // every wave merges the statistics itself, lane t for query t (no barrier)
+    float ft = 0.f, wt = 1.f;                                    // rows past N_T: x = 0
+    if (lane < QB * 16) {
         float e = 0.f;
-        for (int w = 0; w < kWaves; ++w) e += wpart[w * QR + tid];
-        float wt = 1.f;                                          // rows past N_T: x = 0
-        if (tid < NT) {
+        for (int w = 0; w < kWaves; ++w) e += wpart[w * QR + lane];
+        if (lane < NT) {
             const float Et = scale * e;
             const float S = fN + Et;
             wt = fN / S;
             ft = Et / S;
         }
-        st_w[tid] = wt;
     }
-    if (wave == 0) {
-        const float fs = prob::query_sum(ft);
-        if (lane == 0) s_fsum = fs;
-    }
-    __syncthreads();
+    const float fsum = prob::query_sum(ft);
     float wq[QBN];
 #pragma unroll
-    for (int qb = 0; qb < QB; ++qb) wq[qb] = st_w[qb * 16 + lr];
-    const float fsum = s_fsum;
+    for (int qb = 0; qb < QB; ++qb) wq[qb] = __shfl(wt, qb * 16 + lr);
 
     // ---- column sums: per key, sum over the queries of w_t x' -----------------
     const float inv_nt = 1.0f / static_cast<float>(NT);
@@ -816,7 +805,7 @@ hipError_t launch_mp_resident(const Dims& d, float scale, const void* q, const v
     bool global = false, over = false;
     // room for the two-pass fallback (one tile per group) as well
     const size_t lds = std::max(static_cast<size_t>(QR) * C::QS * sizeof(T) +
-                                    static_cast<size_t>(2 * QR + kWaves * QR) * sizeof(float),
+                                    static_cast<size_t>(kWaves * QR) * sizeof(float),
                                 mp_lds<T, D>(d, qcap, global, over));
     auto kern = score_mean_prob_resident_kernel<T, D, kResTiles, QBN>;
     if (lds > 64 * 1024) {

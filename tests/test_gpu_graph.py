@@ -31,6 +31,9 @@ CASES = [
     (_cfg("mha_layer_path", config_id=96, batch=64, num_layers=4, num_heads=6, num_kv_heads=6,
           num_text=12), "mean_logit"),
     (_cfg("gqa_prob", config_id=97), "mean_prob"),
+    # 456 tokens, 40 queries: the register-resident mean-of-probabilities kernel
+    (_cfg("resident_prob", config_id=98, num_text=40, grid_h=19, grid_w=24, keep=60),
+     "mean_prob"),
 ]
 
 

@@ -30,6 +30,9 @@ CASES = [
     (_cfg("mha_layer_path", batch=64), "mean_logit"),
     (_cfg("gqa_staged", config_id=111, num_heads=12, num_kv_heads=3), "mean_logit"),
     (_cfg("mha_prob", config_id=112), "mean_prob"),
+    # 24 x 24 tokens, 64 queries: the register-resident mean-of-probabilities kernel
+    (_cfg("resident_prob", config_id=113, num_text=64, grid_h=24, grid_w=24, keep=100),
+     "mean_prob"),
 ]
 
 

@@ -42,6 +42,9 @@ CASES = [
          num_text=9, keep=12),
     _cfg("gqa4_f32", config_id=93, dtype="f32", num_layers=2, num_heads=8, num_kv_heads=2,
          num_text=5, keep=9),
+    # 462 tokens, 40 queries: the register-resident mean-of-probabilities kernel
+    _cfg("resident_gqa2_d128", config_id=95, num_heads=6, num_kv_heads=3, head_dim=128,
+         num_text=40, grid_h=21, grid_w=22, keep=50, salient_count=8, clusters=2),
     # 25600 tokens: logits in the output rows, selection in segments
     _cfg("large_mha", config_id=94, batch=1, num_layers=1, num_heads=2, num_kv_heads=2,
          num_text=3, grid_h=160, grid_w=160, keep=3000, salient_count=30, clusters=3),

@@ -842,9 +842,10 @@ hipError_t dispatch_mp(const Dims& d, float scale, const void* q, const void* k,
         return launch_mp<T, D, 1>(d, scale, q, k, e, r, qcap, st);
     } else {
         // measured: 4 tiles per group pays when a chunk has 8 query blocks; one tile
-        // per group (114 VGPRs: 4 workgroups per CU) when the LDS also leaves room
-        // for 4 (the LLaVA shape: 34 KiB, stage 413 -> 397 us), else 2 (Qwen2-VL:
-        // 50 KiB, 3 per CU, where one tile measured 284 -> 293 us)
+        // per group (under 128 VGPRs: 4 workgroups per CU) when the LDS also leaves
+        // room for 4 (the LLaVA shape, 34 KiB, before the register-resident kernel
+        // took it: stage 413 -> 397 us), else 2 (Qwen2-VL: 50 KiB, 3 per CU, where one
+        // tile measured 284 -> 293 us)
         if (qcap >= 128) return launch_mp<T, D, 4>(d, scale, q, k, e, r, qcap, st);
         bool global = false, over = false;
         if (4 * mp_lds<T, D>(d, qcap, global, over) <= kLdsPerCu)

@@ -634,26 +634,38 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
         load_keys<NA>(a, kg + static_cast<int64_t>(min(key_of(jj) + lr, N - 1)) * kld + koff);
     };
 
-    // the wave's first key tiles, and keys 0..15 for the references, are requested
-    // before the queries are staged
+    // the queries are requested first, then keys 0..15 for the references and the
+    // wave's first key tiles, so that staging the queries waits for them alone
+    constexpr int EPV = 16 / sizeof(T);                          // elements per 16 bytes
+    constexpr int QPT = (QR * (D / EPV) + kThreads - 1) / kThreads;   // packets per thread
+    f32x4v qv[QPT];
+#pragma unroll
+    for (int i = 0; i < QPT; ++i) {
+        const int idx = min(tid + i * kThreads, QR * (D / EPV) - 1);
+        const int r = idx / (D / EPV), c = idx % (D / EPV);
+        qv[i] = *reinterpret_cast<const f32x4v*>(qh + static_cast<int64_t>(min(r, NT - 1)) * qld +
+                                                 c * EPV);
+    }
+    __builtin_amdgcn_sched_barrier(0);                           // (the request order)
+    AFrag a0[NA];
+    load_keys<NA>(a0, kg + static_cast<int64_t>(min(lr, N - 1)) * kld + koff);
     AFrag a[KB][NA];
 #pragma unroll
     for (int j = 0; j < KB - 1; ++j) load_tile(a[j], j);
-    AFrag a0[NA];
-    load_keys<NA>(a0, kg + static_cast<int64_t>(min(lr, N - 1)) * kld + koff);
+    __builtin_amdgcn_sched_barrier(0);
 
     // ---- stage the queries (rows past N_T are zero) and their references ----
-    {
-        constexpr int EPV = 16 / sizeof(T);
-        for (int idx = tid; idx < QB * 16 * (D / EPV); idx += kThreads) {
+#pragma unroll
+    for (int i = 0; i < QPT; ++i) {
+        const int idx = tid + i * kThreads;
+        if (idx < QR * (D / EPV)) {
             const int r = idx / (D / EPV), c = idx % (D / EPV);
-            f32x4v v = {0.f, 0.f, 0.f, 0.f};
-            if (r < NT) v = *reinterpret_cast<const f32x4v*>(qh + static_cast<int64_t>(r) * qld + c * EPV);
-            *reinterpret_cast<f32x4v*>(qs + r * QS + c * EPV) = v;
+            const f32x4v zero = {0.f, 0.f, 0.f, 0.f};
+            *reinterpret_cast<f32x4v*>(qs + r * QS + c * EPV) = r < NT ? qv[i] : zero;
         }
-        if (tid == 0) s_amax = 0u;
-        __syncthreads();
     }
+    if (tid == 0) s_amax = 0u;
+    __syncthreads();
     // every wave takes all the references itself (a few products; no barrier)
     float cz[QBN];
 #pragma unroll

@@ -272,15 +272,33 @@ __device__ __forceinline__ void mean_prob_two_pass(const T* __restrict__ q,
         const int rows = min(qcap, NT - t0);
         const int QB = (rows + 15) / 16;
         __syncthreads();
-        // ---- stage this chunk of queries (rows past NT are zero) ----
+        // ---- stage this chunk of queries (rows past NT are zero): the thread's
+        // packets are requested in two batches, each before its first store (two
+        // round trips instead of one per packet, half the registers of one batch);
+        // the requests are unconditional (indices past the chunk repeat its last
+        // packet), so no branch makes a store wait for more than its batch
         constexpr int EPV = 16 / sizeof(T);                       // elements per 16 bytes
-        for (int idx = tid; idx < QB * 16 * (D / EPV); idx += kThreads) {
-            const int row = idx / (D / EPV), c = idx % (D / EPV);
-            f32x4v v = {0.f, 0.f, 0.f, 0.f};
-            if (row < rows)
-                v = *reinterpret_cast<const f32x4v*>(qh + static_cast<int64_t>(t0 + row) * qld +
-                                                     c * EPV);
-            *reinterpret_cast<f32x4v*>(qs + row * QS + c * EPV) = v;
+        constexpr int QPT = (C::QC * (D / EPV) + kThreads - 1) / kThreads;
+        constexpr int QPB = (QPT + 1) / 2;                        // packets per batch
+        const int packets = QB * 16 * (D / EPV);
+#pragma unroll 1
+        for (int i0 = 0; i0 < QPT; i0 += QPB) {
+            f32x4v qv[QPB];
+#pragma unroll
+            for (int i = 0; i < QPB; ++i) {
+                const int idx = min(tid + (i0 + i) * kThreads, packets - 1);
+                const int row = idx / (D / EPV), c = idx % (D / EPV);
+                qv[i] = *reinterpret_cast<const f32x4v*>(
+                    qh + static_cast<int64_t>(t0 + min(row, rows - 1)) * qld + c * EPV);
+            }
+#pragma unroll
+            for (int i = 0; i < QPB; ++i) {
+                const int idx = tid + (i0 + i) * kThreads;
+                const int row = idx / (D / EPV), c = idx % (D / EPV);
+                const f32x4v zero = {0.f, 0.f, 0.f, 0.f};
+                if (idx < packets)
+                    *reinterpret_cast<f32x4v*>(qs + row * QS + c * EPV) = row < rows ? qv[i] : zero;
+            }
         }
         for (int qb = 0; qb < QB; ++qb) lE[qb * kThreads] = 0.f;
         if (tid == 0) {

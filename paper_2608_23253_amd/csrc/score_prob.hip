@@ -84,6 +84,8 @@ constexpr size_t kLdsPerCu = 160 * 1024;
 // body computes such a head's column sums with the same arithmetic, so a head's
 // bits do not depend on which kernel a batch runs.
 constexpr int kResTiles = 9, kResMinTiles = 7, kResMaxQueryBlocks = 4;
+// (the per-query statistics of such a head fit one wave: lane t holds query t)
+static_assert(16 * kResMaxQueryBlocks <= kWave, "a head's queries in one wave");
 __host__ __device__ constexpr int tiles_per_wave(int64_t N) {
     return static_cast<int>(((N + 15) / 16 + kWaves - 1) / kWaves);
 }
@@ -619,6 +621,7 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
     using C = ProbCfg<T, D>;
     constexpr int QS = C::QS, NA = C::NA, QR = 16 * QBN;
     constexpr int KB = 3;                                        // key tiles in registers
+    static_assert(QBN >= 1 && QR <= kWave && MAXT >= KB, "resident kernel shape");
     using AFrag = typename C::AFrag;
 
     extern __shared__ __align__(16) unsigned char smem[];

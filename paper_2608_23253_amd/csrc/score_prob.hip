@@ -708,21 +708,29 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
         if (j + KB - 1 < MAXT) load_tile(a[(j + KB - 1) % KB], j + KB - 1);
         const int key0 = key_of(j) + 4 * lg;
         const bool own = j < ntw;
+        // MASKED: some key of the tile is past N or the tile is past the wave's last
+        // (the same values either way: masking only zeroes such keys)
+        auto tile = [&](auto masked) {
 #pragma unroll
-        for (int qb = 0; qb < QB; ++qb) {
-            AFrag bq[NA];
-            load_queries<D>(bq, qs, qb * 16, lr, lg);
-            const f32x4v z = tile_mma<NA>(a[j % KB], bq);
+            for (int qb = 0; qb < QB; ++qb) {
+                AFrag bq[NA];
+                load_queries<D>(bq, qs, qb * 16, lr, lg);
+                const f32x4v z = tile_mma<NA>(a[j % KB], bq);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                float y = z[r] - cz[qb];
-                y = (own && key0 + r < N) ? y : 0.f;
-                amax = fmaxf(amax, fabsf(y));
-                const float xv = p4(y) * y;
-                x[j][qb][r] = xv;
-                E[qb] += xv;
+                for (int r = 0; r < 4; ++r) {
+                    float y = z[r] - cz[qb];
+                    if constexpr (decltype(masked)::value) y = (own && key0 + r < N) ? y : 0.f;
+                    amax = fmaxf(amax, fabsf(y));
+                    const float xv = p4(y) * y;
+                    x[j][qb][r] = xv;
+                    E[qb] += xv;
+                }
             }
-        }
+        };
+        if (__builtin_amdgcn_readfirstlane(own && key_of(j) + 16 <= N))
+            tile(std::false_type{});
+        else
+            tile(std::true_type{});
         // keep the tiles in program order: the compiler would otherwise sink each
         // tile's loads down to its first use, which leaves none in flight
         __builtin_amdgcn_sched_barrier(0);

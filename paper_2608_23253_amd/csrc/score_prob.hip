@@ -697,6 +697,13 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
     }
 
     // ---- pass 1: x = expm1(s y) / s = y P(y), y = z - c_t, kept per logit ------
+    // the first QKEEP query blocks' operands stay in registers for every tile (the
+    // others are read from LDS per tile); not with two blocks, where the registers
+    // would cost a wave per SIMD
+    constexpr int QKEEP = QBN == 2 ? 0 : (QBN < 2 ? QBN : 2);
+    AFrag bkeep[QKEEP > 0 ? QKEEP : 1][NA];
+#pragma unroll
+    for (int qb = 0; qb < QKEEP; ++qb) load_queries<D>(bkeep[qb], qs, qb * 16, lr, lg);
     const ScaledSeries<4> p4(scale);
     float x[MAXT][QBN][4];
     float E[QBN];
@@ -714,7 +721,12 @@ __global__ __launch_bounds__(kThreads, 2) void score_mean_prob_resident_kernel(
 #pragma unroll
             for (int qb = 0; qb < QB; ++qb) {
                 AFrag bq[NA];
-                load_queries<D>(bq, qs, qb * 16, lr, lg);
+                if (qb < QKEEP) {
+#pragma unroll
+                    for (int t = 0; t < NA; ++t) bq[t] = bkeep[qb < QKEEP ? qb : 0][t];
+                } else {
+                    load_queries<D>(bq, qs, qb * 16, lr, lg);
+                }
                 const f32x4v z = tile_mma<NA>(a[j % KB], bq);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {

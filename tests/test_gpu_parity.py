@@ -85,6 +85,16 @@ CASES = [
     _small("resident_q20_d64", config_id=71, num_text=20, grid_h=24, grid_w=24, keep=100,
            salient_count=12, clusters=3),
     _small("resident_q5", config_id=72, num_text=5, grid_h=20, grid_w=25, keep=50),
+    # the resident kernel's boundaries: 385 tokens (7 tiles for the first wave, 6 for
+    # the others) with 16 and 17 queries (one and two query blocks), a single query
+    # over 576 tokens; 384 tokens and 65 queries take the two-pass kernel
+    _small("resident_n385_q16", config_id=74, num_text=16, grid_h=5, grid_w=77, keep=40),
+    _small("resident_n385_q17", config_id=75, head_dim=128, num_text=17, grid_h=11,
+           grid_w=35, keep=40),
+    _small("resident_q1_n576", config_id=76, num_text=1, grid_h=24, grid_w=24, keep=64),
+    _small("two_pass_n384", config_id=77, num_text=64, grid_h=16, grid_w=24, keep=40),
+    _small("two_pass_q65", config_id=78, head_dim=128, num_text=65, grid_h=24, grid_w=24,
+           keep=64),
     synth.heavy_tailed(_small("resident_heavy_q48", config_id=73, head_dim=128, num_text=48,
                               grid_h=22, grid_w=22, keep=40, salient_count=12, clusters=2),
                        name="resident_heavy_q48"),

@@ -25,7 +25,8 @@ torch = pytest.importorskip("torch")
 E = pytest.importorskip("paper_2608_23253_amd")
 from paper_2608_23253_amd import _lib as L  # noqa: E402
 
-CALLS = [("llava", 64, "mean_logit"), ("hires", 1, "mean_logit"), ("qwen2vl_gqa", 2, "mean_prob")]
+CALLS = [("llava", 64, "mean_logit"), ("hires", 1, "mean_logit"), ("qwen2vl_gqa", 2, "mean_prob"),
+         ("llava", 2, "mean_prob")]
 
 
 def _noalloc_raw(qd, kd, cfg, mode):
